@@ -1,0 +1,289 @@
+"""Pins of the CPU oracle against things other than itself: brute force over
+every persistent schedule with an independent simulator, the homogeneous
+closed forms, the no-recomputation closed form, the feasibility threshold
+recurrence, monotonicity and replay of reconstructed sequences."""
+import numpy as np
+import pytest
+
+import model
+from oracle import oracle as orc
+from paper_1911_13214_amd import chaingen
+
+INF = orc.INF
+
+
+def table_rows(C, L):
+    return {(s, t): C[orc.row(L, s, t)] for s in range(1, L + 1) for t in range(s, L + 1)}
+
+
+def test_schedule_family_size():
+    # The persistent schedules of n stages are counted by the large Schroeder
+    # numbers (each sub-chain splits at s' or peels off F_all^s).
+    assert [model.schedule_count(n) for n in range(1, 8)] == [1, 2, 6, 22, 90, 394, 1806]
+    assert sum(1 for _ in model.persistent_schedules(1, 6)) == 394
+
+
+def test_paper_example_sequence_is_valid_and_persistent():
+    # Section 3.1 prints a valid sequence for L = 4 (plus the loss stage 5):
+    # F_ck^1 F_none^2 F_ck^3 F_all^4 F_all^5 B^5 B^4 F_all^3 B^3 F_all^1 F_all^2 B^2 B^1
+    seq = [(model.F_CK, 1), (model.F_NONE, 2), (model.F_CK, 3), (model.F_ALL, 4), (model.F_ALL, 5),
+           (model.B, 5), (model.B, 4), (model.F_ALL, 3), (model.B, 3), (model.F_ALL, 1), (model.F_ALL, 2),
+           (model.B, 2), (model.B, 1)]
+    params = chaingen.random_chains(1, 5, seed=11)
+    ch = model.Chain(params)
+    time, peak = model.simulate(ch, 1, 5, seq)
+    assert time == sum(ch.uf(l) for l in (1, 2, 3, 4, 5, 3, 1, 2)) + sum(ch.ub(l) for l in range(1, 6))
+    assert any(ops == seq for _, ops in model.persistent_schedules(1, 5))
+    # an operation whose input is gone makes the sequence invalid
+    with pytest.raises(model.InvalidSequence):
+        model.simulate(ch, 1, 5, [(model.F_NONE, 1), (model.F_ALL, 3)] + seq[3:])
+
+
+def _check_against_brute_force(params, M):
+    L = params.shape[-1]
+    C, D = orc.solve(params, M)
+    bf = model.brute_force(params, M)
+    for (s, t), (cost, dec) in bf.items():
+        r = orc.row(L, s, t)
+        np.testing.assert_array_equal(C[r], cost, err_msg=f"cost of ({s},{t})")
+        np.testing.assert_array_equal(D[r], dec, err_msg=f"decision of ({s},{t})")
+
+
+@pytest.mark.parametrize("seed", range(8))
+@pytest.mark.parametrize("L", [1, 2, 3, 4, 5, 6])
+def test_brute_force_random(seed, L):
+    params = chaingen.random_chains(1, L, seed=100 * L + seed)
+    M = 20 * L + 40
+    _check_against_brute_force(params, M)
+
+
+def wide_chain(seed, L=5, size_hi=12, over_hi=9):
+    """Random chain with omega_abar >= omega_a and wider overheads, so that
+    every term of both gates can be the binding one."""
+    rng = np.random.default_rng(seed)
+    p = np.zeros((1, 6, L), dtype=np.int64)
+    p[0, 0] = rng.integers(0, 30, L)
+    p[0, 1] = rng.integers(0, 60, L)
+    p[0, 2] = rng.integers(0, size_hi, L)
+    p[0, 3] = p[0, 2] + rng.integers(0, 2 * size_hi, L)
+    p[0, 4] = rng.integers(0, over_hi, L)
+    p[0, 5] = rng.integers(0, over_hi, L)
+    return p
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_brute_force_random_with_overheads_and_big_sizes(seed):
+    _check_against_brute_force(wide_chain(seed), 120)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_brute_force_overhead_heavy(seed):
+    # small activations, large overheads: the first-step term of m_none and
+    # the backward term of m_all become binding
+    _check_against_brute_force(wide_chain(1000 + seed, L=6, size_hi=3, over_hi=26), 80)
+
+
+def tiny_chain(seed):
+    """2 to 5 stages, times in 0..5 (many ties, cheap recomputation), sizes
+    and overheads of random spread with omega_abar >= omega_a."""
+    rng = np.random.default_rng(seed)
+    L = int(rng.integers(2, 6))
+    p = np.zeros((1, 6, L), dtype=np.int64)
+    p[0, 0] = rng.integers(0, 6, L)
+    p[0, 1] = rng.integers(0, 6, L)
+    hi = int(rng.integers(1, 8))
+    p[0, 2] = rng.integers(0, hi, L)
+    p[0, 3] = p[0, 2] + rng.integers(0, hi, L)
+    ohi = int(rng.integers(1, 30))
+    p[0, 4] = rng.integers(0, ohi, L)
+    p[0, 5] = rng.integers(0, ohi, L)
+    return p
+
+
+TINY_M = 60
+
+
+@pytest.mark.parametrize("block", range(5))
+def test_brute_force_tiny_chains(block):
+    for seed in range(60 * block, 60 * (block + 1)):
+        _check_against_brute_force(tiny_chain(seed), TINY_M)
+
+
+def test_brute_force_homogeneous_prefix():
+    params = chaingen.homogeneous_chain(7)
+    _check_against_brute_force(params, 100)
+
+
+def test_homogeneous_closed_forms():
+    # u_f=10, u_b=20, omega_a=5, omega_abar=15, no overheads; n = t-s+1.
+    # n = 1: infeasible below 20, then u_f+u_b = 30.
+    # n >= 2: infeasible below 25; on [25, 29] only s' = t fits, giving
+    # C(n) = C(n-1) + 10(n-1) + 30 = 5n^2 + 25n; from 15n + 5 (the peak of
+    # the no-recomputation schedule) the cost is 30n.
+    params, L, M, _, _ = chaingen.config(1)
+    C, D = orc.solve(params, M)
+    for s in range(1, L + 1):
+        for t in range(s, L + 1):
+            n = t - s + 1
+            row, drow = C[orc.row(L, s, t)], D[orc.row(L, s, t)]
+            if n == 1:
+                assert (row[:20] == INF).all() and (row[20:] == 30).all()
+                continue
+            assert (row[:25] == INF).all() and (drow[:25] == -1).all()
+            assert (row[25:30] == 5 * n * n + 25 * n).all()
+            assert (drow[25:30] == t).all()
+            if 15 * n + 5 <= M:
+                assert (row[15 * n + 5:] == 30 * n).all()
+                assert (row[:15 * n + 5] > 30 * n).all()
+            if n == 2:
+                assert (row[25:35] == 70).all() and (row[35:] == 60).all()
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_no_recomputation_closed_form(cfg):
+    # With every u_f >= 1 the cost is sum(u_f + u_b) exactly when the budget
+    # admits the schedule without recomputation.
+    params, L, M, _, _ = chaingen.config(cfg)
+    ch = model.Chain(params)
+    C, _ = orc.solve(params, M)
+    checked = 0
+    for s in range(1, L + 1):
+        for t in range(s, min(L, s + 12) + 1):
+            total = sum(ch.uf(l) + ch.ub(l) for l in range(s, t + 1))
+            mstar = model.all_fall_peak(ch, s, t)
+            row = C[orc.row(L, s, t)]
+            ms = np.arange(M + 1)
+            np.testing.assert_array_equal(row == total, ms >= mstar)
+            assert (row >= total).all()
+            checked += mstar <= M
+    assert checked > 0
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_feasibility_threshold(cfg):
+    params, L, M, _, _ = chaingen.config(cfg)
+    th = model.feasibility_threshold(params)
+    C, D = orc.solve(params, M)
+    for (s, t), m0 in th.items():
+        row = C[orc.row(L, s, t)]
+        finite = row != INF
+        np.testing.assert_array_equal(finite, np.arange(M + 1) >= m0, err_msg=f"({s},{t})")
+        np.testing.assert_array_equal(D[orc.row(L, s, t)] >= 0, finite)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_monotone_in_budget(cfg):
+    params, L, M, _, _ = chaingen.config(cfg)
+    C, _ = orc.solve(params, M)
+    assert (np.diff(C.astype(np.float64), axis=1) <= 0).all()
+
+
+def _walk_decisions(params, M, C, D, m):
+    """Sequence from the decision table alone."""
+    ch = model.Chain(params)
+    L = ch.L
+    out = []
+
+    def rec(s, t, m):
+        d = int(D[orc.row(L, s, t), m])
+        assert d >= 0
+        if s == t:
+            out.extend([(model.F_ALL, s), (model.B, s)])
+        elif d > 0:
+            out.append((model.F_CK, s))
+            out.extend((model.F_NONE, k) for k in range(s + 1, d))
+            rec(d, t, m - ch.wa(d - 1))
+            rec(s, d - 1, m)
+        else:
+            out.append((model.F_ALL, s))
+            rec(s + 1, t, m - ch.wab(s))
+            out.append((model.B, s))
+
+    rec(1, L, m)
+    return out
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_replay_reconstructed_sequences(cfg):
+    params, L, M, _, _ = chaingen.config(cfg)
+    ch = model.Chain(params)
+    C, D = orc.solve(params, M)
+    top = C[orc.row(L, 1, L)]
+    step = max(1, (M + 1) // 60)
+    for m in list(range(0, M + 1, step)) + [M]:
+        seq = orc.reconstruct(params, M, C, m)
+        if top[m] == INF:
+            assert seq is None
+            continue
+        time, peak = model.simulate(ch, 1, L, seq)
+        assert time == top[m]
+        assert peak <= m
+        assert len(seq) <= L * (L + 1) // 2 + L
+        assert seq == _walk_decisions(params, M, C, D, m)
+
+
+def test_cell_definition_matches_table():
+    params, L, M, _, _ = chaingen.config(2)
+    C, D = orc.solve(params, M)
+    rng = np.random.default_rng(7)
+    for _ in range(3000):
+        s = int(rng.integers(1, L + 1))
+        t = int(rng.integers(s, L + 1))
+        m = int(rng.integers(0, M + 1))
+        v, d = orc.cell(params, M, C, s, t, m)
+        assert v == C[orc.row(L, s, t), m] and d == D[orc.row(L, s, t), m]
+
+
+def test_subchain_locality():
+    # C(s,t,.) depends on stages s..t only: solving a window of the chain
+    # reproduces the matching rows of the full table.
+    params, L, M, _, _ = chaingen.config(2)
+    C, D = orc.solve(params, M)
+    for a, b in [(1, 17), (9, 30), (34, 50)]:
+        sub = np.ascontiguousarray(params[:, :, a - 1:b])
+        Cs, Ds = orc.solve(sub, M)
+        Ls = b - a + 1
+        for s in range(1, Ls + 1):
+            for t in range(s, Ls + 1):
+                np.testing.assert_array_equal(Cs[orc.row(Ls, s, t)], C[orc.row(L, s + a - 1, t + a - 1)])
+                # decisions are stage numbers: shift them back
+                ds = Ds[orc.row(Ls, s, t)].astype(np.int64)
+                ds = np.where(ds > 0, ds + a - 1, ds)
+                np.testing.assert_array_equal(ds, D[orc.row(L, s + a - 1, t + a - 1)])
+
+
+def test_edge_cases():
+    # single stage
+    p = chaingen.random_chains(1, 1, seed=3)
+    C, D = orc.solve(p, 50)
+    ch = model.Chain(p)
+    g = max(ch.wd(1) + ch.wab(1) + ch.of(1), ch.wd(1) + ch.wab(1) + ch.ob(1))
+    assert (C[0, :g] == INF).all() and (C[0, g:] == ch.uf(1) + ch.ub(1)).all()
+    # zero budget range: M = 0
+    C, D = orc.solve(chaingen.random_chains(1, 6, seed=4), 0)
+    assert C.shape == (21, 1) and (C == INF).all() and (D == -1).all()
+    # all sizes zero: everything fits at m = 0 without recomputation
+    p = chaingen.random_chains(1, 7, seed=5)
+    p[:, 2:] = 0
+    C, D = orc.solve(p, 3)
+    assert (C[orc.row(7, 1, 7)] == p[0, 0].sum() + p[0, 1].sum()).all()
+    # sizes beyond the budget: infeasible everywhere
+    p = chaingen.random_chains(1, 5, seed=6)
+    p[:, 2] += 1000
+    p[:, 3] += 1000
+    C, D = orc.solve(p, 100)
+    assert (C == INF).all() and (D == -1).all()
+
+
+def test_domain_checks():
+    p = chaingen.random_chains(1, 4, seed=1)
+    assert orc.check(p, 100)
+    for row, val in [(0, -1), (2, -1), (3, 1 << 30), (5, -3)]:
+        q = p.copy()
+        q[0, row, 1] = val
+        assert not orc.check(q, 100)
+    assert not orc.check(p, -1)
+    assert not orc.check(p, 1 << 30)
+    q = p.copy()
+    q[0, 0, :] = 1 << 57  # L * sum(u_f) beyond 2^60
+    assert not orc.check(q, 100)
