@@ -1,0 +1,166 @@
+"""Benchmark: one step = one rotor_solve, the whole table fill of the
+checkpointing dynamic program (every sub-chain, every budget) for one
+synthetic workload, inputs already resident in device memory.
+
+Prints ONE JSON line on stdout.  Everything else goes to stderr.
+
+  python bench.py [--steps K] [--warmup W] [--workload 1..5] [--no-cpu-baseline]
+
+Only one GPU is supported: --gpus N with N > 1 exits with a message.
+"""
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "DP candidate relaxations/sec (G/s) and solve ms at L=500,M=5000; % of BW roofline"
+HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_diag_kernel.json")
+FILL_SOURCE = os.path.join(ROOT, "paper_1911_13214_amd", "csrc", "rotor_fill.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def work_counts(n_chains, L, M):
+    """Candidate relaxations and algorithmic bytes of one full solve.
+
+    R_ck  = sum over pairs s < t of (t - s) C_1 candidates per budget,
+    R_all = one C_2 candidate per budget of every pair s < t,
+    cells = every (s, t, m).  Each C_1 candidate reads two int64 cells, each
+    C_2 candidate one, each cell writes 8 + 2 bytes."""
+    W = M + 1
+    r_ck = (L ** 3 - L) // 6 * W * n_chains
+    r_all = L * (L - 1) // 2 * W * n_chains
+    cells = L * (L + 1) // 2 * W * n_chains
+    alg_bytes = 16 * r_ck + 8 * r_all + 10 * cells
+    # the diagonal kernels (d >= 1) carry all but the single-stage cells
+    diag_bytes = alg_bytes - 10 * L * W * n_chains
+    return r_ck, r_all, cells, alg_bytes, diag_bytes
+
+
+def cpu_baseline(params, M, stages):
+    """The C oracle, single-threaded, on the sub-chain [1, stages] of the
+    workload with every budget."""
+    from oracle import oracle
+
+    sub = params[:, :, :stages].copy()
+    r_ck, r_all, _, _, _ = work_counts(1, stages, M)
+    t0 = time.perf_counter()
+    oracle.solve(sub, M)
+    dt = time.perf_counter() - t0
+    return {
+        "value": round((r_ck + r_all) / dt / 1e9, 4),
+        "unit": "G relaxations/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"sub-chain [1,{stages}] of the workload chain, all {M + 1} budgets "
+                  f"({r_ck + r_all:.3e} candidates, {dt:.1f} s, single thread, {platform.processor() or 'cpu'})",
+    }
+
+
+def traffic_if_current():
+    """Measured HBM bytes per diagonal launch from the committed counter
+    summary, if it was taken on the current kernel source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    rec = json.load(open(TRAFFIC_FILE))
+    sha = hashlib.sha256(open(FILL_SOURCE, "rb").read()).hexdigest()
+    if rec.get("fill_source_sha256") != sha:
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-stages", type=int, default=160)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: the solver has no multi-GPU path (see the sharding note "
+              "in the design document)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_1911_13214_amd import chaingen, rotor
+
+    params, L, M, n_chains, name = chaingen.config(args.workload)
+    r_ck, r_all, cells, alg_bytes, diag_bytes = work_counts(n_chains, L, M)
+    R = r_ck + r_all
+    dev = torch.device("cuda:0")
+    d_params = rotor.upload_params(params, M, dev)
+    cost, dec = rotor.alloc_tables(n_chains, L, M, dev)
+    stream = torch.cuda.current_stream(dev)
+    log(f"workload {name}: L={L} M={M} chains={n_chains} candidates={R:.4e} alg bytes={alg_bytes:.4e}")
+
+    for _ in range(args.warmup):
+        rotor.rotor_solve(d_params, n_chains, L, M, cost, dec, stream)
+    torch.cuda.synchronize()
+
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        starts[k].record(stream)
+        rotor.rotor_solve(d_params, n_chains, L, M, cost, dec, stream)
+        ends[k].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ev_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    ms = float(np.mean(ev_ms))
+    log(f"per-step ms (events): {[round(x, 3) for x in ev_ms]}; wall {wall * 1e3 / args.steps:.3f} ms/step")
+
+    # parity spot check of the timed output against the stored oracle values
+    check = None
+    golden = os.path.join(ROOT, "tests", "golden", "random_L500_M5000.npz")
+    if args.workload == 5 and os.path.exists(golden):
+        g = np.load(golden)
+        top = rotor.rotor_row_index(L, 1, L)
+        ok = np.array_equal(cost[0, top, :M + 1].cpu().numpy(), g["top_cost"]) and \
+            np.array_equal(dec[0, top, :M + 1].cpu().numpy(), g["top_dec"])
+        check = "top row equals oracle" if ok else "TOP ROW DIFFERS FROM ORACLE"
+        log(check)
+
+    launches = L - 1
+    achieved = diag_bytes / launches / (ms * 1e-3 / launches) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(R / (ms * 1e-3) / 1e9, 3),
+        "unit": "G relaxations/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "strong",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {"workload": name, "L": L, "M": M, "n_chains": n_chains, "candidates_per_step": R,
+                   "alg_bytes_per_step": alg_bytes},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic_if_current(),
+                     "kernel": "diag_kernel", "launches_per_step": launches},
+        "check": check,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(params, M, min(args.cpu_stages, L)) if n_chains == 1 else None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,182 @@
+/*
+ * rotor.h -- C ABI of the MI355X (gfx950) solver for optimal persistent
+ * activation checkpointing on heterogeneous chains.
+ *
+ * The method is the dynamic program of Beaumont, Eyraud-Dubois, Hermann,
+ * Joly and Shilova, "Optimal checkpointing for heterogeneous chains"
+ * (arXiv 1911.13214): Theorem 1 (Section 4.2) defines the optimal time
+ * C_BP(s, t, m) of the sub-chain [s, t] under a memory budget m, Algorithm 1
+ * fills the table and Algorithm 2 rebuilds the operation sequence.
+ *
+ * Units.  Times and sizes are integers: the caller has already expressed
+ * memory as a number of slots (Section 5.2 discretises sizes into S slots,
+ * rounded up).  Costs are int64; an infeasible cell holds ROTOR_INF.
+ *
+ * Chain parameters.  A chain of L stages (stages are numbered 1..L as in
+ * Section 3.1; the loss, if modelled, is simply the last stage) is described
+ * by six rows of L int64 values -- the model inputs of Section 5.1 and
+ * Table 1:
+ *   ROTOR_ROW_UF    u_f^l   time of any forward operation of stage l
+ *   ROTOR_ROW_UB    u_b^l   time of the backward operation B^l
+ *   ROTOR_ROW_WA    w_a^l   size of the stage output a^l; also the size of
+ *                           the gradient delta^l (the paper takes them equal)
+ *   ROTOR_ROW_WABAR w_abar^l size of abar^l, all data F_all^l keeps for B^l
+ *   ROTOR_ROW_OF    o_f^l   memory overhead of the forward operations
+ *   ROTOR_ROW_OB    o_b^l   memory overhead of B^l
+ * Stage l sits at column l-1.  A batch of n_chains chains of equal L is
+ * packed chain-major: params[c][row][l-1], c = 0..n_chains-1.
+ *
+ * Domain.  Every value is >= 0; sizes and overheads are < 2^30; M < 2^30;
+ * for every chain L * sum(u_f) + sum(u_b) < 2^60 (this bounds every finite
+ * cost: a persistent schedule runs each forward at most L times).
+ * rotor_check_params verifies this on a host copy.  Kernels never access
+ * memory out of bounds whatever the parameter values; outside the domain the
+ * table contents are unspecified.
+ *
+ * Budgets.  Column m = 0..M of the tables is the budget of the definition of
+ * C_BP: the input a^{s-1} of the sub-chain is not counted, the gradient
+ * delta^t is.  To count the chain input a^0 as Algorithm 1 does, query the
+ * row (1, L) at M - size(a^0).
+ *
+ * Table layout (device memory, caller-owned).  Per chain, the L(L+1)/2 pairs
+ * (s, t), 1 <= s <= t <= L, are stored by increasing d = t - s and then s:
+ *   row(s, t) = d*L - d*(d-1)/2 + (s-1)
+ * Each row holds `pitch` elements, pitch = M+1 rounded up to a multiple of
+ * 16 (128 bytes of costs); only columns 0..M are written.  The cost table is
+ * int64 and the decision table int16, with the same indexing:
+ *   element(c, s, t, m) = (c * rows + row(s, t)) * pitch + m,
+ *   rows = L(L+1)/2.
+ * Decision values: -1 infeasible; 0 the sequence starts with F_all^s (the C_2
+ * option of Theorem 1, or the single-stage rule of Eq. (DP:Init)); s' in
+ * [s+1, t] it starts with F_ck^s and stores a^{s'-1} next (option C_1 with
+ * split s').  Among equal costs the smallest s' is chosen, and C_1 is
+ * preferred to C_2, so the table is unique.
+ *
+ * Streams.  `stream` is a hipStream_t passed as void* (NULL: the default
+ * stream).  Entry points that take device buffers only enqueue work and
+ * return; argument errors are reported synchronously by the return value,
+ * device-side failures surface at the caller's next synchronisation.  The
+ * library keeps no state between calls and allocates no device memory;
+ * concurrent calls on distinct output buffers are independent.
+ */
+#ifndef ROTOR_H
+#define ROTOR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#ifndef ROTOR_API
+#define ROTOR_API __attribute__((visibility("default")))
+#endif
+
+#define ROTOR_VERSION 1
+#define ROTOR_INF INT64_MAX
+
+/* Status codes. */
+#define ROTOR_OK 0
+#define ROTOR_EINVAL (-1)       /* bad argument (null pointer, size out of range) */
+#define ROTOR_EDOMAIN (-2)      /* a parameter value is outside the domain above */
+#define ROTOR_EDEVICE (-3)      /* the HIP runtime refused a launch or query */
+#define ROTOR_INFEASIBLE (-4)   /* no sequence fits the budget: C(1, L, m) is infinite */
+#define ROTOR_ECAPACITY (-5)    /* the output array is too small; the count holds the size needed */
+#define ROTOR_ECORRUPT (-6)     /* the decision table is not one this library wrote */
+
+/* Rows of the packed parameter array. */
+#define ROTOR_ROW_UF 0
+#define ROTOR_ROW_UB 1
+#define ROTOR_ROW_WA 2
+#define ROTOR_ROW_WABAR 3
+#define ROTOR_ROW_OF 4
+#define ROTOR_ROW_OB 5
+#define ROTOR_N_ROWS 6
+
+/* Operations of Table 1. */
+#define ROTOR_F_CK 0   /* forward, keep the input a^{l-1} (checkpoint) */
+#define ROTOR_F_NONE 1 /* forward, keep nothing but the output a^l */
+#define ROTOR_F_ALL 2  /* forward, keep abar^l for the backward */
+#define ROTOR_B 3      /* backward B^l */
+
+typedef struct {
+    int32_t kind;  /* ROTOR_F_CK, ROTOR_F_NONE, ROTOR_F_ALL or ROTOR_B */
+    int32_t stage; /* 1..L */
+} rotor_op;
+
+/* Largest L accepted by rotor_solve (decisions are int16) and by
+ * rotor_reconstruct (its walk keeps one 8-byte frame per pending sub-chain in
+ * 64 KiB of LDS). */
+#define ROTOR_MAX_L 32767
+#define ROTOR_MAX_L_RECONSTRUCT 8191
+#define ROTOR_MAX_CHAINS 65535
+
+/* Library version (ROTOR_VERSION). */
+ROTOR_API int32_t rotor_version(void);
+
+/* Short English text for a status code. */
+ROTOR_API const char *rotor_status_string(int32_t status);
+
+/* Table geometry for n_chains chains of L stages and budgets 0..M (layout
+ * above).  Any output pointer may be NULL.  Host only; no device work.
+ * Returns ROTOR_OK, or ROTOR_EINVAL if n_chains, L or M is out of range or a
+ * byte count would overflow 64 bits. */
+ROTOR_API int32_t rotor_layout(int32_t n_chains, int32_t L, int64_t M, int64_t *pitch, int64_t *rows_per_chain,
+                     uint64_t *cost_bytes, uint64_t *dec_bytes);
+
+/* Row of the pair (s, t) within one chain (layout above), or -1 unless
+ * 1 <= s <= t <= L.  Host only. */
+ROTOR_API int64_t rotor_row_index(int32_t L, int32_t s, int32_t t);
+
+/* Check HOST parameters [n_chains][6][L] against the domain above.
+ * Returns ROTOR_OK, ROTOR_EINVAL (null pointer, sizes out of range) or
+ * ROTOR_EDOMAIN (a value out of range).  Host only. */
+ROTOR_API int32_t rotor_check_params(const int64_t *h_params, int32_t n_chains, int32_t L, int64_t M);
+
+/* Fill the cost table C_BP(s, t, m) and the decision table for every chain,
+ * every pair 1 <= s <= t <= L and every budget 0 <= m <= M: Theorem 1,
+ * Eq. (DP:Init) for t = s and Eq. (DP:mainrec) for t > s, evaluated by
+ * increasing t - s (every term of the recurrence is a strictly shorter
+ * sub-chain, which Algorithm 1's printed loop order does not respect).
+ *
+ *   d_params  DEVICE, read only: [n_chains][6][L] int64 (layout above).
+ *   d_cost    DEVICE, written: int64, rotor_layout's cost_bytes.
+ *   d_dec     DEVICE, written: int16, rotor_layout's dec_bytes.
+ *   stream    hipStream_t or NULL.
+ * Asynchronous.  Returns ROTOR_OK once every kernel is enqueued, ROTOR_EINVAL
+ * for a null or misaligned pointer or a size out of range, ROTOR_EDEVICE if
+ * a launch fails.  Allocates nothing. */
+ROTOR_API int32_t rotor_solve(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
+                    int16_t *d_dec, void *stream);
+
+/* Algorithm 2 (OptRec): the optimal persistent sequence of the whole chain
+ * [1, L] of chain `chain` for each of n_budgets budgets, walked on the device
+ * from the decision table that rotor_solve wrote.  The F_none steps of a C_1
+ * split stop at stage s'-1 (the stage whose output is stored next; the C_ck
+ * cost charges u_f^s .. u_f^{s'-1}).
+ *
+ *   d_params   DEVICE: the parameters given to rotor_solve.
+ *   d_dec      DEVICE: the decision table rotor_solve wrote (same n_chains,
+ *              L, M).
+ *   d_budgets  DEVICE, n_budgets int64 budgets m (0 <= m <= M).
+ *   d_ops      DEVICE, written: n_budgets x cap rotor_op; the sequence of
+ *              budget b starts at d_ops + b * cap.  A sequence has at most
+ *              L(L+1)/2 + L operations.
+ *   d_count    DEVICE, written: n_budgets int64, the sequence length (on
+ *              ROTOR_ECAPACITY: the length needed; only cap ops are written).
+ *   d_status   DEVICE, written: n_budgets int32, ROTOR_OK, ROTOR_INFEASIBLE
+ *              (C(1, L, m) is infinite; count 0), ROTOR_ECAPACITY,
+ *              ROTOR_EINVAL (budget out of range) or ROTOR_ECORRUPT.
+ * Asynchronous.  Returns ROTOR_OK once enqueued, ROTOR_EINVAL for bad
+ * arguments (including L > ROTOR_MAX_L_RECONSTRUCT), ROTOR_EDEVICE if the
+ * launch fails.  Allocates nothing. */
+ROTOR_API int32_t rotor_reconstruct(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, const int16_t *d_dec,
+                          int32_t chain, int32_t n_budgets, const int64_t *d_budgets, int64_t cap, rotor_op *d_ops,
+                          int64_t *d_count, int32_t *d_status, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ROTOR_H */

@@ -1,0 +1,143 @@
+// C ABI entry points of include/rotor.h: argument checks, table geometry and
+// the launches.  The arithmetic of the method lives in the kernels.
+#include <stdint.h>
+
+#include "rotor_internal.h"
+
+using namespace rotor;
+
+namespace {
+
+constexpr int64_t kMaxSize = (int64_t)1 << 30;
+constexpr uint64_t kCostBound = (uint64_t)1 << 60;
+
+bool sizes_ok(int32_t n_chains, int32_t L, int64_t M)
+{
+    return n_chains >= 1 && n_chains <= ROTOR_MAX_CHAINS && L >= 1 && L <= ROTOR_MAX_L && M >= 0 && M < kMaxSize;
+}
+
+// Number of elements of one table, or 0 on overflow.
+uint64_t table_elems(int32_t n_chains, int32_t L, int64_t M)
+{
+    const unsigned __int128 e = (unsigned __int128)n_chains * (uint64_t)((int64_t)L * (L + 1) / 2) *
+                                (uint64_t)pitch_of(M);
+    if (e * 8 >= ((unsigned __int128)1 << 63))
+        return 0;
+    return (uint64_t)e;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t rotor_version(void) { return ROTOR_VERSION; }
+
+const char *rotor_status_string(int32_t status)
+{
+    switch (status) {
+    case ROTOR_OK: return "ok";
+    case ROTOR_EINVAL: return "invalid argument";
+    case ROTOR_EDOMAIN: return "chain parameter outside the supported domain";
+    case ROTOR_EDEVICE: return "HIP runtime error";
+    case ROTOR_INFEASIBLE: return "no sequence fits the memory budget";
+    case ROTOR_ECAPACITY: return "output array too small";
+    case ROTOR_ECORRUPT: return "decision table inconsistent";
+    default: return "unknown status";
+    }
+}
+
+int32_t rotor_layout(int32_t n_chains, int32_t L, int64_t M, int64_t *pitch, int64_t *rows_per_chain,
+                     uint64_t *cost_bytes, uint64_t *dec_bytes)
+{
+    if (!sizes_ok(n_chains, L, M))
+        return ROTOR_EINVAL;
+    const uint64_t e = table_elems(n_chains, L, M);
+    if (e == 0)
+        return ROTOR_EINVAL;
+    if (pitch)
+        *pitch = pitch_of(M);
+    if (rows_per_chain)
+        *rows_per_chain = (int64_t)L * (L + 1) / 2;
+    if (cost_bytes)
+        *cost_bytes = e * sizeof(int64_t);
+    if (dec_bytes)
+        *dec_bytes = e * sizeof(int16_t);
+    return ROTOR_OK;
+}
+
+int64_t rotor_row_index(int32_t L, int32_t s, int32_t t)
+{
+    if (L < 1 || L > ROTOR_MAX_L || s < 1 || t < s || t > L)
+        return -1;
+    return row_of(L, t - s, s);
+}
+
+int32_t rotor_check_params(const int64_t *h_params, int32_t n_chains, int32_t L, int64_t M)
+{
+    if (!h_params || !sizes_ok(n_chains, L, M))
+        return ROTOR_EINVAL;
+    for (int32_t c = 0; c < n_chains; ++c) {
+        const int64_t *p = h_params + (int64_t)c * ROTOR_N_ROWS * L;
+        uint64_t suf = 0, sub = 0;
+        for (int32_t l = 0; l < L; ++l) {
+            const int64_t uf = p[ROTOR_ROW_UF * L + l], ub = p[ROTOR_ROW_UB * L + l];
+            if (uf < 0 || ub < 0 || (uint64_t)uf >= kCostBound || (uint64_t)ub >= kCostBound)
+                return ROTOR_EDOMAIN;
+            for (int row = ROTOR_ROW_WA; row <= ROTOR_ROW_OB; ++row) {
+                const int64_t v = p[row * L + l];
+                if (v < 0 || v >= kMaxSize)
+                    return ROTOR_EDOMAIN;
+            }
+            suf += (uint64_t)uf;
+            sub += (uint64_t)ub;
+            if (suf >= kCostBound || sub >= kCostBound)
+                return ROTOR_EDOMAIN;
+        }
+        // L * suf + sub < 2^60
+        if (suf > (kCostBound - sub) / (uint64_t)L)
+            return ROTOR_EDOMAIN;
+    }
+    return ROTOR_OK;
+}
+
+int32_t rotor_solve(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
+                    int16_t *d_dec, void *stream)
+{
+    if (!d_params || !d_cost || !d_dec || !sizes_ok(n_chains, L, M) || table_elems(n_chains, L, M) == 0)
+        return ROTOR_EINVAL;
+    if (((uintptr_t)d_params | (uintptr_t)d_cost) % 8 || (uintptr_t)d_dec % 2)
+        return ROTOR_EINVAL;
+    Tables tb;
+    tb.params = d_params;
+    tb.cost = d_cost;
+    tb.dec = d_dec;
+    tb.L = L;
+    tb.M = (int)M;
+    tb.n_chains = n_chains;
+    tb.pitch = pitch_of(M);
+    tb.rows = (int64_t)L * (L + 1) / 2;
+    return launch_fill(tb, (hipStream_t)stream) == hipSuccess ? ROTOR_OK : ROTOR_EDEVICE;
+}
+
+int32_t rotor_reconstruct(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, const int16_t *d_dec,
+                          int32_t chain, int32_t n_budgets, const int64_t *d_budgets, int64_t cap, rotor_op *d_ops,
+                          int64_t *d_count, int32_t *d_status, void *stream)
+{
+    if (!d_params || !d_dec || !d_budgets || !d_count || !d_status || !sizes_ok(n_chains, L, M))
+        return ROTOR_EINVAL;
+    if (L > ROTOR_MAX_L_RECONSTRUCT || chain < 0 || chain >= n_chains || n_budgets < 1 || cap < 0)
+        return ROTOR_EINVAL;
+    if (cap > 0 && !d_ops)
+        return ROTOR_EINVAL;
+    if (table_elems(n_chains, L, M) == 0)
+        return ROTOR_EINVAL;
+    const int64_t pitch = pitch_of(M);
+    const int64_t rows = (int64_t)L * (L + 1) / 2;
+    return launch_reconstruct(d_params + (int64_t)chain * ROTOR_N_ROWS * L, L, (int)M, pitch, rows,
+                              d_dec + (int64_t)chain * rows * pitch, n_budgets, d_budgets, cap, d_ops, d_count,
+                              d_status, (hipStream_t)stream) == hipSuccess
+               ? ROTOR_OK
+               : ROTOR_EDEVICE;
+}
+
+}  // extern "C"

@@ -1,0 +1,210 @@
+"""Python binding of the C ABI in include/rotor.h (``librotor.so``).
+
+Argument marshalling only: every step of the solve and of the sequence walk
+runs in the library's HIP kernels.  PyTorch provides device memory and the
+stream.  If the library has not been built, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "librotor.so")
+
+ROTOR_OK = 0
+ROTOR_EINVAL = -1
+ROTOR_EDOMAIN = -2
+ROTOR_EDEVICE = -3
+ROTOR_INFEASIBLE = -4
+ROTOR_ECAPACITY = -5
+ROTOR_ECORRUPT = -6
+ROTOR_INF = np.iinfo(np.int64).max
+F_CK, F_NONE, F_ALL, B = 0, 1, 2, 3
+N_ROWS = 6
+MAX_L = 32767
+MAX_L_RECONSTRUCT = 8191
+
+# name -> (restype, argtypes) of every function include/rotor.h declares
+_i32, _i64, _u64, _vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_void_p
+_P = ctypes.POINTER
+SIGNATURES = {
+    "rotor_version": (_i32, []),
+    "rotor_status_string": (ctypes.c_char_p, [_i32]),
+    "rotor_layout": (_i32, [_i32, _i32, _i64, _P(_i64), _P(_i64), _P(_u64), _P(_u64)]),
+    "rotor_row_index": (_i64, [_i32, _i32, _i32]),
+    "rotor_check_params": (_i32, [_vp, _i32, _i32, _i64]),
+    "rotor_solve": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp]),
+    "rotor_reconstruct": (_i32, [_vp, _i32, _i32, _i64, _vp, _i32, _i32, _vp, _i64, _vp, _vp, _vp, _vp]),
+}
+
+_lib = None
+
+
+class RotorError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {status_string(status)} ({status})")
+        self.status = status
+
+
+def lib():
+    """The loaded library.  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -c 'import __graft_entry__ as g; "
+                               "g.build()'` (hipcc, gfx950)")
+        l = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            f = getattr(l, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = l
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().rotor_status_string(status).decode()
+
+
+def _check(status: int, what: str):
+    if status != ROTOR_OK:
+        raise RotorError(status, what)
+
+
+def rotor_version() -> int:
+    return lib().rotor_version()
+
+
+def rotor_layout(n_chains: int, L: int, M: int):
+    """(pitch, rows_per_chain, cost_bytes, dec_bytes) of the tables."""
+    pitch, rows = ctypes.c_int64(), ctypes.c_int64()
+    cb, db = ctypes.c_uint64(), ctypes.c_uint64()
+    _check(lib().rotor_layout(n_chains, L, M, ctypes.byref(pitch), ctypes.byref(rows), ctypes.byref(cb),
+                              ctypes.byref(db)), "rotor_layout")
+    return pitch.value, rows.value, cb.value, db.value
+
+
+def rotor_row_index(L: int, s: int, t: int) -> int:
+    return lib().rotor_row_index(L, s, t)
+
+
+def rotor_check_params(params: np.ndarray, M: int) -> int:
+    """Status of the host parameter array [n_chains, 6, L] (ROTOR_OK,
+    ROTOR_EINVAL or ROTOR_EDOMAIN)."""
+    p = np.ascontiguousarray(params, dtype=np.int64)
+    if p.ndim == 2:
+        p = p[None]
+    if p.ndim != 3 or p.shape[1] != N_ROWS:
+        return ROTOR_EINVAL
+    return lib().rotor_check_params(p.ctypes.data, p.shape[0], p.shape[2], M)
+
+
+def _stream_ptr(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def _dev_ptr(t, dtype, what):
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != dtype or not t.is_contiguous():
+        raise ValueError(f"{what} must be a contiguous {dtype} CUDA tensor")
+    return t.data_ptr()
+
+
+def rotor_solve(d_params, n_chains: int, L: int, M: int, d_cost, d_dec, stream=None):
+    """Enqueue the table fill (asynchronous).  ``d_params``: int64 device
+    tensor [n_chains, 6, L]; ``d_cost`` / ``d_dec``: int64 / int16 device
+    tensors with at least rotor_layout's element counts."""
+    import torch
+    _, _, cb, db = rotor_layout(n_chains, L, M)
+    if d_params.numel() < n_chains * N_ROWS * L or d_cost.numel() * 8 < cb or d_dec.numel() * 2 < db:
+        raise ValueError("buffer smaller than the layout requires")
+    _check(lib().rotor_solve(_dev_ptr(d_params, torch.int64, "params"), n_chains, L, M,
+                             _dev_ptr(d_cost, torch.int64, "cost"), _dev_ptr(d_dec, torch.int16, "dec"),
+                             _stream_ptr(stream)), "rotor_solve")
+
+
+def rotor_reconstruct(d_params, n_chains: int, L: int, M: int, d_dec, chain: int, d_budgets, cap: int, d_ops,
+                      d_count, d_status, stream=None):
+    """Enqueue the sequence walk (asynchronous).  ``d_budgets``: int64 device
+    tensor [n]; ``d_ops``: int32 device tensor [n, cap, 2] (kind, stage);
+    ``d_count``: int64 [n]; ``d_status``: int32 [n]."""
+    import torch
+    n = d_budgets.numel()
+    if d_ops.numel() < n * cap * 2 or d_count.numel() < n or d_status.numel() < n:
+        raise ValueError("output buffer too small")
+    ops_ptr = _dev_ptr(d_ops, torch.int32, "ops") if cap > 0 else None
+    _check(lib().rotor_reconstruct(_dev_ptr(d_params, torch.int64, "params"), n_chains, L, M,
+                                   _dev_ptr(d_dec, torch.int16, "dec"), chain, n,
+                                   _dev_ptr(d_budgets, torch.int64, "budgets"), cap, ops_ptr,
+                                   _dev_ptr(d_count, torch.int64, "count"), _dev_ptr(d_status, torch.int32, "status"),
+                                   _stream_ptr(stream)), "rotor_reconstruct")
+
+
+# ---- conveniences (allocation and host copies only) -------------------------
+
+def upload_params(params: np.ndarray, M: int, device="cuda"):
+    """Check the host parameters against the domain, then copy them to the
+    device as an int64 tensor [n_chains, 6, L]."""
+    import torch
+    p = np.ascontiguousarray(params, dtype=np.int64)
+    if p.ndim == 2:
+        p = p[None]
+    _check(rotor_check_params(p, M), "rotor_check_params")
+    return torch.from_numpy(p).to(device)
+
+
+def alloc_tables(n_chains: int, L: int, M: int, device="cuda"):
+    """Uninitialised cost (int64) and decision (int16) tables shaped
+    [n_chains, rows, pitch]."""
+    import torch
+    pitch, rows, _, _ = rotor_layout(n_chains, L, M)
+    cost = torch.empty((n_chains, rows, pitch), dtype=torch.int64, device=device)
+    dec = torch.empty((n_chains, rows, pitch), dtype=torch.int16, device=device)
+    return cost, dec
+
+
+def solve(params: np.ndarray, M: int, device="cuda", stream=None):
+    """Upload, allocate and fill.  Returns (d_params, cost, dec) device
+    tensors; the fill is enqueued on ``stream``."""
+    p = np.asarray(params)
+    if p.ndim == 2:
+        p = p[None]
+    n_chains, _, L = p.shape
+    d_params = upload_params(p, M, device)
+    cost, dec = alloc_tables(n_chains, L, M, device)
+    rotor_solve(d_params, n_chains, L, M, cost, dec, stream)
+    return d_params, cost, dec
+
+
+def reconstruct(d_params, n_chains: int, L: int, M: int, d_dec, chain: int, budgets, stream=None):
+    """Sequences of chain ``chain`` at each budget, as lists of (kind, stage);
+    None where no sequence fits.  Synchronises the stream."""
+    import torch
+    device = d_dec.device
+    budgets = torch.as_tensor(np.asarray(budgets, dtype=np.int64), device=device)
+    n = budgets.numel()
+    cap = L * (L + 1) // 2 + L
+    ops = torch.empty((n, cap, 2), dtype=torch.int32, device=device)
+    count = torch.empty(n, dtype=torch.int64, device=device)
+    status = torch.empty(n, dtype=torch.int32, device=device)
+    rotor_reconstruct(d_params, n_chains, L, M, d_dec, chain, budgets, cap, ops, count, status, stream)
+    if stream is None:
+        torch.cuda.current_stream().synchronize()
+    else:
+        stream.synchronize()
+    count, status = count.cpu().numpy(), status.cpu().numpy()
+    ops = ops.cpu().numpy()
+    out = []
+    for b in range(n):
+        if status[b] == ROTOR_INFEASIBLE:
+            out.append(None)
+            continue
+        _check(int(status[b]), "rotor_reconstruct")
+        out.append([(int(k), int(s)) for k, s in ops[b, :count[b]]])
+    return out

@@ -1,0 +1,238 @@
+"""GPU parity: the HIP tables (through the C ABI) against the CPU oracle, bit
+for bit.  Costs are int64 and decisions int16, so the bar is exact equality
+of every cell.  Run on an MI355X with ``pytest -m gpu``."""
+import os
+
+import numpy as np
+import pytest
+
+import model
+from gpu_util import canonical_hashes, chain_tables, gpu_rows_in_oracle_order, solve_on_gpu
+from oracle import oracle as orc
+from paper_1911_13214_amd import chaingen
+from test_oracle_pins import TINY_M, tiny_chain, wide_chain
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def say(msg):
+    print(msg, flush=True)
+
+
+def assert_same(params, M, cost, dec, c=0, order=None):
+    L = params.shape[-1]
+    C, D = orc.solve(params[c:c + 1] if params.ndim == 3 else params, M)
+    gc, gd = chain_tables(cost, dec, c, L, M, order)
+    if not np.array_equal(gc, C):
+        bad = np.argwhere(gc != C)[0]
+        raise AssertionError(f"cost differs first at oracle row {bad[0]} m={bad[1]}: gpu {gc[tuple(bad)]} "
+                             f"oracle {C[tuple(bad)]}")
+    if not np.array_equal(gd, D):
+        bad = np.argwhere(gd != D)[0]
+        raise AssertionError(f"decision differs first at oracle row {bad[0]} m={bad[1]}: gpu {gd[tuple(bad)]} "
+                             f"oracle {D[tuple(bad)]}")
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_parity_full_tables(cfg):
+    params, L, M, _, name = chaingen.config(cfg)
+    say(f"parity {name}")
+    _, cost, dec = solve_on_gpu(params, M)
+    assert_same(params, M, cost, dec)
+
+
+def test_parity_batch_256_chains():
+    params, L, M, n, name = chaingen.config(4)
+    say(f"parity {name}")
+    _, cost, dec = solve_on_gpu(params, M)
+    order = gpu_rows_in_oracle_order(L)
+    for c in list(range(0, n, 17)) + [n - 1]:
+        assert_same(params, M, cost, dec, c, order)
+    g = np.load(os.path.join(GOLDEN, "batch256_L64_M640.npz"))
+    hc, hd = canonical_hashes(cost, dec, L, M)
+    assert hc == str(g["hash_cost"]) and hd == str(g["hash_dec"])
+
+
+def test_parity_large_chain():
+    params, L, M, _, name = chaingen.config(5)
+    say(f"parity {name}")
+    g = np.load(os.path.join(GOLDEN, "random_L500_M5000.npz"))
+    _, cost, dec = solve_on_gpu(params, M)
+    order = gpu_rows_in_oracle_order(L)
+    top = order[orc.row(L, 1, L)]
+    np.testing.assert_array_equal(cost[0, top, :M + 1].cpu().numpy(), g["top_cost"])
+    np.testing.assert_array_equal(dec[0, top, :M + 1].cpu().numpy(), g["top_dec"])
+    cells = g["cells"]
+    rows = order[[orc.row(L, int(s), int(t)) for s, t, _ in cells]]
+    gc = cost[0].cpu().numpy()
+    gd = dec[0].cpu().numpy()
+    np.testing.assert_array_equal(gc[rows, cells[:, 2]], g["cell_cost"])
+    np.testing.assert_array_equal(gd[rows, cells[:, 2]], g["cell_dec"])
+    # windows of the chain, solved by the oracle now: C(s,t,.) depends on
+    # stages s..t only
+    for a, b in [(1, 36), (233, 268), (465, 500)]:
+        sub = np.ascontiguousarray(params[:, :, a - 1:b])
+        C, D = orc.solve(sub, M)
+        Ls = b - a + 1
+        for s in range(1, Ls + 1):
+            for t in range(s, Ls + 1):
+                r = order[orc.row(L, s + a - 1, t + a - 1)]
+                np.testing.assert_array_equal(gc[r, :M + 1], C[orc.row(Ls, s, t)])
+                ds = D[orc.row(Ls, s, t)].astype(np.int64)
+                np.testing.assert_array_equal(gd[r, :M + 1], np.where(ds > 0, ds + a - 1, ds))
+    del gc, gd
+    hc, hd = canonical_hashes(cost, dec, L, M)
+    assert hc == str(g["hash_cost"]), "whole cost table hash"
+    assert hd == str(g["hash_dec"]), "whole decision table hash"
+
+
+@pytest.mark.parametrize("L,M,seed", [(1, 0, 1), (1, 37, 2), (2, 15, 3), (3, 16, 4), (5, 1, 9), (17, 255, 5),
+                                      (33, 257, 6), (40, 1023, 7), (64, 300, 8)])
+def test_edge_shapes(L, M, seed):
+    say(f"edge L={L} M={M}")
+    params = chaingen.random_chains(1, L, seed=seed)
+    _, cost, dec = solve_on_gpu(params, M)
+    assert_same(params, M, cost, dec)
+
+
+def test_tiny_and_wide_chains():
+    for seed in range(40):
+        p = tiny_chain(seed)
+        _, cost, dec = solve_on_gpu(p, TINY_M)
+        assert_same(p, TINY_M, cost, dec)
+    for seed in range(6):
+        p = wide_chain(seed, L=12, size_hi=40, over_hi=30)
+        _, cost, dec = solve_on_gpu(p, 400)
+        assert_same(p, 400, cost, dec)
+
+
+def test_shifts_beyond_the_budget():
+    # sizes larger than M: every shifted read falls below budget 0
+    p = chaingen.random_chains(1, 9, seed=12)
+    p[0, 2, ::2] += 300
+    p[0, 3, ::3] += 500
+    _, cost, dec = solve_on_gpu(p, 200)
+    assert_same(p, 200, cost, dec)
+
+
+def test_zero_sizes_any_length():
+    # no memory needed anywhere: with u_f >= 1 the no-recomputation schedule
+    # is optimal for every budget, F_all first everywhere
+    L, M = 700, 3
+    p = chaingen.random_chains(1, L, seed=13)
+    p[0, 2:] = 0
+    d_params, cost, dec = solve_on_gpu(p, M)
+    pre = np.concatenate([[0], np.cumsum(p[0, 0] + p[0, 1])])
+    gc = cost[0].cpu().numpy()
+    gd = dec[0].cpu().numpy()
+    for d in (0, 1, 2, 350, L - 1):
+        for s in sorted({1, min(2, L - d), L - d}):
+            t = s + d
+            r = d * L - d * (d - 1) // 2 + s - 1
+            assert (gc[r, :M + 1] == pre[t] - pre[s - 1]).all()
+            assert (gd[r, :M + 1] == 0).all()
+    from paper_1911_13214_amd import rotor
+    seq = rotor.reconstruct(d_params, 1, L, M, dec, 0, [0])[0]
+    assert seq == [(orc.F_ALL, l) for l in range(1, L + 1)] + [(orc.B, l) for l in range(L, 0, -1)]
+
+
+def test_large_budget_range():
+    p = chaingen.random_chains(1, 4, seed=14)
+    M = (1 << 18) + 5
+    _, cost, dec = solve_on_gpu(p, M)
+    assert_same(p, M, cost, dec)
+
+
+def test_batch_equals_single_solves():
+    params = chaingen.random_chains(9, 23, seed=15)
+    M = 230
+    _, cost, dec = solve_on_gpu(params, M)
+    for c in range(9):
+        _, c1, d1 = solve_on_gpu(params[c:c + 1], M)
+        assert np.array_equal(cost[c].cpu().numpy()[:, :M + 1], c1[0].cpu().numpy()[:, :M + 1])
+        assert np.array_equal(dec[c].cpu().numpy()[:, :M + 1], d1[0].cpu().numpy()[:, :M + 1])
+        assert_same(params, M, cost, dec, c)
+
+
+def test_deterministic():
+    params, L, M, _, _ = chaingen.config(3)
+    _, c1, d1 = solve_on_gpu(params, M)
+    _, c2, d2 = solve_on_gpu(params, M)
+    assert np.array_equal(c1[..., :M + 1].cpu().numpy(), c2[..., :M + 1].cpu().numpy())
+    assert np.array_equal(d1[..., :M + 1].cpu().numpy(), d2[..., :M + 1].cpu().numpy())
+
+
+def test_non_default_stream():
+    import torch
+    params, L, M, _, _ = chaingen.config(2)
+    st = torch.cuda.Stream()
+    with torch.cuda.stream(st):
+        _, cost, dec = solve_on_gpu(params, M, stream=st)
+    assert_same(params, M, cost, dec)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_reconstruct_matches_oracle(cfg):
+    from paper_1911_13214_amd import rotor
+    params, L, M, _, name = chaingen.config(cfg)
+    say(f"reconstruct {name}")
+    d_params, cost, dec = solve_on_gpu(params, M)
+    C, _ = orc.solve(params, M)
+    budgets = list(range(0, M + 1, max(1, (M + 1) // 97))) + [M]
+    seqs = rotor.reconstruct(d_params, 1, L, M, dec, 0, budgets)
+    for m, seq in zip(budgets, seqs):
+        assert seq == orc.reconstruct(params, M, C, m), m
+
+
+def test_reconstruct_batch_chain_and_replay():
+    from paper_1911_13214_amd import rotor
+    params, L, M, n, _ = chaingen.config(4)
+    d_params, cost, dec = solve_on_gpu(params, M)
+    for c in (0, 77, 255):
+        C, _ = orc.solve(params[c:c + 1], M)
+        budgets = [100, 200, 400, M]
+        for m, seq in zip(budgets, rotor.reconstruct(d_params, n, L, M, dec, c, budgets)):
+            assert seq == orc.reconstruct(params[c:c + 1], M, C, m)
+
+
+def test_reconstruct_large_chain_replays():
+    from paper_1911_13214_amd import rotor
+    params, L, M, _, _ = chaingen.config(5)
+    g = np.load(os.path.join(GOLDEN, "random_L500_M5000.npz"))
+    d_params, cost, dec = solve_on_gpu(params, M)
+    ch = model.Chain(params)
+    budgets = [m for m in range(0, M + 1, 250) if g["top_cost"][m] != orc.INF] + [M]
+    for m, seq in zip(budgets, rotor.reconstruct(d_params, 1, L, M, dec, 0, budgets)):
+        time, peak = model.simulate(ch, 1, L, seq)
+        assert time == g["top_cost"][m] and peak <= m
+
+
+def test_reconstruct_status_codes():
+    import torch
+
+    from paper_1911_13214_amd import rotor
+    params, L, M, _, _ = chaingen.config(1)
+    d_params, cost, dec = solve_on_gpu(params, M)
+    assert rotor.reconstruct(d_params, 1, L, M, dec, 0, [0, 24]) == [None, None]
+    budgets = torch.tensor([50, M + 1, -1, 100], dtype=torch.int64, device="cuda")
+    cap = 5
+    ops = torch.zeros((4, cap, 2), dtype=torch.int32, device="cuda")
+    count = torch.zeros(4, dtype=torch.int64, device="cuda")
+    status = torch.zeros(4, dtype=torch.int32, device="cuda")
+    rotor.rotor_reconstruct(d_params, 1, L, M, dec, 0, budgets, cap, ops, count, status)
+    torch.cuda.synchronize()
+    C, _ = orc.solve(params, M)
+    full50 = orc.reconstruct(params, M, C, 50)
+    st, cnt = status.cpu().tolist(), count.cpu().tolist()
+    assert st == [rotor.ROTOR_ECAPACITY, rotor.ROTOR_EINVAL, rotor.ROTOR_EINVAL, rotor.ROTOR_ECAPACITY]
+    assert cnt[0] == len(full50)
+    assert [tuple(x) for x in ops[0].cpu().tolist()] == full50[:cap]
+    # a table the library did not write is reported, not walked out of bounds
+    bad = dec.clone()
+    top = rotor.rotor_row_index(L, 1, L)
+    bad[0, top, 60] = L + 5
+    rotor.rotor_reconstruct(d_params, 1, L, M, bad, 0, torch.tensor([60], device="cuda"), 200, ops.new_zeros(1, 200, 2),
+                            count[:1], status[:1])
+    torch.cuda.synchronize()
+    assert status[0].item() == rotor.ROTOR_ECORRUPT
