@@ -85,7 +85,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-stages", type=int, default=160)
+    ap.add_argument("--cpu-stages", type=int, default=300)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="before timing, run one plain device-to-device copy of this many MiB so that a "
+                         "counter run can scale FETCH_SIZE / WRITE_SIZE by a kernel of known traffic")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the solver has no multi-GPU path (see the sharding note "
@@ -105,6 +108,15 @@ def main():
     cost, dec = rotor.alloc_tables(n_chains, L, M, dev)
     stream = torch.cuda.current_stream(dev)
     log(f"workload {name}: L={L} M={M} chains={n_chains} candidates={R:.4e} alg bytes={alg_bytes:.4e}")
+
+    if args.calibrate_copy:
+        src = torch.ones(args.calibrate_copy << 17, dtype=torch.int64, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy: {args.calibrate_copy} MiB read, {args.calibrate_copy} MiB written")
+        del src, dst
 
     for _ in range(args.warmup):
         rotor.rotor_solve(d_params, n_chains, L, M, cost, dec, stream)
