@@ -21,7 +21,6 @@ sys.path.insert(0, ROOT)
 
 METRIC = "DP candidate relaxations/sec (G/s) and solve ms at L=500,M=5000; % of BW roofline"
 HBM_PEAK_GBS = 8000.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_diag_kernel.json")
 FILL_SOURCE = os.path.join(ROOT, "paper_1911_13214_amd", "csrc", "rotor_fill.hip")
 
 
@@ -66,12 +65,13 @@ def cpu_baseline(params, M, stages):
     }
 
 
-def traffic_if_current():
-    """Measured HBM bytes per diagonal launch from the committed counter
-    summary, if it was taken on the current kernel source."""
-    if not os.path.exists(TRAFFIC_FILE):
+def traffic_if_current(kernel_class):
+    """Measured HBM bytes per launch of a kernel class from the committed
+    counter summary, if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel_class}_kernel.json")
+    if not os.path.exists(path):
         return None
-    rec = json.load(open(TRAFFIC_FILE))
+    rec = json.load(open(path))
     sha = hashlib.sha256(open(FILL_SOURCE, "rb").read()).hexdigest()
     if rec.get("fill_source_sha256") != sha:
         return None
@@ -86,6 +86,7 @@ def main():
     ap.add_argument("--workload", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-stages", type=int, default=300)
+    ap.add_argument("--profile-steps", type=int, default=2)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="before timing, run one plain device-to-device copy of this many MiB so that a "
                          "counter run can scale FETCH_SIZE / WRITE_SIZE by a kernel of known traffic")
@@ -147,8 +148,34 @@ def main():
         check = "top row equals oracle" if ok else "TOP ROW DIFFERS FROM ORACLE"
         log(check)
 
-    launches = L - 1
-    achieved = diag_bytes / launches / (ms * 1e-3 / launches) / 1e9
+    # per-kernel-class breakdown, HIP events around every launch on the same
+    # stream (separate steps, after the timed region)
+    classes = None
+    for _ in range(args.profile_steps):
+        st = rotor.rotor_solve_timed(d_params, n_chains, L, M, cost, dec, stream)
+        if classes is None:
+            classes = st
+        else:
+            for k in classes:
+                classes[k]["ms"] += st[k]["ms"]
+    for k in classes:
+        classes[k]["ms"] /= args.profile_steps
+    assert sum(c["split_candidates"] for c in classes.values()) == r_ck
+    assert sum(c["all_candidates"] for c in classes.values()) == r_all
+    kernels = {}
+    for k, c in classes.items():
+        if c["launches"] == 0:
+            continue
+        alg = 16 * c["split_candidates"] + 8 * c["all_candidates"] + 10 * c["cells"]
+        kernels[k] = {"launches": c["launches"], "ms": round(c["ms"], 3),
+                      "avg_launch_us": round(c["ms"] * 1e3 / c["launches"], 2),
+                      "candidates": c["split_candidates"] + c["all_candidates"], "alg_bytes": alg,
+                      "alg_GBps": round(alg / (c["ms"] * 1e-3) / 1e9, 1)}
+    dom = max(kernels, key=lambda k: kernels[k]["ms"])
+    kd = kernels[dom]
+    # achieved = algorithmic bytes per launch / average launch duration
+    achieved = kd["alg_bytes"] / kd["launches"] / (kd["ms"] * 1e-3 / kd["launches"]) / 1e9
+    log("kernel classes: " + json.dumps(kernels))
     out = {
         "metric": METRIC,
         "value": round(R / (ms * 1e-3) / 1e9, 3),
@@ -165,8 +192,11 @@ def main():
         "config": {"workload": name, "L": L, "M": M, "n_chains": n_chains, "candidates_per_step": R,
                    "alg_bytes_per_step": alg_bytes},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic_if_current(),
-                     "kernel": "diag_kernel", "launches_per_step": launches},
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic_if_current(dom),
+                     "kernel": f"{dom}_kernel", "launches_per_step": kd["launches"],
+                     "avg_launch_us": kd["avg_launch_us"]},
+        "kernels": kernels,
+        "solve_alg_GBps": round(alg_bytes / (ms * 1e-3) / 1e9, 1),
         "check": check,
     }
     if not args.no_cpu_baseline:

@@ -26,8 +26,8 @@
  * Stage l sits at column l-1.  A batch of n_chains chains of equal L is
  * packed chain-major: params[c][row][l-1], c = 0..n_chains-1.
  *
- * Domain.  Every value is >= 0; sizes and overheads are < 2^30; M < 2^30;
- * for every chain L * sum(u_f) + sum(u_b) < 2^60 (this bounds every finite
+ * Domain.  Every value is >= 0; sizes and overheads are < 2^30; M < 2^28;
+ * for every chain L * sum(u_f) + sum(u_b) < 2^44 (this bounds every finite
  * cost: a persistent schedule runs each forward at most L times).
  * rotor_check_params verifies this on a host copy.  Kernels never access
  * memory out of bounds whatever the parameter values; outside the domain the
@@ -39,8 +39,8 @@
  * row (1, L) at M - size(a^0).
  *
  * Table layout (device memory, caller-owned).  Per chain, the L(L+1)/2 pairs
- * (s, t), 1 <= s <= t <= L, are stored by increasing d = t - s and then s:
- *   row(s, t) = d*L - d*(d-1)/2 + (s-1)
+ * (s, t), 1 <= s <= t <= L, are stored s-major (by s, then t):
+ *   row(s, t) = (s-1)*L - (s-1)*(s-2)/2 + (t-s)
  * Each row holds `pitch` elements, pitch = M+1 rounded up to a multiple of
  * 16 (128 bytes of costs); only columns 0..M are written.  The cost table is
  * int64 and the decision table int16, with the same indexing:
@@ -149,6 +149,29 @@ ROTOR_API int32_t rotor_check_params(const int64_t *h_params, int32_t n_chains, 
  * a launch fails.  Allocates nothing. */
 ROTOR_API int32_t rotor_solve(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
                     int16_t *d_dec, void *stream);
+
+/* Kernel classes of the fill, for rotor_solve_timed. */
+#define ROTOR_KERNEL_LEAF 0   /* single-stage cells, Eq. (DP:Init) */
+#define ROTOR_KERNEL_DIAG 1   /* pairs inside one 16-stage diagonal block, all splits */
+#define ROTOR_KERNEL_MIDDLE 2 /* split points whose operands lie in finished blocks */
+#define ROTOR_KERNEL_EDGE 3   /* remaining split points, C_2, gates, final cells */
+#define ROTOR_N_KERNEL_CLASSES 4
+
+typedef struct {
+    int32_t launches;          /* kernel launches of this class */
+    double ms;                 /* summed launch durations, from HIP events */
+    uint64_t split_candidates; /* C_1 candidates evaluated (split point x budget x pair) */
+    uint64_t all_candidates;   /* C_2 candidates evaluated (budget x pair) */
+    uint64_t cells;            /* final (cost, decision) cells written */
+} rotor_kernel_stats;
+
+/* rotor_solve, plus a breakdown of the fill by kernel class: a HIP event pair
+ * is recorded on `stream` around every launch, and the call waits for the
+ * stream.  stats: HOST array of ROTOR_N_KERNEL_CLASSES entries, overwritten.
+ * Summed over the classes, split_candidates is (L^3 - L)/6 (M+1) n_chains and
+ * all_candidates L(L-1)/2 (M+1) n_chains.  Same return codes as rotor_solve. */
+ROTOR_API int32_t rotor_solve_timed(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
+                                    int16_t *d_dec, void *stream, rotor_kernel_stats *stats);
 
 /* Algorithm 2 (OptRec): the optimal persistent sequence of the whole chain
  * [1, L] of chain `chain` for each of n_budgets budgets, walked on the device

@@ -91,17 +91,17 @@ int64_t oracle_m_none(int L, const int64_t *p, int s, int t)
 }
 
 /* Input domain shared with the GPU library: non-negative values, sizes and
- * overheads below 2^30, M below 2^30, and L * sum(u_f) + sum(u_b) below 2^60
+ * overheads below 2^30, M below 2^28, and L * sum(u_f) + sum(u_b) below 2^44
  * (a bound on every finite cost: no stage is run forward more than L times in
  * a persistent schedule). */
 int oracle_check(int L, int64_t M, const int64_t *p)
 {
-    if (L < 1 || L > 32767 || M < 0 || M >= ((int64_t)1 << 30))
+    if (L < 1 || L > 32767 || M < 0 || M >= ((int64_t)1 << 28))
         return -1;
     orc_chain c = {L, M, p};
     uint64_t suf = 0, sub = 0;
     for (int l = 1; l <= L; ++l) {
-        if (uf(&c, l) < 0 || ub(&c, l) < 0 || uf(&c, l) >= ((int64_t)1 << 60) || ub(&c, l) >= ((int64_t)1 << 60))
+        if (uf(&c, l) < 0 || ub(&c, l) < 0 || uf(&c, l) >= ((int64_t)1 << 44) || ub(&c, l) >= ((int64_t)1 << 44))
             return -1;
         int64_t s[4] = {wa(&c, l), wab(&c, l), of(&c, l), ob(&c, l)};
         for (int k = 0; k < 4; ++k)
@@ -109,11 +109,11 @@ int oracle_check(int L, int64_t M, const int64_t *p)
                 return -1;
         suf += (uint64_t)uf(&c, l);
         sub += (uint64_t)ub(&c, l);
-        if (suf >= ((uint64_t)1 << 60) || sub >= ((uint64_t)1 << 60))
+        if (suf >= ((uint64_t)1 << 44) || sub >= ((uint64_t)1 << 44))
             return -1;
     }
-    /* L * suf + sub < 2^60, written without overflow */
-    if (suf > (((uint64_t)1 << 60) - sub) / (uint64_t)L)
+    /* L * suf + sub < 2^44, written without overflow */
+    if (suf > (((uint64_t)1 << 44) - sub) / (uint64_t)L)
         return -1;
     return 0;
 }

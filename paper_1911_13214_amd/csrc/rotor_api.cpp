@@ -2,6 +2,8 @@
 // the launches.  The arithmetic of the method lives in the kernels.
 #include <stdint.h>
 
+#include <vector>
+
 #include "rotor_internal.h"
 
 using namespace rotor;
@@ -9,11 +11,12 @@ using namespace rotor;
 namespace {
 
 constexpr int64_t kMaxSize = (int64_t)1 << 30;
-constexpr uint64_t kCostBound = (uint64_t)1 << 60;
+constexpr int64_t kMaxBudget = (int64_t)1 << 28;
+constexpr uint64_t kCostBound = (uint64_t)1 << 44;
 
 bool sizes_ok(int32_t n_chains, int32_t L, int64_t M)
 {
-    return n_chains >= 1 && n_chains <= ROTOR_MAX_CHAINS && L >= 1 && L <= ROTOR_MAX_L && M >= 0 && M < kMaxSize;
+    return n_chains >= 1 && n_chains <= ROTOR_MAX_CHAINS && L >= 1 && L <= ROTOR_MAX_L && M >= 0 && M < kMaxBudget;
 }
 
 // Number of elements of one table, or 0 on overflow.
@@ -25,6 +28,84 @@ uint64_t table_elems(int32_t n_chains, int32_t L, int64_t M)
         return 0;
     return (uint64_t)e;
 }
+
+bool solve_args_ok(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, const int64_t *d_cost,
+                   const int16_t *d_dec)
+{
+    if (!d_params || !d_cost || !d_dec || !sizes_ok(n_chains, L, M) || table_elems(n_chains, L, M) == 0)
+        return false;
+    return !(((uintptr_t)d_params | (uintptr_t)d_cost) % 8 || (uintptr_t)d_dec % 2);
+}
+
+Tables make_tables(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost, int16_t *d_dec)
+{
+    Tables tb;
+    tb.params = d_params;
+    tb.cost = d_cost;
+    tb.dec = d_dec;
+    tb.L = L;
+    tb.M = (int)M;
+    tb.n_chains = n_chains;
+    tb.pitch = pitch_of(M);
+    tb.rows = (int64_t)L * (L + 1) / 2;
+    return tb;
+}
+
+// Records an event pair around every launch and adds up the work counts.
+struct TimingObserver : LaunchObserver {
+    struct Pair {
+        hipEvent_t start, stop;
+        KernelClass k;
+    };
+    std::vector<Pair> pairs;
+    rotor_kernel_stats *stats;
+
+    explicit TimingObserver(rotor_kernel_stats *st) : stats(st)
+    {
+        for (int k = 0; k < ROTOR_N_KERNEL_CLASSES; ++k)
+            stats[k] = rotor_kernel_stats{0, 0.0, 0, 0, 0};
+    }
+    hipError_t before(KernelClass k, hipStream_t s) override
+    {
+        Pair p{nullptr, nullptr, k};
+        hipError_t e = hipEventCreate(&p.start);
+        if (e == hipSuccess)
+            e = hipEventCreate(&p.stop);
+        if (e == hipSuccess)
+            e = hipEventRecord(p.start, s);
+        pairs.push_back(p);
+        return e;
+    }
+    hipError_t after(KernelClass k, const LaunchWork &w, hipStream_t s) override
+    {
+        rotor_kernel_stats &st = stats[k];
+        st.launches += 1;
+        st.split_candidates += w.split_candidates;
+        st.all_candidates += w.all_candidates;
+        st.cells += w.cells;
+        return hipEventRecord(pairs.back().stop, s);
+    }
+    hipError_t finish(hipStream_t s)
+    {
+        hipError_t e = hipStreamSynchronize(s);
+        for (Pair &p : pairs) {
+            float ms = 0.f;
+            if (e == hipSuccess && p.start && p.stop)
+                e = hipEventElapsedTime(&ms, p.start, p.stop);
+            stats[p.k].ms += ms;
+        }
+        return e;
+    }
+    ~TimingObserver() override
+    {
+        for (Pair &p : pairs) {
+            if (p.start)
+                (void)hipEventDestroy(p.start);
+            if (p.stop)
+                (void)hipEventDestroy(p.stop);
+        }
+    }
+};
 
 }  // namespace
 
@@ -69,7 +150,7 @@ int64_t rotor_row_index(int32_t L, int32_t s, int32_t t)
 {
     if (L < 1 || L > ROTOR_MAX_L || s < 1 || t < s || t > L)
         return -1;
-    return row_of(L, t - s, s);
+    return row_of(L, s, t);
 }
 
 int32_t rotor_check_params(const int64_t *h_params, int32_t n_chains, int32_t L, int64_t M)
@@ -93,7 +174,7 @@ int32_t rotor_check_params(const int64_t *h_params, int32_t n_chains, int32_t L,
             if (suf >= kCostBound || sub >= kCostBound)
                 return ROTOR_EDOMAIN;
         }
-        // L * suf + sub < 2^60
+        // L * suf + sub < 2^44
         if (suf > (kCostBound - sub) / (uint64_t)L)
             return ROTOR_EDOMAIN;
     }
@@ -103,20 +184,22 @@ int32_t rotor_check_params(const int64_t *h_params, int32_t n_chains, int32_t L,
 int32_t rotor_solve(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
                     int16_t *d_dec, void *stream)
 {
-    if (!d_params || !d_cost || !d_dec || !sizes_ok(n_chains, L, M) || table_elems(n_chains, L, M) == 0)
+    if (!solve_args_ok(d_params, n_chains, L, M, d_cost, d_dec))
         return ROTOR_EINVAL;
-    if (((uintptr_t)d_params | (uintptr_t)d_cost) % 8 || (uintptr_t)d_dec % 2)
-        return ROTOR_EINVAL;
-    Tables tb;
-    tb.params = d_params;
-    tb.cost = d_cost;
-    tb.dec = d_dec;
-    tb.L = L;
-    tb.M = (int)M;
-    tb.n_chains = n_chains;
-    tb.pitch = pitch_of(M);
-    tb.rows = (int64_t)L * (L + 1) / 2;
+    const Tables tb = make_tables(d_params, n_chains, L, M, d_cost, d_dec);
     return launch_fill(tb, (hipStream_t)stream) == hipSuccess ? ROTOR_OK : ROTOR_EDEVICE;
+}
+
+int32_t rotor_solve_timed(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
+                          int16_t *d_dec, void *stream, rotor_kernel_stats *stats)
+{
+    if (!stats || !solve_args_ok(d_params, n_chains, L, M, d_cost, d_dec))
+        return ROTOR_EINVAL;
+    const Tables tb = make_tables(d_params, n_chains, L, M, d_cost, d_dec);
+    TimingObserver obs(stats);
+    hipError_t e = launch_fill(tb, (hipStream_t)stream, &obs);
+    const hipError_t f = obs.finish((hipStream_t)stream);
+    return (e == hipSuccess && f == hipSuccess) ? ROTOR_OK : ROTOR_EDEVICE;
 }
 
 int32_t rotor_reconstruct(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, const int16_t *d_dec,

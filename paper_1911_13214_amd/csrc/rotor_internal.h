@@ -9,11 +9,12 @@
 
 namespace rotor {
 
-// Row of the pair (s, t), d = t - s, in a chain's table: rows are stored by
-// increasing d, then by s (1-based).
-__host__ __device__ inline int64_t row_of(int L, int d, int s)
+// Row of the pair (s, t), 1 <= s <= t <= L, in a chain's table: the upper
+// triangle stored s-major, so the rows (s, s), (s, s+1), ..., (s, L) are
+// consecutive and the row of (s, t+1) follows the row of (s, t).
+__host__ __device__ inline int64_t row_of(int L, int s, int t)
 {
-    return (int64_t)d * L - (int64_t)d * (d - 1) / 2 + (s - 1);
+    return (int64_t)(s - 1) * L - (int64_t)(s - 1) * (s - 2) / 2 + (t - s);
 }
 
 __host__ __device__ inline int64_t pitch_of(int64_t M) { return (M + 1 + 15) / 16 * 16; }
@@ -30,8 +31,26 @@ struct Tables {
     int64_t rows;           // L(L+1)/2
 };
 
+// Kernel classes of the fill, in the order of rotor_kernel_stats.
+enum KernelClass { kLeaf = 0, kDiag = 1, kMiddle = 2, kEdge = 3 };
+
+// Work of one launch, counted exactly from its grid: C_1 candidates (split
+// points times budgets), C_2 candidates and final cells written.
+struct LaunchWork {
+    uint64_t split_candidates;
+    uint64_t all_candidates;
+    uint64_t cells;
+};
+
+// Optional hooks around every launch of the fill (timing, accounting).
+struct LaunchObserver {
+    virtual hipError_t before(KernelClass k, hipStream_t s) = 0;
+    virtual hipError_t after(KernelClass k, const LaunchWork &w, hipStream_t s) = 0;
+    virtual ~LaunchObserver() {}
+};
+
 // Enqueue the whole table fill on `stream`.  Returns a HIP error code.
-hipError_t launch_fill(const Tables &tb, hipStream_t stream);
+hipError_t launch_fill(const Tables &tb, hipStream_t stream, LaunchObserver *obs = nullptr);
 
 // Enqueue the sequence walk (one workgroup per budget).
 hipError_t launch_reconstruct(const int64_t *params, int L, int M, int64_t pitch, int64_t rows,

@@ -55,7 +55,7 @@ __global__ void walk_kernel(const int64_t *__restrict__ params, int L, int M, in
         }
         const int t = (int)((f >> 32) & 0x7fff);
         const int64_t m = (int64_t)(uint32_t)f;
-        const int dv = dec[row_of(L, t - s, s) * pitch + m];
+        const int dv = dec[row_of(L, s, t) * pitch + m];
         if (dv < 0) {
             st = root ? ROTOR_INFEASIBLE : ROTOR_ECORRUPT;
             break;

@@ -38,7 +38,15 @@ SIGNATURES = {
     "rotor_check_params": (_i32, [_vp, _i32, _i32, _i64]),
     "rotor_solve": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp]),
     "rotor_reconstruct": (_i32, [_vp, _i32, _i32, _i64, _vp, _i32, _i32, _vp, _i64, _vp, _vp, _vp, _vp]),
+    "rotor_solve_timed": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp, _vp]),
 }
+
+KERNEL_CLASSES = ("leaf", "diag", "middle", "edge")
+
+
+class KernelStats(ctypes.Structure):
+    _fields_ = [("launches", ctypes.c_int32), ("ms", ctypes.c_double), ("split_candidates", ctypes.c_uint64),
+                ("all_candidates", ctypes.c_uint64), ("cells", ctypes.c_uint64)]
 
 _lib = None
 
@@ -127,6 +135,20 @@ def rotor_solve(d_params, n_chains: int, L: int, M: int, d_cost, d_dec, stream=N
     _check(lib().rotor_solve(_dev_ptr(d_params, torch.int64, "params"), n_chains, L, M,
                              _dev_ptr(d_cost, torch.int64, "cost"), _dev_ptr(d_dec, torch.int16, "dec"),
                              _stream_ptr(stream)), "rotor_solve")
+
+
+def rotor_solve_timed(d_params, n_chains: int, L: int, M: int, d_cost, d_dec, stream=None):
+    """rotor_solve with a per-kernel-class breakdown (synchronous).  Returns
+    {class: {launches, ms, split_candidates, all_candidates, cells}}."""
+    import torch
+    _, _, cb, db = rotor_layout(n_chains, L, M)
+    if d_params.numel() < n_chains * N_ROWS * L or d_cost.numel() * 8 < cb or d_dec.numel() * 2 < db:
+        raise ValueError("buffer smaller than the layout requires")
+    stats = (KernelStats * len(KERNEL_CLASSES))()
+    _check(lib().rotor_solve_timed(_dev_ptr(d_params, torch.int64, "params"), n_chains, L, M,
+                                   _dev_ptr(d_cost, torch.int64, "cost"), _dev_ptr(d_dec, torch.int16, "dec"),
+                                   _stream_ptr(stream), ctypes.cast(stats, ctypes.c_void_p)), "rotor_solve_timed")
+    return {name: {f: getattr(st, f) for f, _ in KernelStats._fields_} for name, st in zip(KERNEL_CLASSES, stats)}
 
 
 def rotor_reconstruct(d_params, n_chains: int, L: int, M: int, d_dec, chain: int, d_budgets, cap: int, d_ops,

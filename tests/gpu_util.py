@@ -8,12 +8,16 @@ from oracle import oracle as orc
 
 
 def gpu_rows_in_oracle_order(L: int) -> np.ndarray:
-    """For each oracle row (s-major), the library's row (by d = t - s, then s)."""
+    """For each oracle row, the library's row of the same pair (s, t), from
+    the layout the C ABI documents (both are s-major today; the mapping keeps
+    the tests independent of that)."""
+    from paper_1911_13214_amd import rotor
+
     idx = np.empty(L * (L + 1) // 2, dtype=np.int64)
     for s in range(1, L + 1):
-        t = np.arange(s, L + 1)
-        d = t - s
-        idx[orc.row(L, s, s):orc.row(L, s, L) + 1] = d * L - d * (d - 1) // 2 + (s - 1)
+        for t in range(s, L + 1):
+            idx[orc.row(L, s, t)] = (s - 1) * L - (s - 1) * (s - 2) // 2 + (t - s)
+    assert idx[-1] == rotor.rotor_row_index(L, L, L) and idx[0] == rotor.rotor_row_index(L, 1, 1)
     return idx
 
 

@@ -51,21 +51,16 @@ def test_layout(n_chains, L, M):
     assert cb == n_chains * rows * pitch * 8 and db == n_chains * rows * pitch * 2
 
 
-def test_row_index_is_a_bijection_by_diagonal():
+def test_row_index_is_s_major():
     L = 9
-    seen = []
-    for s in range(1, L + 1):
-        for t in range(s, L + 1):
-            seen.append((rotor.rotor_row_index(L, s, t), t - s, s))
-    idx = sorted(seen)
-    assert [i for i, _, _ in idx] == list(range(L * (L + 1) // 2))
-    # stored by increasing t - s, then s
-    assert [(d, s) for _, d, s in idx] == sorted((d, s) for _, d, s in idx)
+    rows = [rotor.rotor_row_index(L, s, t) for s in range(1, L + 1) for t in range(s, L + 1)]
+    # the rows of (s, s), (s, s+1), ..., (s, L) are consecutive, s ascending
+    assert rows == list(range(L * (L + 1) // 2))
     for bad in [(0, 1), (2, 1), (1, L + 1)]:
         assert rotor.rotor_row_index(L, *bad) == -1
 
 
-@pytest.mark.parametrize("args", [(0, 10, 100), (1, 0, 100), (1, 32768, 1), (1, 10, -1), (1, 10, 1 << 30),
+@pytest.mark.parametrize("args", [(0, 10, 100), (1, 0, 100), (1, 32768, 1), (1, 10, -1), (1, 10, 1 << 28),
                                   (65536, 10, 10)])
 def test_layout_rejects_bad_sizes(args):
     with pytest.raises(rotor.RotorError) as e:
@@ -75,7 +70,7 @@ def test_layout_rejects_bad_sizes(args):
 
 def test_layout_rejects_byte_overflow():
     with pytest.raises(rotor.RotorError):
-        rotor.rotor_layout(65535, 32767, (1 << 30) - 1)
+        rotor.rotor_layout(65535, 32767, (1 << 28) - 1)
 
 
 def test_check_params():
@@ -88,8 +83,13 @@ def test_check_params():
         q[1, row, 3] = val
         assert rotor.rotor_check_params(q, 100) == rotor.ROTOR_EDOMAIN
     q = p.copy()
-    q[0, 0, :] = 1 << 57
+    q[0, 0, :] = 1 << 44  # one value beyond the bound
     assert rotor.rotor_check_params(q, 100) == rotor.ROTOR_EDOMAIN
+    q = p.copy()
+    q[0, 0, :] = 1 << 41  # each value fits, L * sum(u_f) = 25 * 2^41 does not
+    assert rotor.rotor_check_params(q, 100) == rotor.ROTOR_EDOMAIN
+    q[0, 0, :] = (1 << 44) // 26
+    assert rotor.rotor_check_params(q, 100) == rotor.ROTOR_OK
     assert rotor.rotor_check_params(p, -1) == rotor.ROTOR_EINVAL
     assert rotor.rotor_check_params(p[:, :4], 10) == rotor.ROTOR_EINVAL
 

@@ -129,7 +129,8 @@ def test_zero_sizes_any_length():
     for d in (0, 1, 2, 350, L - 1):
         for s in sorted({1, min(2, L - d), L - d}):
             t = s + d
-            r = d * L - d * (d - 1) // 2 + s - 1
+            from paper_1911_13214_amd import rotor
+            r = rotor.rotor_row_index(L, s, t)
             assert (gc[r, :M + 1] == pre[t] - pre[s - 1]).all()
             assert (gd[r, :M + 1] == 0).all()
     from paper_1911_13214_amd import rotor
@@ -236,3 +237,19 @@ def test_reconstruct_status_codes():
                             count[:1], status[:1])
     torch.cuda.synchronize()
     assert status[0].item() == rotor.ROTOR_ECORRUPT
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_timed_solve_matches_and_counts_the_work(cfg):
+    from paper_1911_13214_amd import rotor
+    params, L, M, n, _ = chaingen.config(cfg)
+    d_params, cost, dec = solve_on_gpu(params, M)
+    c2, d2 = rotor.alloc_tables(n, L, M)
+    stats = rotor.rotor_solve_timed(d_params, n, L, M, c2, d2)
+    assert np.array_equal(cost[..., :M + 1].cpu().numpy(), c2[..., :M + 1].cpu().numpy())
+    assert np.array_equal(dec[..., :M + 1].cpu().numpy(), d2[..., :M + 1].cpu().numpy())
+    W = M + 1
+    assert sum(s["split_candidates"] for s in stats.values()) == (L ** 3 - L) // 6 * W * n
+    assert sum(s["all_candidates"] for s in stats.values()) == L * (L - 1) // 2 * W * n
+    assert sum(s["cells"] for s in stats.values()) == L * (L + 1) // 2 * W * n
+    assert all(s["ms"] >= 0 for s in stats.values()) and stats["leaf"]["launches"] == 1

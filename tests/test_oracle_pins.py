@@ -283,7 +283,8 @@ def test_domain_checks():
         q[0, row, 1] = val
         assert not orc.check(q, 100)
     assert not orc.check(p, -1)
-    assert not orc.check(p, 1 << 30)
+    assert not orc.check(p, 1 << 28)
+    assert orc.check(p, (1 << 28) - 1)
     q = p.copy()
-    q[0, 0, :] = 1 << 57  # L * sum(u_f) beyond 2^60
+    q[0, 0, :] = 1 << 41  # L * sum(u_f) = 16 * 2^41, beyond 2^44
     assert not orc.check(q, 100)
