@@ -107,6 +107,7 @@ def main():
     dev = torch.device("cuda:0")
     d_params = rotor.upload_params(params, M, dev)
     cost, dec = rotor.alloc_tables(n_chains, L, M, dev)
+    work = rotor.alloc_workspace(n_chains, L, M, dev)
     stream = torch.cuda.current_stream(dev)
     log(f"workload {name}: L={L} M={M} chains={n_chains} candidates={R:.4e} alg bytes={alg_bytes:.4e}")
 
@@ -120,7 +121,7 @@ def main():
         del src, dst
 
     for _ in range(args.warmup):
-        rotor.rotor_solve(d_params, n_chains, L, M, cost, dec, stream)
+        rotor.rotor_solve(d_params, n_chains, L, M, cost, dec, work, stream)
     torch.cuda.synchronize()
 
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
@@ -129,7 +130,7 @@ def main():
     t0 = time.perf_counter()
     for k in range(args.steps):
         starts[k].record(stream)
-        rotor.rotor_solve(d_params, n_chains, L, M, cost, dec, stream)
+        rotor.rotor_solve(d_params, n_chains, L, M, cost, dec, work, stream)
         ends[k].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -152,7 +153,7 @@ def main():
     # stream (separate steps, after the timed region)
     classes = None
     for _ in range(args.profile_steps):
-        st = rotor.rotor_solve_timed(d_params, n_chains, L, M, cost, dec, stream)
+        st = rotor.rotor_solve_timed(d_params, n_chains, L, M, cost, dec, work, stream)
         if classes is None:
             classes = st
         else:

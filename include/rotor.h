@@ -56,8 +56,9 @@
  * stream).  Entry points that take device buffers only enqueue work and
  * return; argument errors are reported synchronously by the return value,
  * device-side failures surface at the caller's next synchronisation.  The
- * library keeps no state between calls and allocates no device memory;
- * concurrent calls on distinct output buffers are independent.
+ * library keeps no state between calls and allocates no device memory (the
+ * caller passes the solve's workspace); concurrent calls on distinct output
+ * buffers and workspaces are independent.
  */
 #ifndef ROTOR_H
 #define ROTOR_H
@@ -134,28 +135,39 @@ ROTOR_API int64_t rotor_row_index(int32_t L, int32_t s, int32_t t);
  * ROTOR_EDOMAIN (a value out of range).  Host only. */
 ROTOR_API int32_t rotor_check_params(const int64_t *h_params, int32_t n_chains, int32_t L, int64_t M);
 
+/* Bytes of device workspace rotor_solve needs for these sizes: per-pair
+ * gates, prefix sums, per-chain flags and a compact 4-byte-per-cell copy of
+ * the cost table (about 40% of cost_bytes + dec_bytes).  Host only.  Returns
+ * ROTOR_OK or ROTOR_EINVAL (as rotor_layout). */
+ROTOR_API int32_t rotor_workspace_bytes(int32_t n_chains, int32_t L, int64_t M, uint64_t *bytes);
+
 /* Fill the cost table C_BP(s, t, m) and the decision table for every chain,
  * every pair 1 <= s <= t <= L and every budget 0 <= m <= M: Theorem 1,
- * Eq. (DP:Init) for t = s and Eq. (DP:mainrec) for t > s, evaluated by
- * increasing t - s (every term of the recurrence is a strictly shorter
- * sub-chain, which Algorithm 1's printed loop order does not respect).
+ * Eq. (DP:Init) for t = s and Eq. (DP:mainrec) for t > s, evaluated so that
+ * every term is read after it is final (Algorithm 1's printed loop order does
+ * not respect this; the fill goes by increasing t - s within 16 x 16 blocks of
+ * pairs, block-diagonal by block-diagonal).
  *
  *   d_params  DEVICE, read only: [n_chains][6][L] int64 (layout above).
  *   d_cost    DEVICE, written: int64, rotor_layout's cost_bytes.
  *   d_dec     DEVICE, written: int16, rotor_layout's dec_bytes.
+ *   d_work    DEVICE scratch of at least rotor_workspace_bytes, caller-owned;
+ *             its contents on entry do not matter and on exit are unspecified.
  *   stream    hipStream_t or NULL.
  * Asynchronous.  Returns ROTOR_OK once every kernel is enqueued, ROTOR_EINVAL
- * for a null or misaligned pointer or a size out of range, ROTOR_EDEVICE if
- * a launch fails.  Allocates nothing. */
+ * for a null or misaligned pointer, a size out of range or a workspace too
+ * small, ROTOR_EDEVICE if a launch fails.  Allocates nothing.  Calls that
+ * share a workspace must not overlap. */
 ROTOR_API int32_t rotor_solve(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
-                    int16_t *d_dec, void *stream);
+                              int16_t *d_dec, void *d_work, uint64_t work_bytes, void *stream);
 
 /* Kernel classes of the fill, for rotor_solve_timed. */
 #define ROTOR_KERNEL_LEAF 0   /* single-stage cells, Eq. (DP:Init) */
 #define ROTOR_KERNEL_DIAG 1   /* pairs inside one 16-stage diagonal block, all splits */
 #define ROTOR_KERNEL_MIDDLE 2 /* split points whose operands lie in finished blocks */
 #define ROTOR_KERNEL_EDGE 3   /* remaining split points, C_2, gates, final cells */
-#define ROTOR_N_KERNEL_CLASSES 4
+#define ROTOR_KERNEL_PREP 4   /* gates, prefix sums and value path of every chain */
+#define ROTOR_N_KERNEL_CLASSES 5
 
 typedef struct {
     int32_t launches;          /* kernel launches of this class */
@@ -171,7 +183,8 @@ typedef struct {
  * Summed over the classes, split_candidates is (L^3 - L)/6 (M+1) n_chains and
  * all_candidates L(L-1)/2 (M+1) n_chains.  Same return codes as rotor_solve. */
 ROTOR_API int32_t rotor_solve_timed(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
-                                    int16_t *d_dec, void *stream, rotor_kernel_stats *stats);
+                                    int16_t *d_dec, void *d_work, uint64_t work_bytes, void *stream,
+                                    rotor_kernel_stats *stats);
 
 /* Algorithm 2 (OptRec): the optimal persistent sequence of the whole chain
  * [1, L] of chain `chain` for each of n_budgets budgets, walked on the device

@@ -30,11 +30,13 @@ uint64_t table_elems(int32_t n_chains, int32_t L, int64_t M)
 }
 
 bool solve_args_ok(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, const int64_t *d_cost,
-                   const int16_t *d_dec)
+                   const int16_t *d_dec, const void *d_work, uint64_t work_bytes)
 {
-    if (!d_params || !d_cost || !d_dec || !sizes_ok(n_chains, L, M) || table_elems(n_chains, L, M) == 0)
+    if (!d_params || !d_cost || !d_dec || !d_work || !sizes_ok(n_chains, L, M) || table_elems(n_chains, L, M) == 0)
         return false;
-    return !(((uintptr_t)d_params | (uintptr_t)d_cost) % 8 || (uintptr_t)d_dec % 2);
+    if (work_bytes < work_layout(n_chains, L, pitch_of(M)).total)
+        return false;
+    return !(((uintptr_t)d_params | (uintptr_t)d_cost | (uintptr_t)d_work) % 8 || (uintptr_t)d_dec % 2);
 }
 
 Tables make_tables(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost, int16_t *d_dec)
@@ -181,23 +183,35 @@ int32_t rotor_check_params(const int64_t *h_params, int32_t n_chains, int32_t L,
     return ROTOR_OK;
 }
 
-int32_t rotor_solve(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
-                    int16_t *d_dec, void *stream)
+int32_t rotor_workspace_bytes(int32_t n_chains, int32_t L, int64_t M, uint64_t *bytes)
 {
-    if (!solve_args_ok(d_params, n_chains, L, M, d_cost, d_dec))
+    if (!sizes_ok(n_chains, L, M) || table_elems(n_chains, L, M) == 0)
+        return ROTOR_EINVAL;
+    if (bytes)
+        *bytes = work_layout(n_chains, L, pitch_of(M)).total;
+    return ROTOR_OK;
+}
+
+int32_t rotor_solve(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
+                    int16_t *d_dec, void *d_work, uint64_t work_bytes, void *stream)
+{
+    if (!solve_args_ok(d_params, n_chains, L, M, d_cost, d_dec, d_work, work_bytes))
         return ROTOR_EINVAL;
     const Tables tb = make_tables(d_params, n_chains, L, M, d_cost, d_dec);
-    return launch_fill(tb, (hipStream_t)stream) == hipSuccess ? ROTOR_OK : ROTOR_EDEVICE;
+    const Work w = work_view(d_work, n_chains, L, tb.pitch);
+    return launch_fill(tb, w, (hipStream_t)stream) == hipSuccess ? ROTOR_OK : ROTOR_EDEVICE;
 }
 
 int32_t rotor_solve_timed(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
-                          int16_t *d_dec, void *stream, rotor_kernel_stats *stats)
+                          int16_t *d_dec, void *d_work, uint64_t work_bytes, void *stream,
+                          rotor_kernel_stats *stats)
 {
-    if (!stats || !solve_args_ok(d_params, n_chains, L, M, d_cost, d_dec))
+    if (!stats || !solve_args_ok(d_params, n_chains, L, M, d_cost, d_dec, d_work, work_bytes))
         return ROTOR_EINVAL;
     const Tables tb = make_tables(d_params, n_chains, L, M, d_cost, d_dec);
+    const Work w = work_view(d_work, n_chains, L, tb.pitch);
     TimingObserver obs(stats);
-    hipError_t e = launch_fill(tb, (hipStream_t)stream, &obs);
+    hipError_t e = launch_fill(tb, w, (hipStream_t)stream, &obs);
     const hipError_t f = obs.finish((hipStream_t)stream);
     return (e == hipSuccess && f == hipSuccess) ? ROTOR_OK : ROTOR_EDEVICE;
 }

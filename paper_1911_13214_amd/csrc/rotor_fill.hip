@@ -7,18 +7,21 @@
 //                          Y(k, t) = C(k+1, t, m - w_a^k),
 // a min-plus product over k, batched over the budget m; option C_2 is
 // u_f^s + u_b^s + C(s+1, t, m - w_abar^s).  Every term lies on a strictly
-// shorter sub-chain.
+// shorter sub-chain.  Ties go to the smallest s', then to C_1 over C_2.
 //
-// Keys.  A candidate is carried as one unsigned 64-bit key
-//     (value << 16) | s'
-// so one unsigned min keeps the smallest value and, among equal values, the
-// smallest split s' -- the tie rule of the decision table.  C_2 is keyed with
-// the low field 0xFFFF, above every split, so C_1 wins ties against it.
-// Finite costs are below 2^44 (the domain), a value is a prefix sum plus two
-// costs (< 2^46), so finite keys are below 2^62.  A loaded cost is shifted
-// into place and the high word of the shifted value clamped to 2^30: finite
-// costs are unchanged and INT64_MAX becomes just above 2^62, so any key with
-// an infinite operand is at least 2^62 and a sum of two keys never wraps.
+// Two value paths, chosen per chain by prep_kernel:
+//  - narrow, when L sum(u_f) + sum(u_b) < 2^30: every finite candidate is the
+//    time of a valid schedule, hence below 2^30, so operands are read from a
+//    compact uint32 copy of the table (INT64_MAX stored as 0xFFFFFFFF) and
+//    added with unsigned saturation; the best value and its split are kept
+//    side by side and splits are visited in increasing s' with a strict <;
+//  - wide, otherwise: operands are the int64 cells and a candidate is one
+//    64-bit key (value << 16) | s', so one unsigned min keeps the smallest
+//    value and, among equal values, the smallest split.  Finite values are
+//    below 2^46 (domain bound 2^44 on costs); a loaded cost is shifted into
+//    place with its high word clamped to 2^30, so INT64_MAX lands just above
+//    2^62 and a sum of two keys never wraps.
+// C_2 is given the split field 0xFFFF (above every split), so C_1 wins ties.
 //
 // Schedule.  The triangle of pairs is cut into 16 x 16 blocks (I, J) of stage
 // ranges S_I x S_J.  Diagonal blocks (I, I) are filled diagonal by diagonal
@@ -39,12 +42,11 @@ namespace rotor {
 namespace {
 
 constexpr int64_t kInf = INT64_MAX;
-constexpr int kT = 16;    // block side, in stages
-constexpr int kSub = 8;   // per-wave register tile side
-constexpr uint64_t kKeyInf = 1ull << 62;   // keys at or above this are infinite
-constexpr uint64_t kShiftedOut = 1ull << 62;  // Y key of a budget shifted below 0
-constexpr uint32_t kHiClamp = 1u << 30;
-constexpr uint64_t kAllLow = 0xFFFF;       // low field of a C_2 key
+constexpr int kT = 16;   // block side, in stages
+constexpr int kSub = 8;  // per-wave register tile side
+constexpr uint32_t kAllSplit = 0xFFFF;  // split field of a C_2 candidate
+constexpr uint32_t kInf32 = 0xFFFFFFFFu;
+constexpr uint64_t kNarrowBound = 1ull << 30;
 
 struct ChainRows {
     const int64_t *uf, *ub, *wa, *wabar, *of, *ob;  // stage l at index l-1
@@ -57,69 +59,207 @@ __device__ inline ChainRows chain_rows(const int64_t *__restrict__ params, int L
             p + ROTOR_ROW_WABAR * L, p + ROTOR_ROW_OF * L, p + ROTOR_ROW_OB * L};
 }
 
-// A stored cost shifted into the value field of a key: finite costs (< 2^44)
-// become cost << 16, INT64_MAX (whose shift fills the high word) has its high
-// word clamped to 2^30, i.e. becomes at least 2^62.
-__device__ inline uint64_t key_of(int64_t v)
-{
-    const uint64_t t = (uint64_t)v << 16;
-    const uint32_t hi = min((uint32_t)(t >> 32), kHiClamp);
-    return ((uint64_t)hi << 32) | (uint32_t)t;
-}
-
-typedef const __attribute__((address_space(1))) int64_t *global_cptr;
+typedef const __attribute__((address_space(1))) int64_t *global_c64;
+typedef const __attribute__((address_space(1))) uint32_t *global_c32;
 
 // Load budget m of a table row: global address space, 32-bit byte offset
 // (M < 2^28).
-__device__ inline int64_t load_at(const int64_t *row, int m)
+__device__ inline int64_t load64(const int64_t *row, int m)
 {
-    return *(global_cptr)((const char *)row + (uint32_t)m * 8u);
+    return *(global_c64)((const char *)row + (uint32_t)m * 8u);
+}
+__device__ inline uint32_t load32(const uint32_t *row, int m)
+{
+    return *(global_c32)((const char *)row + (uint32_t)m * 4u);
 }
 
-// m_all(s, t): peak of F_all^s with delta^t stored, and of B^s with delta^s
-// stored (Section 4.2; delta has the size of a).
-__device__ inline int64_t gate_all(const ChainRows &r, int s, int t)
-{
-    int64_t fwd = r.wa[t - 1] + r.wabar[s - 1] + r.of[s - 1];
-    int64_t bwd = r.wa[s - 1] + r.wabar[s - 1] + r.ob[s - 1];
-    return fwd > bwd ? fwd : bwd;
-}
-
-// The j-term of m_none(s, t) for one j in (s, t): F_none^j with a^{j-1} and
-// delta^t stored.
-__device__ inline int64_t none_term(const ChainRows &r, int j)
-{
-    return r.wa[j - 2] + r.wa[j - 1] + r.of[j - 1];
-}
-
-// m_none(s, t), t > s, given the max of the j-terms over s < j < t (0 when
-// the range is empty): peak of F_ck^s and F_none^{s+1..t-1} with delta^t
-// stored (Section 4.2).
-__device__ inline int64_t gate_none(const ChainRows &r, int s, int t, int64_t jmax)
-{
-    const int64_t first = r.wa[s - 1] + r.of[s - 1];
-    return r.wa[t - 1] + (first > jmax ? first : jmax);
-}
-
+__device__ inline uint32_t sat_add(uint32_t a, uint32_t b) { return __builtin_elementwise_add_sat(a, b); }
 __device__ inline uint64_t umin(uint64_t a, uint64_t b) { return b < a ? b : a; }
 
-// Final value and decision of a cell from its best key.
-__device__ inline void store_cell(int64_t *cost, int16_t *dec, int64_t idx, uint64_t best)
+// Per-chain views of the workspace.
+struct ChainWork {
+    const int64_t *pre;    // [L+1] prefix sums of u_f
+    const int32_t *gnone;  // [rows] m_none(s, t), t > s
+    const int32_t *gall;   // [rows] m_all(s, t)
+    uint32_t *shadow;      // [rows][pitch] compact copy of the costs
+    bool narrow;
+};
+
+__device__ inline ChainWork chain_work(const Work &w, int L, int64_t rows, int64_t pitch, int c)
 {
-    if (best >= kKeyInf) {
+    ChainWork cw;
+    cw.pre = w.pre + (int64_t)c * (L + 1);
+    cw.gnone = w.gnone + (int64_t)c * rows;
+    cw.gall = w.gall + (int64_t)c * rows;
+    cw.shadow = w.shadow + (int64_t)c * rows * pitch;
+    cw.narrow = w.flags[c] != 0;
+    return cw;
+}
+
+// ---------------------------------------------------------------------------
+// Value paths.  X is the left operand with its u_f prefix, Y the shifted
+// right operand; relax() folds one candidate into an accumulator.
+
+// A stored cost shifted into the value field of a wide key.
+__device__ inline uint64_t key_of(int64_t v)
+{
+    const uint64_t t = (uint64_t)v << 16;
+    const uint32_t hi = min((uint32_t)(t >> 32), 1u << 30);
+    return ((uint64_t)hi << 32) | (uint32_t)t;
+}
+
+struct Wide {
+    typedef int64_t Raw;
+    typedef uint64_t X;
+    typedef uint64_t Y;
+    struct Acc {
+        uint64_t key;
+    };
+    static constexpr bool kShadow = false;
+    static constexpr uint64_t kShiftedOut = 1ull << 62;
+    __device__ static Raw load(const int64_t *crow, const uint32_t *, int m) { return load64(crow, m); }
+    __device__ static void init(Acc &a) { a.key = ~0ull; }
+    // ok = false: the budget of Y was shifted below 0, the candidate is infinite
+    __device__ static X xop(Raw x, uint64_t prefix, uint32_t sp, bool ok)
+    {
+        return key_of(x) + (ok ? ((prefix << 16) | sp) : kShiftedOut);
+    }
+    __device__ static Y yop(Raw y) { return key_of(y); }
+    __device__ static void relax(Acc &a, X x, Y y, uint32_t) { a.key = umin(a.key, x + y); }
+    // the stored middle partial counts u_f from the first middle split on
+    __device__ static void merge_stored(Acc &a, int64_t stored, uint64_t prefix)
+    {
+        a.key = umin(a.key, (uint64_t)stored + (prefix << 16));
+    }
+    __device__ static void relax_all(Acc &a, Raw y, uint64_t ufub)
+    {
+        a.key = umin(a.key, key_of(y) + ((ufub << 16) | kAllSplit));
+    }
+    __device__ static int64_t stored(const Acc &a) { return (int64_t)a.key; }
+    __device__ static bool finite(const Acc &a) { return a.key < (1ull << 62); }
+    __device__ static int64_t value(const Acc &a) { return (int64_t)(a.key >> 16); }
+    __device__ static uint32_t split(const Acc &a) { return (uint32_t)(a.key & 0xFFFF); }
+};
+
+struct Narrow {
+    typedef uint32_t Raw;
+    typedef uint32_t X;
+    typedef uint32_t Y;
+    struct Acc {
+        uint32_t val;
+        uint32_t sp;
+    };
+    static constexpr bool kShadow = true;
+    __device__ static Raw load(const int64_t *, const uint32_t *srow, int m) { return load32(srow, m); }
+    __device__ static void init(Acc &a)
+    {
+        a.val = kInf32;
+        a.sp = 0;
+    }
+    __device__ static X xop(Raw x, uint64_t prefix, uint32_t, bool ok)
+    {
+        return sat_add(x, ok ? (uint32_t)prefix : kInf32);
+    }
+    __device__ static Y yop(Raw y) { return y; }
+    // splits are visited in increasing s': a strict < keeps the smallest
+    __device__ static void relax(Acc &a, X x, Y y, uint32_t sp)
+    {
+        const uint32_t v = sat_add(x, y);
+        const bool b = v < a.val;
+        a.val = b ? v : a.val;
+        a.sp = b ? sp : a.sp;
+    }
+    __device__ static void merge_stored(Acc &a, int64_t stored, uint64_t prefix)
+    {
+        const uint32_t v = sat_add((uint32_t)((uint64_t)stored >> 32), (uint32_t)prefix);
+        const bool b = v < a.val;
+        a.val = b ? v : a.val;
+        a.sp = b ? (uint32_t)stored : a.sp;
+    }
+    __device__ static void relax_all(Acc &a, Raw y, uint64_t ufub)
+    {
+        const uint32_t v = sat_add(y, (uint32_t)ufub);
+        const bool b = v < a.val;
+        a.val = b ? v : a.val;
+        a.sp = b ? kAllSplit : a.sp;
+    }
+    __device__ static int64_t stored(const Acc &a) { return (int64_t)(((uint64_t)a.val << 32) | a.sp); }
+    __device__ static bool finite(const Acc &a) { return a.val != kInf32; }
+    __device__ static int64_t value(const Acc &a) { return (int64_t)a.val; }
+    __device__ static uint32_t split(const Acc &a) { return a.sp; }
+};
+
+// Final cost and decision of a cell, and its compact copy on the narrow path.
+// idx is relative to the chain's tables.
+template <class P>
+__device__ inline void store_cell(int64_t *cost, int16_t *dec, uint32_t *shadow, int64_t idx,
+                                  const typename P::Acc &a)
+{
+    if (P::finite(a)) {
+        const uint32_t sp = P::split(a);
+        cost[idx] = P::value(a);
+        dec[idx] = sp == kAllSplit ? (int16_t)0 : (int16_t)sp;
+        if (P::kShadow)
+            shadow[idx] = (uint32_t)P::value(a);
+    } else {
         cost[idx] = kInf;
         dec[idx] = -1;
-    } else {
-        const uint32_t low = (uint32_t)(best & 0xFFFF);
-        cost[idx] = (int64_t)(best >> 16);
-        dec[idx] = low == kAllLow ? (int16_t)0 : (int16_t)low;
+        if (P::kShadow)
+            shadow[idx] = kInf32;
+    }
+}
+
+// ---------------------------------------------------------------------------
+
+// Gates, prefix sums and the value path of every chain.  One thread per s
+// writes the row s of both gate tables: m_all(s, t) (peak of F_all^s with
+// delta^t stored, and of B^s with delta^s stored) and m_none(s, t) (peak of
+// F_ck^s and F_none^{s+1..t-1} with delta^t stored), Section 4.2; delta has
+// the size of a.  Gates above INT32_MAX are clamped: any gate above M < 2^28
+// is never met.
+__global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ params, int L, int64_t rows,
+                                                  Work w)
+{
+    const int c = blockIdx.y;
+    const int s = blockIdx.x * 64 + threadIdx.x + 1;
+    const ChainRows r = chain_rows(params, L, c);
+    auto clamp32 = [](int64_t v) { return (int32_t)(v < INT32_MAX ? v : INT32_MAX); };
+    if (s <= L) {
+        int32_t *gn = w.gnone + (int64_t)c * rows;
+        int32_t *ga = w.gall + (int64_t)c * rows;
+        const int64_t first = r.wa[s - 1] + r.of[s - 1];
+        const int64_t bwd = r.wa[s - 1] + r.wabar[s - 1] + r.ob[s - 1];
+        int64_t jmax = 0;  // max over s < j < t of w_a^{j-1} + w_a^j + o_f^j
+        for (int t = s; t <= L; ++t) {
+            const int64_t row = row_of(L, s, t);
+            const int64_t fwd = r.wa[t - 1] + r.wabar[s - 1] + r.of[s - 1];
+            ga[row] = clamp32(fwd > bwd ? fwd : bwd);
+            if (t >= s + 2) {
+                const int64_t v = r.wa[t - 3] + r.wa[t - 2] + r.of[t - 2];  // j = t - 1
+                jmax = v > jmax ? v : jmax;
+            }
+            gn[row] = t > s ? clamp32(r.wa[t - 1] + (first > jmax ? first : jmax)) : 0;
+        }
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        int64_t *pre = w.pre + (int64_t)c * (L + 1);
+        uint64_t acc = 0, sub = 0;
+        pre[0] = 0;
+        for (int l = 1; l <= L; ++l) {
+            acc += (uint64_t)r.uf[l - 1];
+            sub += (uint64_t)r.ub[l - 1];
+            pre[l] = (int64_t)acc;
+        }
+        // a bound on every finite cost: no forward runs more than L times
+        const unsigned __int128 bound = (unsigned __int128)acc * (unsigned)L + sub;
+        w.flags[c] = bound < kNarrowBound ? 1 : 0;
     }
 }
 
 // Eq. (DP:Init): single-stage sub-chains.
 __global__ __launch_bounds__(256) void leaf_kernel(const int64_t *__restrict__ params, int L, int M,
                                                    int64_t pitch, int64_t rows, int64_t *__restrict__ cost,
-                                                   int16_t *__restrict__ dec)
+                                                   int16_t *__restrict__ dec, Work w)
 {
     const int c = blockIdx.z;
     const int s = blockIdx.y + 1;
@@ -127,181 +267,175 @@ __global__ __launch_bounds__(256) void leaf_kernel(const int64_t *__restrict__ p
     if (m > M)
         return;
     const ChainRows r = chain_rows(params, L, c);
-    const bool ok = m >= gate_all(r, s, s);
-    const int64_t idx = ((int64_t)c * rows + row_of(L, s, s)) * pitch + m;
-    cost[idx] = ok ? r.uf[s - 1] + r.ub[s - 1] : kInf;
-    dec[idx] = ok ? 0 : -1;
+    const ChainWork cw = chain_work(w, L, rows, pitch, c);
+    const int64_t row = row_of(L, s, s);
+    const bool ok = m >= cw.gall[row];
+    const int64_t idx = row * pitch + m;
+    const int64_t v = r.uf[s - 1] + r.ub[s - 1];
+    cost[(int64_t)c * rows * pitch + idx] = ok ? v : kInf;
+    dec[(int64_t)c * rows * pitch + idx] = ok ? 0 : -1;
+    if (cw.narrow)
+        cw.shadow[idx] = ok ? (uint32_t)v : kInf32;
 }
 
-// Eq. (DP:mainrec) for the pairs (s, s + d) of one diagonal, all splits in
-// one pass; with `in_block` only pairs inside one diagonal block are done.
+// Eq. (DP:mainrec) for the pairs (s, s + d) inside one diagonal block, all
+// splits in one pass.  Rows (s, s'-1) are consecutive; the row of (s'+1, t)
+// is L - s' rows after the row of (s', t).
+template <class P>
+__device__ inline void diag_body(const ChainRows &r, const ChainWork &cw, int L, int m, int64_t pitch, int s,
+                                 int t, int64_t *tab, int16_t *dtab)
+{
+    const int64_t cell = row_of(L, s, t);
+    typename P::Acc acc;
+    P::init(acc);
+    uint64_t prefix = 0;
+    int64_t left = row_of(L, s, s) * pitch;
+    int64_t right = row_of(L, s + 1, t) * pitch;
+    for (int sp = s + 1; sp <= t; ++sp) {
+        prefix += (uint64_t)r.uf[sp - 2];
+        const int ri = m - (int)r.wa[sp - 2];
+        const typename P::X x = P::xop(P::load(tab + left, cw.shadow + left, m), prefix, (uint32_t)sp, ri >= 0);
+        const typename P::Y y = P::yop(P::load(tab + right, cw.shadow + right, ri >= 0 ? ri : 0));
+        P::relax(acc, x, y, (uint32_t)sp);
+        left += pitch;
+        right += (int64_t)(L - sp) * pitch;
+    }
+    if (m < cw.gnone[cell])
+        P::init(acc);
+    if (m >= cw.gall[cell]) {
+        const int ri = m - (int)r.wabar[s - 1];
+        if (ri >= 0) {
+            const int64_t below = row_of(L, s + 1, t) * pitch;
+            P::relax_all(acc, P::load(tab + below, cw.shadow + below, ri), (uint64_t)(r.uf[s - 1] + r.ub[s - 1]));
+        }
+    }
+    store_cell<P>(tab, dtab, cw.shadow, cell * pitch + m, acc);
+}
+
 __global__ __launch_bounds__(256) void diag_kernel(const int64_t *__restrict__ params, int L, int M,
-                                                   int64_t pitch, int64_t rows, int d, int in_block,
-                                                   int64_t *__restrict__ cost, int16_t *__restrict__ dec)
+                                                   int64_t pitch, int64_t rows, int d, int64_t *__restrict__ cost,
+                                                   int16_t *__restrict__ dec, Work w)
 {
     const int c = blockIdx.z;
     const int s = blockIdx.y + 1;
     const int t = s + d;
-    if (in_block && (s - 1) / kT != (t - 1) / kT)
+    if ((s - 1) / kT != (t - 1) / kT)
         return;
     const int m = blockIdx.x * 256 + threadIdx.x;
-    const ChainRows r = chain_rows(params, L, c);
-    int64_t jmax = 0;
-    for (int j = s + 1; j < t; ++j) {
-        const int64_t v = none_term(r, j);
-        jmax = v > jmax ? v : jmax;
-    }
-    const int64_t g1 = gate_none(r, s, t, jmax);
-    const int64_t g2 = gate_all(r, s, t);
     if (m > M)
         return;
-    const int64_t *tab = cost + (int64_t)c * rows * pitch;
-
-    // C_1, splits in increasing s'; rows (s, s'-1) are consecutive, the row of
-    // (s'+1, t) is L - s' rows after the row of (s', t).
-    uint64_t best = ~0ull;
-    uint64_t prefix = 0;
-    const int64_t *left = tab + row_of(L, s, s) * pitch;
-    const int64_t *right = tab + row_of(L, s + 1, t) * pitch;
-#pragma unroll 4
-    for (int sp = s + 1; sp <= t; ++sp) {
-        prefix += (uint64_t)r.uf[sp - 2];
-        const int64_t w = r.wa[sp - 2];
-        const int ri = m - (int)w;
-        const uint64_t x = key_of(load_at(left, m)) + (ri >= 0 ? ((prefix << 16) | (uint64_t)sp) : kShiftedOut);
-        const uint64_t y = key_of(load_at(right, ri >= 0 ? ri : 0));
-        best = umin(best, x + y);
-        left += pitch;
-        right += (int64_t)(L - sp) * pitch;
-    }
-    if (m < g1)
-        best = ~0ull;
-    if (m >= g2) {
-        const int ri = m - (int)r.wabar[s - 1];
-        if (ri >= 0) {
-            const uint64_t v = key_of(load_at(tab + row_of(L, s + 1, t) * pitch, ri));
-            best = umin(best, v + (((uint64_t)(r.uf[s - 1] + r.ub[s - 1]) << 16) | kAllLow));
-        }
-    }
-    const int64_t idx = ((int64_t)c * rows + row_of(L, s, t)) * pitch + m;
-    store_cell(cost, dec, idx, best);
+    const ChainRows r = chain_rows(params, L, c);
+    const ChainWork cw = chain_work(w, L, rows, pitch, c);
+    int64_t *tab = cost + (int64_t)c * rows * pitch;
+    int16_t *dtab = dec + (int64_t)c * rows * pitch;
+    if (cw.narrow)
+        diag_body<Narrow>(r, cw, L, m, pitch, s, t, tab, dtab);
+    else
+        diag_body<Wide>(r, cw, L, m, pitch, s, t, tab, dtab);
 }
 
 // Middle splits of every block (I, I + D) of one block-diagonal.  A workgroup
 // is one block at 64 budgets; its four waves hold the four 8 x 8 quarters of
-// the block, one key per pair and lane.  For each middle split k the wave
-// loads X for its 8 rows and Y for its 8 columns (the waves sharing rows or
-// columns hit the same lines in L1/L2) and updates 64 keys; two register sets
+// the block, one accumulator per pair and lane.  For each middle split k the
+// wave loads X for its 8 rows and Y for its 8 columns (the waves sharing rows
+// or columns meet in L1/L2) and relaxes 64 accumulators; two register sets
 // alternate so the loads of split k+1 are in flight during the updates of k.
 // The prefix of u_f starts at the first middle split; edge_kernel adds the
-// part from s.  Keys are stored in the cost table, where edge_kernel finishes
-// the cells.
+// part from s.  Partials are stored in the cost table, where edge_kernel
+// finishes the cells.
+template <class P>
 struct MiddleTile {
-    const int64_t *xrow[kSub];  // row (s0 + i, k)
-    const int64_t *yrow;        // row (k + 1, t0)
-    int64_t ystep[kSub];        // row of (k + 1, t0 + j) relative to yrow
+    int64_t xrow[kSub];  // element offset of row (s0 + i, k)
+    int64_t yrow;        // element offset of row (k + 1, t0)
+    int64_t ystep[kSub]; // row of (k + 1, t0 + j) relative to yrow, in elements
+    const int64_t *tab;
+    const uint32_t *shadow;
     int mc;
-};
 
-__device__ inline void middle_load(const MiddleTile &tl, int ri, int64_t (&rx)[kSub], int64_t (&ry)[kSub])
-{
-#pragma unroll
-    for (int i = 0; i < kSub; ++i)
-        rx[i] = load_at(tl.xrow[i], tl.mc);
-#pragma unroll
-    for (int j = 0; j < kSub; ++j)
-        ry[j] = load_at(tl.yrow + tl.ystep[j], ri >= 0 ? ri : 0);
-}
-
-__device__ inline void middle_update(uint64_t (&key)[kSub][kSub], const int64_t (&rx)[kSub],
-                                     const int64_t (&ry)[kSub], uint64_t pk)
-{
-    uint64_t x[kSub], y[kSub];
-#pragma unroll
-    for (int i = 0; i < kSub; ++i)
-        x[i] = key_of(rx[i]) + pk;
-#pragma unroll
-    for (int j = 0; j < kSub; ++j)
-        y[j] = key_of(ry[j]);
-#pragma unroll
-    for (int i = 0; i < kSub; ++i)
-#pragma unroll
-        for (int j = 0; j < kSub; ++j)
-            key[i][j] = umin(key[i][j], x[i] + y[j]);
-}
-
-__global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__ params, int L, int M,
-                                                     int64_t pitch, int64_t rows, int delta,
-                                                     int64_t *__restrict__ cost)
-{
-    const int c = blockIdx.z;
-    const int I = blockIdx.y;
-    const int J = I + delta;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int lane = threadIdx.x & 63;
-    const int m = blockIdx.x * 64 + lane;
-    const int s0 = I * kT + (wave >> 1) * kSub + 1;
-    const int t0 = J * kT + (wave & 1) * kSub + 1;
-    if (t0 > L)
-        return;
-    const int nt = min(kSub, L - t0 + 1);
-    const ChainRows r = chain_rows(params, L, c);
-    int64_t *tab = cost + (int64_t)c * rows * pitch;
-    const int k_lo = (I + 1) * kT;
-    const int k_hi = J * kT;
-
-    // X row of (s0 + i, k) advances one row per k; Y rows of (k+1, t0 + j) are
-    // j rows after the row of (k+1, t0), which advances L - k - 1 rows per k.
-    // Columns past L (last block) read the last valid column.
-    MiddleTile tl;
-#pragma unroll
-    for (int i = 0; i < kSub; ++i)
-        tl.xrow[i] = tab + row_of(L, s0 + i, k_lo) * pitch;
-#pragma unroll
-    for (int j = 0; j < kSub; ++j)
-        tl.ystep[j] = (int64_t)(j < nt ? j : nt - 1) * pitch;
-    tl.yrow = tab + row_of(L, k_lo + 1, t0) * pitch;
-    tl.mc = m <= M ? m : M;
-    auto advance = [&](int k) {  // from split k to k + 1
+    __device__ void load(int ri, typename P::Raw (&rx)[kSub], typename P::Raw (&ry)[kSub]) const
+    {
 #pragma unroll
         for (int i = 0; i < kSub; ++i)
-            tl.xrow[i] += pitch;
-        tl.yrow += (int64_t)(L - k - 1) * pitch;
-    };
+            rx[i] = P::load(tab + xrow[i], shadow + xrow[i], mc);
+        const int yi = ri >= 0 ? ri : 0;
+#pragma unroll
+        for (int j = 0; j < kSub; ++j)
+            ry[j] = P::load(tab + yrow + ystep[j], shadow + yrow + ystep[j], yi);
+    }
+    __device__ void advance(int L, int k, int64_t pitch)  // from split k to k + 1
+    {
+#pragma unroll
+        for (int i = 0; i < kSub; ++i)
+            xrow[i] += pitch;
+        yrow += (int64_t)(L - k - 1) * pitch;
+    }
+};
 
-    uint64_t key[kSub][kSub];
+template <class P>
+__device__ inline void middle_update(typename P::Acc (&acc)[kSub][kSub], const typename P::Raw (&rx)[kSub],
+                                     const typename P::Raw (&ry)[kSub], uint64_t prefix, uint32_t sp, bool ok)
+{
+    typename P::X x[kSub];
+    typename P::Y y[kSub];
+#pragma unroll
+    for (int i = 0; i < kSub; ++i)
+        x[i] = P::xop(rx[i], prefix, sp, ok);
+#pragma unroll
+    for (int j = 0; j < kSub; ++j)
+        y[j] = P::yop(ry[j]);
 #pragma unroll
     for (int i = 0; i < kSub; ++i)
 #pragma unroll
         for (int j = 0; j < kSub; ++j)
-            key[i][j] = ~0ull;
+            P::relax(acc[i][j], x[i], y[j], sp);
+}
 
-    // a budget shifted below 0 makes every candidate of the split infinite:
-    // it is folded into the constant added to X
+template <class P>
+__device__ inline void middle_body(const ChainRows &r, const ChainWork &cw, int L, int M, int m, int64_t pitch,
+                                   int s0, int t0, int nt, int k_lo, int k_hi, int64_t *tab)
+{
+    MiddleTile<P> tl;
+#pragma unroll
+    for (int i = 0; i < kSub; ++i)
+        tl.xrow[i] = row_of(L, s0 + i, k_lo) * pitch;
+#pragma unroll
+    for (int j = 0; j < kSub; ++j)
+        tl.ystep[j] = (int64_t)(j < nt ? j : nt - 1) * pitch;  // columns past L read the last one
+    tl.yrow = row_of(L, k_lo + 1, t0) * pitch;
+    tl.tab = tab;
+    tl.shadow = cw.shadow;
+    tl.mc = m <= M ? m : M;
+
+    typename P::Acc acc[kSub][kSub];
+#pragma unroll
+    for (int i = 0; i < kSub; ++i)
+#pragma unroll
+        for (int j = 0; j < kSub; ++j)
+            P::init(acc[i][j]);
+
     uint64_t prefix = 0;
-    auto pk_of = [&](int k, int ri) {
-        prefix += (uint64_t)r.uf[k - 1];
-        return ri >= 0 ? ((prefix << 16) | (uint64_t)(k + 1)) : kShiftedOut;
-    };
-    int64_t ax[kSub], ay[kSub], bx[kSub], by[kSub];
+    typename P::Raw ax[kSub], ay[kSub], bx[kSub], by[kSub];
     int k = k_lo;
     int ra = tl.mc - (int)r.wa[k - 1];
-    middle_load(tl, ra, ax, ay);
+    tl.load(ra, ax, ay);
     for (; k + 1 <= k_hi; k += 2) {
-        advance(k);
+        tl.advance(L, k, pitch);
         const int rb = tl.mc - (int)r.wa[k];
-        middle_load(tl, rb, bx, by);
-        middle_update(key, ax, ay, pk_of(k, ra));
+        tl.load(rb, bx, by);
+        prefix += (uint64_t)r.uf[k - 1];
+        middle_update<P>(acc, ax, ay, prefix, (uint32_t)(k + 1), ra >= 0);
         if (k + 2 <= k_hi) {
-            advance(k + 1);
+            tl.advance(L, k + 1, pitch);
             ra = tl.mc - (int)r.wa[k + 1];
-            middle_load(tl, ra, ax, ay);
+            tl.load(ra, ax, ay);
         }
-        middle_update(key, bx, by, pk_of(k + 1, rb));
+        prefix += (uint64_t)r.uf[k];
+        middle_update<P>(acc, bx, by, prefix, (uint32_t)(k + 2), rb >= 0);
     }
-    if (k == k_hi)
-        middle_update(key, ax, ay, pk_of(k, ra));
-
+    if (k == k_hi) {
+        prefix += (uint64_t)r.uf[k - 1];
+        middle_update<P>(acc, ax, ay, prefix, (uint32_t)(k + 1), ra >= 0);
+    }
     if (m > M)
         return;
 #pragma unroll
@@ -309,109 +443,108 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
 #pragma unroll
         for (int j = 0; j < kSub; ++j)
             if (j < nt)
-                tab[row_of(L, s0 + i, t0 + j) * pitch + m] = (int64_t)key[i][j];
+                tab[row_of(L, s0 + i, t0 + j) * pitch + m] = P::stored(acc[i][j]);
 }
 
-// Sum (uf over [k_lo, k_hi]) and max (m_none j-terms over (s, t)) across
-// the workgroup.
-__device__ inline void block_reduce(uint64_t &sum, int64_t &mx)
+__global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__ params, int L, int M,
+                                                     int64_t pitch, int64_t rows, int delta,
+                                                     int64_t *__restrict__ cost, Work w)
 {
-    __shared__ uint64_t s_sum[4];
-    __shared__ int64_t s_max[4];
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        sum += (uint64_t)__shfl_xor((long long)sum, off);
-        const int64_t o = (int64_t)__shfl_xor((long long)mx, off);
-        mx = o > mx ? o : mx;
-    }
-    const int wave = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0) {
-        s_sum[wave] = sum;
-        s_max[wave] = mx;
-    }
-    __syncthreads();
-    sum = s_sum[0] + s_sum[1] + s_sum[2] + s_sum[3];
-    mx = s_max[0];
-#pragma unroll
-    for (int w = 1; w < 4; ++w)
-        mx = s_max[w] > mx ? s_max[w] : mx;
+    const int c = blockIdx.z;
+    const int I = blockIdx.y;
+    const int J = I + delta;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int m = blockIdx.x * 64 + (threadIdx.x & 63);
+    const int s0 = I * kT + (wave >> 1) * kSub + 1;
+    const int t0 = J * kT + (wave & 1) * kSub + 1;
+    if (t0 > L)
+        return;
+    const int nt = min(kSub, L - t0 + 1);
+    const ChainRows r = chain_rows(params, L, c);
+    const ChainWork cw = chain_work(w, L, rows, pitch, c);
+    int64_t *tab = cost + (int64_t)c * rows * pitch;
+    const int k_lo = (I + 1) * kT;
+    const int k_hi = J * kT;
+    if (cw.narrow)
+        middle_body<Narrow>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, tab);
+    else
+        middle_body<Wide>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, tab);
 }
 
 // Edge splits, C_2 and the gates for the cells a + b = q of every block
 // (I, I + D) of one block-diagonal; a workgroup is one cell at 256 budgets.
+// Splits are met in increasing order: low, then the stored middle partial,
+// then high.
+template <class P>
+__device__ inline void edge_body(const ChainRows &r, const ChainWork &cw, int L, int m, int64_t pitch, int s,
+                                 int t, int k_lo, int k_hi, int64_t *tab, int16_t *dtab)
+{
+    const int64_t cell = row_of(L, s, t);
+    typename P::Acc acc;
+    P::init(acc);
+    // low splits k = s .. k_lo - 1: X from block (I, I), Y from this block
+    uint64_t prefix = 0;
+    int64_t xr = row_of(L, s, s) * pitch;
+    int64_t yr = row_of(L, s + 1, t) * pitch;
+    for (int k = s; k < k_lo; ++k) {
+        prefix += (uint64_t)r.uf[k - 1];
+        const int ri = m - (int)r.wa[k - 1];
+        const typename P::X x = P::xop(P::load(tab + xr, cw.shadow + xr, m), prefix, (uint32_t)(k + 1), ri >= 0);
+        const typename P::Y y = P::yop(P::load(tab + yr, cw.shadow + yr, ri >= 0 ? ri : 0));
+        P::relax(acc, x, y, (uint32_t)(k + 1));
+        xr += pitch;
+        yr += (int64_t)(L - k - 1) * pitch;
+    }
+    // middle splits: the stored partial counts u_f from k_lo on
+    P::merge_stored(acc, load64(tab + cell * pitch, m), prefix);
+    // high splits k = 16J + 1 .. t - 1: X from this block, Y from block (J, J)
+    prefix += (uint64_t)(cw.pre[k_hi] - cw.pre[k_lo - 1]);
+    xr = row_of(L, s, k_hi + 1) * pitch;
+    yr = (k_hi + 2 <= t ? row_of(L, k_hi + 2, t) : 0) * pitch;
+    for (int k = k_hi + 1; k < t; ++k) {
+        prefix += (uint64_t)r.uf[k - 1];
+        const int ri = m - (int)r.wa[k - 1];
+        const typename P::X x = P::xop(P::load(tab + xr, cw.shadow + xr, m), prefix, (uint32_t)(k + 1), ri >= 0);
+        const typename P::Y y = P::yop(P::load(tab + yr, cw.shadow + yr, ri >= 0 ? ri : 0));
+        P::relax(acc, x, y, (uint32_t)(k + 1));
+        xr += pitch;
+        yr += (int64_t)(L - k - 1) * pitch;
+    }
+    if (m < cw.gnone[cell])
+        P::init(acc);
+    if (m >= cw.gall[cell]) {
+        const int ri = m - (int)r.wabar[s - 1];
+        if (ri >= 0) {
+            const int64_t below = row_of(L, s + 1, t) * pitch;
+            P::relax_all(acc, P::load(tab + below, cw.shadow + below, ri), (uint64_t)(r.uf[s - 1] + r.ub[s - 1]));
+        }
+    }
+    store_cell<P>(tab, dtab, cw.shadow, cell * pitch + m, acc);
+}
+
 __global__ __launch_bounds__(256) void edge_kernel(const int64_t *__restrict__ params, int L, int M,
                                                    int64_t pitch, int64_t rows, int delta, int q, int a_min,
-                                                   int n_q, int64_t *__restrict__ cost, int16_t *__restrict__ dec)
+                                                   int n_q, int64_t *__restrict__ cost, int16_t *__restrict__ dec,
+                                                   Work w)
 {
     const int c = blockIdx.z;
     const int blk = blockIdx.y / n_q;
     const int a = a_min + (blockIdx.y - blk * n_q);
-    const int b = q - a;
     const int I = blk;
     const int J = I + delta;
     const int s = (I + 1) * kT - a;
-    const int t = J * kT + 1 + b;
-    if (t > L)
-        return;  // the whole workgroup, before any barrier
-    const int k_lo = (I + 1) * kT;
-    const int k_hi = J * kT;
-    const ChainRows r = chain_rows(params, L, c);
-
-    uint64_t mid_sum = 0;  // sum of u_f over the middle splits
-    int64_t jmax = 0;      // max of the m_none j-terms over (s, t)
-    for (int j = k_lo + (int)threadIdx.x; j <= k_hi; j += 256)
-        mid_sum += (uint64_t)r.uf[j - 1];
-    for (int j = s + 1 + (int)threadIdx.x; j < t; j += 256) {
-        const int64_t v = none_term(r, j);
-        jmax = v > jmax ? v : jmax;
-    }
-    block_reduce(mid_sum, jmax);
-
+    const int t = J * kT + 1 + (q - a);
     const int m = blockIdx.x * 256 + threadIdx.x;
-    if (m > M)
+    if (t > L || m > M)
         return;
+    const ChainRows r = chain_rows(params, L, c);
+    const ChainWork cw = chain_work(w, L, rows, pitch, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
-    const int64_t cell = row_of(L, s, t) * pitch + m;
-
-    // low splits k = s .. k_lo - 1: X from block (I, I), Y from this block
-    uint64_t best = ~0ull;
-    uint64_t prefix = 0;
-    const int64_t *xr = tab + row_of(L, s, s) * pitch;
-    const int64_t *yr = tab + row_of(L, s + 1, t) * pitch;
-    for (int k = s; k < k_lo; ++k) {
-        prefix += (uint64_t)r.uf[k - 1];
-        const int ri = m - (int)r.wa[k - 1];
-        const uint64_t x = key_of(load_at(xr, m)) + (ri >= 0 ? ((prefix << 16) | (uint64_t)(k + 1)) : kShiftedOut);
-        const uint64_t y = key_of(load_at(yr, ri >= 0 ? ri : 0));
-        best = umin(best, x + y);
-        xr += pitch;
-        yr += (int64_t)(L - k - 1) * pitch;
-    }
-    // middle splits: the stored key counts u_f from k_lo on
-    best = umin(best, (uint64_t)load_at(tab + row_of(L, s, t) * pitch, m) + (prefix << 16));
-    // high splits k = 16J + 1 .. t - 1: X from this block, Y from block (J, J)
-    prefix += mid_sum;
-    xr = tab + row_of(L, s, k_hi + 1) * pitch;
-    yr = tab + row_of(L, k_hi + 2, t) * pitch;
-    for (int k = k_hi + 1; k < t; ++k) {
-        prefix += (uint64_t)r.uf[k - 1];
-        const int ri = m - (int)r.wa[k - 1];
-        const uint64_t x = key_of(load_at(xr, m)) + (ri >= 0 ? ((prefix << 16) | (uint64_t)(k + 1)) : kShiftedOut);
-        const uint64_t y = key_of(load_at(yr, ri >= 0 ? ri : 0));
-        best = umin(best, x + y);
-        xr += pitch;
-        yr += (int64_t)(L - k - 1) * pitch;
-    }
-    if (m < gate_none(r, s, t, jmax))
-        best = ~0ull;
-    if (m >= gate_all(r, s, t)) {
-        const int ri = m - (int)r.wabar[s - 1];
-        if (ri >= 0) {
-            const uint64_t v = key_of(load_at(tab + row_of(L, s + 1, t) * pitch, ri));
-            best = umin(best, v + (((uint64_t)(r.uf[s - 1] + r.ub[s - 1]) << 16) | kAllLow));
-        }
-    }
-    store_cell(tab, dec + (int64_t)c * rows * pitch, cell, best);
+    int16_t *dtab = dec + (int64_t)c * rows * pitch;
+    if (cw.narrow)
+        edge_body<Narrow>(r, cw, L, m, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
+    else
+        edge_body<Wide>(r, cw, L, m, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
 }
 
 hipError_t check() { return hipGetLastError(); }
@@ -430,7 +563,34 @@ uint64_t in_block_pairs(int L, int d)
 
 }  // namespace
 
-hipError_t launch_fill(const Tables &tb, hipStream_t stream, LaunchObserver *obs)
+WorkLayout work_layout(int n_chains, int L, int64_t pitch)
+{
+    auto align = [](uint64_t x) { return (x + 255) / 256 * 256; };
+    const uint64_t rows = (uint64_t)L * (L + 1) / 2;
+    WorkLayout wl;
+    wl.flags = 0;
+    wl.pre = align(wl.flags + 4ull * n_chains);
+    wl.gnone = align(wl.pre + 8ull * n_chains * (L + 1));
+    wl.gall = align(wl.gnone + 4ull * n_chains * rows);
+    wl.shadow = align(wl.gall + 4ull * n_chains * rows);
+    wl.total = align(wl.shadow + 4ull * n_chains * rows * (uint64_t)pitch);
+    return wl;
+}
+
+Work work_view(void *base, int n_chains, int L, int64_t pitch)
+{
+    const WorkLayout wl = work_layout(n_chains, L, pitch);
+    char *b = (char *)base;
+    Work w;
+    w.flags = (int32_t *)(b + wl.flags);
+    w.pre = (int64_t *)(b + wl.pre);
+    w.gnone = (int32_t *)(b + wl.gnone);
+    w.gall = (int32_t *)(b + wl.gall);
+    w.shadow = (uint32_t *)(b + wl.shadow);
+    return w;
+}
+
+hipError_t launch_fill(const Tables &tb, const Work &w, hipStream_t stream, LaunchObserver *obs)
 {
     const int L = tb.L;
     const uint64_t W = (uint64_t)tb.M + 1;
@@ -446,10 +606,15 @@ hipError_t launch_fill(const Tables &tb, hipStream_t stream, LaunchObserver *obs
     auto before = [&](KernelClass k) -> hipError_t { return obs ? obs->before(k, stream) : hipSuccess; };
     hipError_t e;
 
+    if ((e = before(kPrep)) != hipSuccess)
+        return e;
+    prep_kernel<<<dim3((L + 63) / 64, tb.n_chains), 64, 0, stream>>>(tb.params, L, tb.rows, w);
+    if ((e = launched(kPrep, 0, 0, 0)) != hipSuccess)
+        return e;
     if ((e = before(kLeaf)) != hipSuccess)
         return e;
     leaf_kernel<<<dim3(mb256, L, tb.n_chains), 256, 0, stream>>>(tb.params, L, tb.M, tb.pitch, tb.rows, tb.cost,
-                                                                 tb.dec);
+                                                                 tb.dec, w);
     if ((e = launched(kLeaf, 0, 0, (uint64_t)L)) != hipSuccess)
         return e;
     // diagonal blocks
@@ -457,7 +622,7 @@ hipError_t launch_fill(const Tables &tb, hipStream_t stream, LaunchObserver *obs
         if ((e = before(kDiag)) != hipSuccess)
             return e;
         diag_kernel<<<dim3(mb256, L - d, tb.n_chains), 256, 0, stream>>>(tb.params, L, tb.M, tb.pitch, tb.rows, d,
-                                                                         1, tb.cost, tb.dec);
+                                                                         tb.cost, tb.dec, w);
         const uint64_t pairs = in_block_pairs(L, d);
         if ((e = launched(kDiag, pairs * d, pairs, pairs)) != hipSuccess)
             return e;
@@ -471,7 +636,7 @@ hipError_t launch_fill(const Tables &tb, hipStream_t stream, LaunchObserver *obs
         if ((e = before(kMiddle)) != hipSuccess)
             return e;
         middle_kernel<<<dim3(mb64, nb - delta, tb.n_chains), 256, 0, stream>>>(tb.params, L, tb.M, tb.pitch,
-                                                                               tb.rows, delta, tb.cost);
+                                                                               tb.rows, delta, tb.cost, w);
         if ((e = launched(kMiddle, pairs * (uint64_t)((delta - 1) * kT + 1), 0, 0)) != hipSuccess)
             return e;
         for (int q = 0; q <= 2 * kT - 2; ++q) {
@@ -485,7 +650,7 @@ hipError_t launch_fill(const Tables &tb, hipStream_t stream, LaunchObserver *obs
             if ((e = before(kEdge)) != hipSuccess)
                 return e;
             edge_kernel<<<dim3(mb256, (nb - delta) * n_q, tb.n_chains), 256, 0, stream>>>(
-                tb.params, L, tb.M, tb.pitch, tb.rows, delta, q, a_min, n_q, tb.cost, tb.dec);
+                tb.params, L, tb.M, tb.pitch, tb.rows, delta, q, a_min, n_q, tb.cost, tb.dec, w);
             if ((e = launched(kEdge, cells * (uint64_t)q, cells, cells)) != hipSuccess)
                 return e;
         }

@@ -31,8 +31,26 @@ struct Tables {
     int64_t rows;           // L(L+1)/2
 };
 
+// Device workspace of a fill: per-chain value-path flag, prefix sums of u_f,
+// the gates m_none and m_all of every pair, and a compact uint32 copy of the
+// cost table (used by chains whose costs stay below 2^30).
+struct Work {
+    int32_t *flags;    // [n_chains]
+    int64_t *pre;      // [n_chains][L + 1]
+    int32_t *gnone;    // [n_chains][rows]
+    int32_t *gall;     // [n_chains][rows]
+    uint32_t *shadow;  // [n_chains][rows][pitch]
+};
+
+// Byte offsets of the workspace sections (each 256-byte aligned).
+struct WorkLayout {
+    uint64_t flags, pre, gnone, gall, shadow, total;
+};
+WorkLayout work_layout(int n_chains, int L, int64_t pitch);
+Work work_view(void *base, int n_chains, int L, int64_t pitch);
+
 // Kernel classes of the fill, in the order of rotor_kernel_stats.
-enum KernelClass { kLeaf = 0, kDiag = 1, kMiddle = 2, kEdge = 3 };
+enum KernelClass { kLeaf = 0, kDiag = 1, kMiddle = 2, kEdge = 3, kPrep = 4 };
 
 // Work of one launch, counted exactly from its grid: C_1 candidates (split
 // points times budgets), C_2 candidates and final cells written.
@@ -50,7 +68,7 @@ struct LaunchObserver {
 };
 
 // Enqueue the whole table fill on `stream`.  Returns a HIP error code.
-hipError_t launch_fill(const Tables &tb, hipStream_t stream, LaunchObserver *obs = nullptr);
+hipError_t launch_fill(const Tables &tb, const Work &w, hipStream_t stream, LaunchObserver *obs = nullptr);
 
 // Enqueue the sequence walk (one workgroup per budget).
 hipError_t launch_reconstruct(const int64_t *params, int L, int M, int64_t pitch, int64_t rows,

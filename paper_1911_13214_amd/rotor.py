@@ -36,12 +36,13 @@ SIGNATURES = {
     "rotor_layout": (_i32, [_i32, _i32, _i64, _P(_i64), _P(_i64), _P(_u64), _P(_u64)]),
     "rotor_row_index": (_i64, [_i32, _i32, _i32]),
     "rotor_check_params": (_i32, [_vp, _i32, _i32, _i64]),
-    "rotor_solve": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp]),
+    "rotor_workspace_bytes": (_i32, [_i32, _i32, _i64, _P(_u64)]),
+    "rotor_solve": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp, _u64, _vp]),
     "rotor_reconstruct": (_i32, [_vp, _i32, _i32, _i64, _vp, _i32, _i32, _vp, _i64, _vp, _vp, _vp, _vp]),
-    "rotor_solve_timed": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp, _vp]),
+    "rotor_solve_timed": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp, _u64, _vp, _vp]),
 }
 
-KERNEL_CLASSES = ("leaf", "diag", "middle", "edge")
+KERNEL_CLASSES = ("leaf", "diag", "middle", "edge", "prep")
 
 
 class KernelStats(ctypes.Structure):
@@ -95,6 +96,12 @@ def rotor_layout(n_chains: int, L: int, M: int):
     return pitch.value, rows.value, cb.value, db.value
 
 
+def rotor_workspace_bytes(n_chains: int, L: int, M: int) -> int:
+    b = ctypes.c_uint64()
+    _check(lib().rotor_workspace_bytes(n_chains, L, M, ctypes.byref(b)), "rotor_workspace_bytes")
+    return b.value
+
+
 def rotor_row_index(L: int, s: int, t: int) -> int:
     return lib().rotor_row_index(L, s, t)
 
@@ -124,30 +131,33 @@ def _dev_ptr(t, dtype, what):
     return t.data_ptr()
 
 
-def rotor_solve(d_params, n_chains: int, L: int, M: int, d_cost, d_dec, stream=None):
+def _solve_ptrs(d_params, n_chains, L, M, d_cost, d_dec, d_work):
+    import torch
+    _, _, cb, db = rotor_layout(n_chains, L, M)
+    if d_params.numel() < n_chains * N_ROWS * L or d_cost.numel() * 8 < cb or d_dec.numel() * 2 < db:
+        raise ValueError("buffer smaller than the layout requires")
+    if not isinstance(d_work, torch.Tensor) or not d_work.is_cuda or not d_work.is_contiguous():
+        raise ValueError("workspace must be a contiguous CUDA tensor")
+    return (_dev_ptr(d_params, torch.int64, "params"), _dev_ptr(d_cost, torch.int64, "cost"),
+            _dev_ptr(d_dec, torch.int16, "dec"), d_work.data_ptr(), d_work.numel() * d_work.element_size())
+
+
+def rotor_solve(d_params, n_chains: int, L: int, M: int, d_cost, d_dec, d_work, stream=None):
     """Enqueue the table fill (asynchronous).  ``d_params``: int64 device
     tensor [n_chains, 6, L]; ``d_cost`` / ``d_dec``: int64 / int16 device
-    tensors with at least rotor_layout's element counts."""
-    import torch
-    _, _, cb, db = rotor_layout(n_chains, L, M)
-    if d_params.numel() < n_chains * N_ROWS * L or d_cost.numel() * 8 < cb or d_dec.numel() * 2 < db:
-        raise ValueError("buffer smaller than the layout requires")
-    _check(lib().rotor_solve(_dev_ptr(d_params, torch.int64, "params"), n_chains, L, M,
-                             _dev_ptr(d_cost, torch.int64, "cost"), _dev_ptr(d_dec, torch.int16, "dec"),
-                             _stream_ptr(stream)), "rotor_solve")
+    tensors with at least rotor_layout's element counts; ``d_work``: device
+    tensor of at least rotor_workspace_bytes."""
+    p, c, d, w, wb = _solve_ptrs(d_params, n_chains, L, M, d_cost, d_dec, d_work)
+    _check(lib().rotor_solve(p, n_chains, L, M, c, d, w, wb, _stream_ptr(stream)), "rotor_solve")
 
 
-def rotor_solve_timed(d_params, n_chains: int, L: int, M: int, d_cost, d_dec, stream=None):
+def rotor_solve_timed(d_params, n_chains: int, L: int, M: int, d_cost, d_dec, d_work, stream=None):
     """rotor_solve with a per-kernel-class breakdown (synchronous).  Returns
     {class: {launches, ms, split_candidates, all_candidates, cells}}."""
-    import torch
-    _, _, cb, db = rotor_layout(n_chains, L, M)
-    if d_params.numel() < n_chains * N_ROWS * L or d_cost.numel() * 8 < cb or d_dec.numel() * 2 < db:
-        raise ValueError("buffer smaller than the layout requires")
+    p, c, d, w, wb = _solve_ptrs(d_params, n_chains, L, M, d_cost, d_dec, d_work)
     stats = (KernelStats * len(KERNEL_CLASSES))()
-    _check(lib().rotor_solve_timed(_dev_ptr(d_params, torch.int64, "params"), n_chains, L, M,
-                                   _dev_ptr(d_cost, torch.int64, "cost"), _dev_ptr(d_dec, torch.int16, "dec"),
-                                   _stream_ptr(stream), ctypes.cast(stats, ctypes.c_void_p)), "rotor_solve_timed")
+    _check(lib().rotor_solve_timed(p, n_chains, L, M, c, d, w, wb, _stream_ptr(stream),
+                                   ctypes.cast(stats, ctypes.c_void_p)), "rotor_solve_timed")
     return {name: {f: getattr(st, f) for f, _ in KernelStats._fields_} for name, st in zip(KERNEL_CLASSES, stats)}
 
 
@@ -191,16 +201,26 @@ def alloc_tables(n_chains: int, L: int, M: int, device="cuda"):
     return cost, dec
 
 
+def alloc_workspace(n_chains: int, L: int, M: int, device="cuda"):
+    """Uninitialised device workspace of rotor_workspace_bytes (int64 words)."""
+    import torch
+    return torch.empty(((rotor_workspace_bytes(n_chains, L, M) + 7) // 8,), dtype=torch.int64, device=device)
+
+
 def solve(params: np.ndarray, M: int, device="cuda", stream=None):
     """Upload, allocate and fill.  Returns (d_params, cost, dec) device
-    tensors; the fill is enqueued on ``stream``."""
+    tensors; the fill is enqueued on ``stream`` (the workspace is released to
+    torch's caching allocator on that stream)."""
     p = np.asarray(params)
     if p.ndim == 2:
         p = p[None]
     n_chains, _, L = p.shape
     d_params = upload_params(p, M, device)
     cost, dec = alloc_tables(n_chains, L, M, device)
-    rotor_solve(d_params, n_chains, L, M, cost, dec, stream)
+    work = alloc_workspace(n_chains, L, M, device)
+    rotor_solve(d_params, n_chains, L, M, cost, dec, work, stream)
+    if stream is not None:
+        work.record_stream(stream)
     return d_params, cost, dec
 
 

@@ -68,6 +68,16 @@ def test_layout_rejects_bad_sizes(args):
     assert e.value.status == rotor.ROTOR_EINVAL
 
 
+@pytest.mark.parametrize("n_chains,L,M", [(1, 1, 0), (1, 500, 5000), (256, 64, 640), (3, 7, 15)])
+def test_workspace_size(n_chains, L, M):
+    pitch, rows, cb, db = rotor.rotor_layout(n_chains, L, M)
+    ws = rotor.rotor_workspace_bytes(n_chains, L, M)
+    # a 4-byte copy of every cell plus per-pair gates and per-stage prefixes
+    assert ws >= n_chains * rows * (4 * pitch + 8) + n_chains * 8 * (L + 1)
+    assert ws <= n_chains * rows * (4 * pitch + 8) + n_chains * 8 * (L + 1) + 5 * 256 + 4 * n_chains
+    assert ws % 256 == 0
+
+
 def test_layout_rejects_byte_overflow():
     with pytest.raises(rotor.RotorError):
         rotor.rotor_layout(65535, 32767, (1 << 28) - 1)
@@ -97,13 +107,21 @@ def test_check_params():
 def test_solve_and_reconstruct_reject_bad_arguments_before_any_device_work():
     lib = rotor.lib()
     fake = ctypes.c_void_p(0x1000)
-    assert lib.rotor_solve(None, 1, 10, 100, fake, fake, None) == rotor.ROTOR_EINVAL
-    assert lib.rotor_solve(fake, 1, 10, 100, None, fake, None) == rotor.ROTOR_EINVAL
-    assert lib.rotor_solve(fake, 1, 10, 100, fake, None, None) == rotor.ROTOR_EINVAL
-    assert lib.rotor_solve(fake, 0, 10, 100, fake, fake, None) == rotor.ROTOR_EINVAL
-    assert lib.rotor_solve(fake, 1, 10, -3, fake, fake, None) == rotor.ROTOR_EINVAL
-    assert lib.rotor_solve(ctypes.c_void_p(0x1004), 1, 10, 100, fake, fake, None) == rotor.ROTOR_EINVAL
-    assert lib.rotor_solve(fake, 1, 10, 100, fake, ctypes.c_void_p(0x1001), None) == rotor.ROTOR_EINVAL
+    big = 1 << 40
+    need = rotor.rotor_workspace_bytes(1, 10, 100)
+    assert lib.rotor_solve(None, 1, 10, 100, fake, fake, fake, big, None) == rotor.ROTOR_EINVAL
+    assert lib.rotor_solve(fake, 1, 10, 100, None, fake, fake, big, None) == rotor.ROTOR_EINVAL
+    assert lib.rotor_solve(fake, 1, 10, 100, fake, None, fake, big, None) == rotor.ROTOR_EINVAL
+    assert lib.rotor_solve(fake, 1, 10, 100, fake, fake, None, big, None) == rotor.ROTOR_EINVAL
+    assert lib.rotor_solve(fake, 1, 10, 100, fake, fake, fake, need - 1, None) == rotor.ROTOR_EINVAL
+    assert lib.rotor_solve(fake, 0, 10, 100, fake, fake, fake, big, None) == rotor.ROTOR_EINVAL
+    assert lib.rotor_solve(fake, 1, 10, -3, fake, fake, fake, big, None) == rotor.ROTOR_EINVAL
+    assert lib.rotor_solve(ctypes.c_void_p(0x1004), 1, 10, 100, fake, fake, fake, big, None) == rotor.ROTOR_EINVAL
+    assert lib.rotor_solve(fake, 1, 10, 100, fake, ctypes.c_void_p(0x1001), fake, big, None) == rotor.ROTOR_EINVAL
+    assert lib.rotor_solve(fake, 1, 10, 100, fake, fake, ctypes.c_void_p(0x1004), big, None) == rotor.ROTOR_EINVAL
+    stats = (rotor.KernelStats * 5)()
+    assert lib.rotor_solve_timed(fake, 1, 10, 100, fake, fake, fake, need - 1, None,
+                                 ctypes.cast(stats, ctypes.c_void_p)) == rotor.ROTOR_EINVAL
     r = lib.rotor_reconstruct
     assert r(fake, 1, 10, 100, fake, 1, 1, fake, 10, fake, fake, fake, None) == rotor.ROTOR_EINVAL  # chain
     assert r(fake, 1, 10, 100, fake, 0, 0, fake, 10, fake, fake, fake, None) == rotor.ROTOR_EINVAL  # n_budgets

@@ -245,7 +245,7 @@ def test_timed_solve_matches_and_counts_the_work(cfg):
     params, L, M, n, _ = chaingen.config(cfg)
     d_params, cost, dec = solve_on_gpu(params, M)
     c2, d2 = rotor.alloc_tables(n, L, M)
-    stats = rotor.rotor_solve_timed(d_params, n, L, M, c2, d2)
+    stats = rotor.rotor_solve_timed(d_params, n, L, M, c2, d2, rotor.alloc_workspace(n, L, M))
     assert np.array_equal(cost[..., :M + 1].cpu().numpy(), c2[..., :M + 1].cpu().numpy())
     assert np.array_equal(dec[..., :M + 1].cpu().numpy(), d2[..., :M + 1].cpu().numpy())
     W = M + 1
@@ -253,3 +253,47 @@ def test_timed_solve_matches_and_counts_the_work(cfg):
     assert sum(s["all_candidates"] for s in stats.values()) == L * (L - 1) // 2 * W * n
     assert sum(s["cells"] for s in stats.values()) == L * (L + 1) // 2 * W * n
     assert all(s["ms"] >= 0 for s in stats.values()) and stats["leaf"]["launches"] == 1
+    assert stats["prep"]["launches"] == 1
+
+
+def wide_costs_chain(seed, L):
+    """A chain whose cost bound L sum(u_f) + sum(u_b) exceeds 2^30, so the
+    solver takes its 64-bit value path."""
+    p = chaingen.random_chains(1, L, seed=seed)
+    p[0, 0] *= 1 << 22
+    p[0, 1] *= 1 << 22
+    assert L * p[0, 0].sum() + p[0, 1].sum() >= 1 << 30
+    return p
+
+
+@pytest.mark.parametrize("L,M,seed", [(5, 60, 1), (23, 230, 2), (40, 400, 3), (70, 300, 4)])
+def test_wide_value_path(L, M, seed):
+    p = wide_costs_chain(seed, L)
+    say(f"wide L={L} M={M}")
+    _, cost, dec = solve_on_gpu(p, M)
+    assert_same(p, M, cost, dec)
+
+
+def test_batch_mixing_value_paths():
+    # chains of one call may take different value paths
+    params = chaingen.random_chains(6, 37, seed=21)
+    for c in (1, 4):
+        params[c, 0] *= 1 << 22
+        params[c, 1] *= 1 << 22
+    M = 200
+    _, cost, dec = solve_on_gpu(params, M)
+    for c in range(6):
+        assert_same(params, M, cost, dec, c)
+
+
+def test_workspace_too_small_is_rejected():
+    import torch
+    from paper_1911_13214_amd import rotor
+    params, L, M, n, _ = chaingen.config(2)
+    d_params = rotor.upload_params(params, M)
+    cost, dec = rotor.alloc_tables(n, L, M)
+    need = rotor.rotor_workspace_bytes(n, L, M)
+    small = torch.empty(need // 8 - 1, dtype=torch.int64, device="cuda")
+    with pytest.raises(rotor.RotorError) as e:
+        rotor.rotor_solve(d_params, n, L, M, cost, dec, small)
+    assert e.value.status == rotor.ROTOR_EINVAL
