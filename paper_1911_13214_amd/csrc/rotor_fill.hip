@@ -278,6 +278,38 @@ __global__ __launch_bounds__(256) void leaf_kernel(const int64_t *__restrict__ p
         cw.shadow[idx] = ok ? (uint32_t)v : kInf32;
 }
 
+// Relax the consecutive splits k = k0 .. k0 + n - 1 (n <= kT - 1, uniform)
+// of the pair (s, t): X rows (s, k) are consecutive from xrow, the Y row of
+// (k+1, t) starts at yrow and advances L - k - 1 rows per k.  All loads are
+// issued before the first relaxation so their latencies overlap.
+template <class P>
+__device__ inline void relax_run(typename P::Acc &acc, const ChainRows &r, const int64_t *tab,
+                                 const uint32_t *shadow, int L, int m, int64_t pitch, int k0, int n, int64_t xrow,
+                                 int64_t yrow, uint64_t &prefix)
+{
+    typename P::Raw rx[kT - 1], ry[kT - 1];
+    int ri[kT - 1];
+#pragma unroll
+    for (int i = 0; i < kT - 1; ++i) {
+        if (i < n) {
+            const int k = k0 + i;
+            ri[i] = m - (int)r.wa[k - 1];
+            rx[i] = P::load(tab + xrow, shadow + xrow, m);
+            ry[i] = P::load(tab + yrow, shadow + yrow, ri[i] >= 0 ? ri[i] : 0);
+            xrow += pitch;
+            yrow += (int64_t)(L - k - 1) * pitch;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < kT - 1; ++i) {
+        if (i < n) {
+            const int k = k0 + i;
+            prefix += (uint64_t)r.uf[k - 1];
+            P::relax(acc, P::xop(rx[i], prefix, (uint32_t)(k + 1), ri[i] >= 0), P::yop(ry[i]), (uint32_t)(k + 1));
+        }
+    }
+}
+
 // Eq. (DP:mainrec) for the pairs (s, s + d) inside one diagonal block, all
 // splits in one pass.  Rows (s, s'-1) are consecutive; the row of (s'+1, t)
 // is L - s' rows after the row of (s', t).
@@ -289,17 +321,8 @@ __device__ inline void diag_body(const ChainRows &r, const ChainWork &cw, int L,
     typename P::Acc acc;
     P::init(acc);
     uint64_t prefix = 0;
-    int64_t left = row_of(L, s, s) * pitch;
-    int64_t right = row_of(L, s + 1, t) * pitch;
-    for (int sp = s + 1; sp <= t; ++sp) {
-        prefix += (uint64_t)r.uf[sp - 2];
-        const int ri = m - (int)r.wa[sp - 2];
-        const typename P::X x = P::xop(P::load(tab + left, cw.shadow + left, m), prefix, (uint32_t)sp, ri >= 0);
-        const typename P::Y y = P::yop(P::load(tab + right, cw.shadow + right, ri >= 0 ? ri : 0));
-        P::relax(acc, x, y, (uint32_t)sp);
-        left += pitch;
-        right += (int64_t)(L - sp) * pitch;
-    }
+    relax_run<P>(acc, r, tab, cw.shadow, L, m, pitch, s, t - s, row_of(L, s, s) * pitch,
+                 row_of(L, s + 1, t) * pitch, prefix);
     if (m < cw.gnone[cell])
         P::init(acc);
     if (m >= cw.gall[cell]) {
@@ -484,32 +507,15 @@ __device__ inline void edge_body(const ChainRows &r, const ChainWork &cw, int L,
     P::init(acc);
     // low splits k = s .. k_lo - 1: X from block (I, I), Y from this block
     uint64_t prefix = 0;
-    int64_t xr = row_of(L, s, s) * pitch;
-    int64_t yr = row_of(L, s + 1, t) * pitch;
-    for (int k = s; k < k_lo; ++k) {
-        prefix += (uint64_t)r.uf[k - 1];
-        const int ri = m - (int)r.wa[k - 1];
-        const typename P::X x = P::xop(P::load(tab + xr, cw.shadow + xr, m), prefix, (uint32_t)(k + 1), ri >= 0);
-        const typename P::Y y = P::yop(P::load(tab + yr, cw.shadow + yr, ri >= 0 ? ri : 0));
-        P::relax(acc, x, y, (uint32_t)(k + 1));
-        xr += pitch;
-        yr += (int64_t)(L - k - 1) * pitch;
-    }
+    relax_run<P>(acc, r, tab, cw.shadow, L, m, pitch, s, k_lo - s, row_of(L, s, s) * pitch,
+                 row_of(L, s + 1, t) * pitch, prefix);
     // middle splits: the stored partial counts u_f from k_lo on
     P::merge_stored(acc, load64(tab + cell * pitch, m), prefix);
     // high splits k = 16J + 1 .. t - 1: X from this block, Y from block (J, J)
     prefix += (uint64_t)(cw.pre[k_hi] - cw.pre[k_lo - 1]);
-    xr = row_of(L, s, k_hi + 1) * pitch;
-    yr = (k_hi + 2 <= t ? row_of(L, k_hi + 2, t) : 0) * pitch;
-    for (int k = k_hi + 1; k < t; ++k) {
-        prefix += (uint64_t)r.uf[k - 1];
-        const int ri = m - (int)r.wa[k - 1];
-        const typename P::X x = P::xop(P::load(tab + xr, cw.shadow + xr, m), prefix, (uint32_t)(k + 1), ri >= 0);
-        const typename P::Y y = P::yop(P::load(tab + yr, cw.shadow + yr, ri >= 0 ? ri : 0));
-        P::relax(acc, x, y, (uint32_t)(k + 1));
-        xr += pitch;
-        yr += (int64_t)(L - k - 1) * pitch;
-    }
+    if (t > k_hi + 1)
+        relax_run<P>(acc, r, tab, cw.shadow, L, m, pitch, k_hi + 1, t - k_hi - 1, row_of(L, s, k_hi + 1) * pitch,
+                     row_of(L, k_hi + 2, t) * pitch, prefix);
     if (m < cw.gnone[cell])
         P::init(acc);
     if (m >= cw.gall[cell]) {
