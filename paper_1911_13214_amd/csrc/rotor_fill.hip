@@ -9,12 +9,20 @@
 // u_f^s + u_b^s + C(s+1, t, m - w_abar^s).  Every term lies on a strictly
 // shorter sub-chain.  Ties go to the smallest s', then to C_1 over C_2.
 //
-// Two value paths, chosen per chain by prep_kernel:
-//  - narrow, when L sum(u_f) + sum(u_b) < 2^30: every finite candidate is the
-//    time of a valid schedule, hence below 2^30, so operands are read from a
-//    compact uint32 copy of the table (INT64_MAX stored as 0xFFFFFFFF) and
-//    added with unsigned saturation; the best value and its split are kept
-//    side by side and splits are visited in increasing s' with a strict <;
+// Value paths, chosen per chain by prep_kernel from a bound V on every
+// finite cost: stage j runs forward at most L - j + 1 times in any schedule of
+// the family (induction on the recurrence), so V = sum_j (L - j + 1) u_f^j +
+// sum_j u_b^j, and every C_1 or C_2 candidate, being the time of such a
+// schedule of its sub-chain, is at most V.
+//  - narrow, when V < 2^30: operands are read from a compact uint32 copy of
+//    the table (INT64_MAX stored as 0xFFFFFFFF) and added with unsigned
+//    saturation; the best value and its split are kept side by side and
+//    splits are visited in increasing s' with a strict <;
+//  - packed (middle products of narrow chains, when (V + 1) << S fits below
+//    2^32 - 1 for the S bits of the block's middle split range): a candidate
+//    is one uint32 key (value << S) | (s' - first middle split), so one
+//    saturating add and one unsigned min relax it, ties going to the smaller
+//    split;
 //  - wide, otherwise: operands are the int64 cells and a candidate is one
 //    64-bit key (value << 16) | s', so one unsigned min keeps the smallest
 //    value and, among equal values, the smallest split.  Finite values are
@@ -76,6 +84,11 @@ __device__ inline uint32_t load32(const uint32_t *row, int m)
 __device__ inline uint32_t sat_add(uint32_t a, uint32_t b) { return __builtin_elementwise_add_sat(a, b); }
 __device__ inline uint64_t umin(uint64_t a, uint64_t b) { return b < a ? b : a; }
 
+// Per-chain mode word written by prep_kernel: bit 0 narrow path, bits 8..15
+// the largest S with (V + 1) << S <= 2^32 - 1 (packed middle keys).
+constexpr int32_t kModeNarrow = 1;
+__host__ __device__ inline int packed_bits(int32_t mode) { return (mode >> 8) & 0xFF; }
+
 // Per-chain views of the workspace.
 struct ChainWork {
     const int64_t *pre;    // [L+1] prefix sums of u_f
@@ -92,7 +105,7 @@ __device__ inline ChainWork chain_work(const Work &w, int L, int64_t rows, int64
     cw.gnone = w.gnone + (int64_t)c * rows;
     cw.gall = w.gall + (int64_t)c * rows;
     cw.shadow = w.shadow + (int64_t)c * rows * pitch;
-    cw.narrow = w.flags[c] != 0;
+    cw.narrow = (w.flags[c] & kModeNarrow) != 0;
     return cw;
 }
 
@@ -211,48 +224,92 @@ __device__ inline void store_cell(int64_t *cost, int16_t *dec, uint32_t *shadow,
 
 // ---------------------------------------------------------------------------
 
-// Gates, prefix sums and the value path of every chain.  One thread per s
-// writes the row s of both gate tables: m_all(s, t) (peak of F_all^s with
-// delta^t stored, and of B^s with delta^s stored) and m_none(s, t) (peak of
-// F_ck^s and F_none^{s+1..t-1} with delta^t stored), Section 4.2; delta has
-// the size of a.  Gates above INT32_MAX are clamped: any gate above M < 2^28
-// is never met.
-__global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ params, int L, int64_t rows,
-                                                  Work w)
+// Gates of every pair, prefix sums and value path of every chain.
+// Workgroups 0 .. G-2 of a chain write the gate rows of 64 consecutive s:
+// m_all(s, t) (peak of F_all^s with delta^t stored, and of B^s with delta^s
+// stored) and m_none(s, t) (peak of F_ck^s and F_none^{s+1..t-1} with delta^t
+// stored), Section 4.2; delta has the size of a.  The per-t terms are staged
+// in LDS 64 stages at a time.  Gates above INT32_MAX are clamped: any gate
+// above M < 2^28 is never met.  The last workgroup of a chain scans u_f with
+// one wave.
+__global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ params, int L, int64_t rows, Work w)
 {
     const int c = blockIdx.y;
-    const int s = blockIdx.x * 64 + threadIdx.x + 1;
+    const int lane = threadIdx.x;
     const ChainRows r = chain_rows(params, L, c);
     auto clamp32 = [](int64_t v) { return (int32_t)(v < INT32_MAX ? v : INT32_MAX); };
-    if (s <= L) {
-        int32_t *gn = w.gnone + (int64_t)c * rows;
-        int32_t *ga = w.gall + (int64_t)c * rows;
-        const int64_t first = r.wa[s - 1] + r.of[s - 1];
-        const int64_t bwd = r.wa[s - 1] + r.wabar[s - 1] + r.ob[s - 1];
-        int64_t jmax = 0;  // max over s < j < t of w_a^{j-1} + w_a^j + o_f^j
-        for (int t = s; t <= L; ++t) {
-            const int64_t row = row_of(L, s, t);
-            const int64_t fwd = r.wa[t - 1] + r.wabar[s - 1] + r.of[s - 1];
-            ga[row] = clamp32(fwd > bwd ? fwd : bwd);
-            if (t >= s + 2) {
-                const int64_t v = r.wa[t - 3] + r.wa[t - 2] + r.of[t - 2];  // j = t - 1
-                jmax = v > jmax ? v : jmax;
-            }
-            gn[row] = t > s ? clamp32(r.wa[t - 1] + (first > jmax ? first : jmax)) : 0;
+    if (blockIdx.x == gridDim.x - 1) {
+        // lane l sums a segment of stages, then the segment sums are scanned
+        const int seg = (L + 63) / 64;
+        const int lo = min(L, lane * seg), hi = min(L, lo + seg);
+        uint64_t su = 0, sb = 0, sp = 0;
+        for (int l = lo; l < hi; ++l) {
+            su += (uint64_t)r.uf[l];
+            sb += (uint64_t)r.ub[l];
         }
-    }
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        uint64_t incl = su;
+        for (int off = 1; off < 64; off *= 2) {
+            const uint64_t v = __shfl_up(incl, off);
+            if (lane >= off)
+                incl += v;
+        }
         int64_t *pre = w.pre + (int64_t)c * (L + 1);
-        uint64_t acc = 0, sub = 0;
-        pre[0] = 0;
-        for (int l = 1; l <= L; ++l) {
-            acc += (uint64_t)r.uf[l - 1];
-            sub += (uint64_t)r.ub[l - 1];
-            pre[l] = (int64_t)acc;
+        uint64_t run = incl - su;
+        for (int l = lo; l < hi; ++l) {
+            run += (uint64_t)r.uf[l];
+            pre[l + 1] = (int64_t)run;
+            sp += run;
         }
-        // a bound on every finite cost: no forward runs more than L times
-        const unsigned __int128 bound = (unsigned __int128)acc * (unsigned)L + sub;
-        w.flags[c] = bound < kNarrowBound ? 1 : 0;
+        for (int off = 32; off > 0; off /= 2) {
+            sb += __shfl_xor(sb, off);
+            sp += __shfl_xor(sp, off);
+        }
+        if (lane == 63) {
+            pre[0] = 0;
+            // V = sum_l P[l] + sum_j u_b^j = sum_j (L - j + 1) u_f^j + sum_j u_b^j
+            // (below 2^60 in the domain)
+            const uint64_t bound = sp + sb;
+            int32_t mode = 0;
+            if (bound < kNarrowBound) {
+                const uint64_t q = 0xFFFFFFFFull / (bound + 1);  // >= 4
+                mode = kModeNarrow | ((63 - __clzll((long long)q)) << 8);
+            }
+            w.flags[c] = mode;
+        }
+        return;
+    }
+    __shared__ int64_t lwa[64], lv[64];
+    const int s0 = blockIdx.x * 64 + 1;
+    const int s = s0 + lane;
+    int32_t *gn = w.gnone + (int64_t)c * rows;
+    int32_t *ga = w.gall + (int64_t)c * rows;
+    int64_t first = 0, bwd = 0, fpart = 0;
+    if (s <= L) {
+        first = r.wa[s - 1] + r.of[s - 1];
+        bwd = r.wa[s - 1] + r.wabar[s - 1] + r.ob[s - 1];
+        fpart = r.wabar[s - 1] + r.of[s - 1];
+    }
+    int64_t jmax = 0;  // max over s < j < t of w_a^{j-1} + w_a^j + o_f^j
+    int64_t row = s <= L ? row_of(L, s, s) : 0;
+    for (int t0 = s0; t0 <= L; t0 += 64) {
+        __syncthreads();
+        const int tt = t0 + lane;
+        if (tt <= L) {
+            lwa[lane] = r.wa[tt - 1];
+            lv[lane] = tt >= 3 ? r.wa[tt - 3] + r.wa[tt - 2] + r.of[tt - 2] : 0;  // the term of j = tt - 1
+        }
+        __syncthreads();
+        if (s > L)
+            continue;
+        const int n = min(64, L - t0 + 1);
+        for (int i = max(0, s - t0); i < n; ++i) {
+            const int t = t0 + i;
+            ga[row] = clamp32(max(lwa[i] + fpart, bwd));
+            if (t >= s + 2)
+                jmax = max(jmax, lv[i]);
+            gn[row] = t > s ? clamp32(lwa[i] + max(first, jmax)) : 0;
+            ++row;
+        }
     }
 }
 
@@ -295,7 +352,9 @@ __device__ inline void relax_run(typename P::Acc &acc, const ChainRows &r, const
             const int k = k0 + i;
             ri[i] = m - (int)r.wa[k - 1];
             rx[i] = P::load(tab + xrow, shadow + xrow, m);
-            ry[i] = P::load(tab + yrow, shadow + yrow, ri[i] >= 0 ? ri[i] : 0);
+            // a budget shifted below 0 reads the lane's own budget (in bounds);
+            // xop discards the candidate
+            ry[i] = P::load(tab + yrow, shadow + yrow, ri[i] >= 0 ? ri[i] : m);
             xrow += pitch;
             yrow += (int64_t)(L - k - 1) * pitch;
         }
@@ -355,6 +414,14 @@ __global__ __launch_bounds__(256) void diag_kernel(const int64_t *__restrict__ p
         diag_body<Narrow>(r, cw, L, m, pitch, s, t, tab, dtab);
     else
         diag_body<Wide>(r, cw, L, m, pitch, s, t, tab, dtab);
+}
+
+// Whether the middle products of a chain whose middle split range has
+// span + 1 splits use packed keys.
+__device__ inline bool middle_packed(int32_t mode, int span)
+{
+    const int S = span > 0 ? 32 - __clz(span) : 0;
+    return (mode & kModeNarrow) && S <= packed_bits(mode);
 }
 
 // Middle splits of every block (I, I + D) of one block-diagonal.  A workgroup
@@ -488,10 +555,118 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     const int k_lo = (I + 1) * kT;
     const int k_hi = J * kT;
+    if (middle_packed(w.flags[c], k_hi - k_lo))
+        return;  // middle_packed_kernel takes this chain
     if (cw.narrow)
         middle_body<Narrow>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, tab);
     else
         middle_body<Wide>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, tab);
+}
+
+// Packed middle products (same blocks, workgroups and tiling as
+// middle_kernel).  With S the bit width of k - k_lo, a loaded value v becomes
+// v << S by a rotation that leaves 0xFFFFFFFF (infinity) unchanged; X also
+// gets (prefix << S) | (k - k_lo) by a saturating add, Y nothing more, so a
+// candidate is sat(x + y) and the minimum key is the smallest value with,
+// among equal values, the smallest split.  A budget shifted below 0 turns the
+// X term of that lane into infinity.  The partial is stored in the narrow
+// format (value << 32) | s' that edge_kernel merges.
+__device__ inline uint32_t rot_left(uint32_t v, int S) { return __builtin_amdgcn_alignbit(v, v, (32 - S) & 31); }
+
+__device__ inline void packed_update(uint32_t (&acc)[kSub][kSub], const uint32_t (&rx)[kSub],
+                                     const uint32_t (&ry)[kSub], uint32_t add, int S)
+{
+    uint32_t x[kSub], y[kSub];
+#pragma unroll
+    for (int i = 0; i < kSub; ++i)
+        x[i] = sat_add(rot_left(rx[i], S), add);
+#pragma unroll
+    for (int j = 0; j < kSub; ++j)
+        y[j] = rot_left(ry[j], S);
+#pragma unroll
+    for (int i = 0; i < kSub; ++i)
+#pragma unroll
+        for (int j = 0; j < kSub; ++j)
+            acc[i][j] = min(acc[i][j], sat_add(x[i], y[j]));
+}
+
+__global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__restrict__ params, int L, int M,
+                                                            int64_t pitch, int64_t rows, int delta,
+                                                            int64_t *__restrict__ cost, Work w)
+{
+    const int c = blockIdx.z;
+    const int I = blockIdx.y;
+    const int J = I + delta;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int m = blockIdx.x * 64 + (threadIdx.x & 63);
+    const int s0 = I * kT + (wave >> 1) * kSub + 1;
+    const int t0 = J * kT + (wave & 1) * kSub + 1;
+    const int k_lo = (I + 1) * kT;
+    const int k_hi = J * kT;
+    if (t0 > L || !middle_packed(w.flags[c], k_hi - k_lo))
+        return;
+    const int nt = min(kSub, L - t0 + 1);
+    const int S = k_hi > k_lo ? 32 - __clz(k_hi - k_lo) : 0;
+    const ChainRows r = chain_rows(params, L, c);
+    const ChainWork cw = chain_work(w, L, rows, pitch, c);
+    int64_t *tab = cost + (int64_t)c * rows * pitch;
+
+    MiddleTile<Narrow> tl;
+#pragma unroll
+    for (int i = 0; i < kSub; ++i)
+        tl.xrow[i] = row_of(L, s0 + i, k_lo) * pitch;
+#pragma unroll
+    for (int j = 0; j < kSub; ++j)
+        tl.ystep[j] = (int64_t)(j < nt ? j : nt - 1) * pitch;  // columns past L read the last one
+    tl.yrow = row_of(L, k_lo + 1, t0) * pitch;
+    tl.tab = tab;
+    tl.shadow = cw.shadow;
+    tl.mc = m <= M ? m : M;
+
+    uint32_t acc[kSub][kSub];
+#pragma unroll
+    for (int i = 0; i < kSub; ++i)
+#pragma unroll
+        for (int j = 0; j < kSub; ++j)
+            acc[i][j] = kInf32;
+
+    uint32_t prefix = 0;  // sum of u_f from k_lo to k, at most V
+    uint32_t ax[kSub], ay[kSub], bx[kSub], by[kSub];
+    auto add_of = [&](int k, int ri) { return ri >= 0 ? (prefix << S) | (uint32_t)(k - k_lo) : kInf32; };
+    int k = k_lo;
+    int ra = tl.mc - (int)r.wa[k - 1];
+    tl.load(ra, ax, ay);
+    for (; k + 1 <= k_hi; k += 2) {
+        tl.advance(L, k, pitch);
+        const int rb = tl.mc - (int)r.wa[k];
+        tl.load(rb, bx, by);
+        prefix += (uint32_t)r.uf[k - 1];
+        packed_update(acc, ax, ay, add_of(k, ra), S);
+        if (k + 2 <= k_hi) {
+            tl.advance(L, k + 1, pitch);
+            ra = tl.mc - (int)r.wa[k + 1];
+            tl.load(ra, ax, ay);
+        }
+        prefix += (uint32_t)r.uf[k];
+        packed_update(acc, bx, by, add_of(k + 1, rb), S);
+    }
+    if (k == k_hi) {
+        prefix += (uint32_t)r.uf[k - 1];
+        packed_update(acc, ax, ay, add_of(k, ra), S);
+    }
+    if (m > M)
+        return;
+    const uint32_t mask = (1u << S) - 1u;
+#pragma unroll
+    for (int i = 0; i < kSub; ++i)
+#pragma unroll
+        for (int j = 0; j < kSub; ++j)
+            if (j < nt) {
+                const uint32_t v = acc[i][j];
+                const uint64_t stored = v == kInf32 ? (uint64_t)kInf32 << 32
+                                                    : ((uint64_t)(v >> S) << 32) | (uint32_t)(k_lo + 1 + (v & mask));
+                tab[row_of(L, s0 + i, t0 + j) * pitch + m] = (int64_t)stored;
+            }
 }
 
 // Edge splits, C_2 and the gates for the cells a + b = q of every block
@@ -614,7 +789,7 @@ hipError_t launch_fill(const Tables &tb, const Work &w, hipStream_t stream, Laun
 
     if ((e = before(kPrep)) != hipSuccess)
         return e;
-    prep_kernel<<<dim3((L + 63) / 64, tb.n_chains), 64, 0, stream>>>(tb.params, L, tb.rows, w);
+    prep_kernel<<<dim3((L + 63) / 64 + 1, tb.n_chains), 64, 0, stream>>>(tb.params, L, tb.rows, w);
     if ((e = launched(kPrep, 0, 0, 0)) != hipSuccess)
         return e;
     if ((e = before(kLeaf)) != hipSuccess)
@@ -641,9 +816,16 @@ hipError_t launch_fill(const Tables &tb, const Work &w, hipStream_t stream, Laun
             pairs += (uint64_t)kT * (uint64_t)min(kT, L - (I + delta) * kT);
         if ((e = before(kMiddle)) != hipSuccess)
             return e;
+        // each chain is taken by one of the two kernels, the other returns at once
+        middle_packed_kernel<<<dim3(mb64, nb - delta, tb.n_chains), 256, 0, stream>>>(
+            tb.params, L, tb.M, tb.pitch, tb.rows, delta, tb.cost, w);
+        if ((e = launched(kMiddle, pairs * (uint64_t)((delta - 1) * kT + 1), 0, 0)) != hipSuccess)
+            return e;
+        if ((e = before(kMiddle)) != hipSuccess)
+            return e;
         middle_kernel<<<dim3(mb64, nb - delta, tb.n_chains), 256, 0, stream>>>(tb.params, L, tb.M, tb.pitch,
                                                                                tb.rows, delta, tb.cost, w);
-        if ((e = launched(kMiddle, pairs * (uint64_t)((delta - 1) * kT + 1), 0, 0)) != hipSuccess)
+        if ((e = launched(kMiddle, 0, 0, 0)) != hipSuccess)
             return e;
         for (int q = 0; q <= 2 * kT - 2; ++q) {
             const int a_min = q - (kT - 1) > 0 ? q - (kT - 1) : 0;

@@ -256,13 +256,25 @@ def test_timed_solve_matches_and_counts_the_work(cfg):
     assert stats["prep"]["launches"] == 1
 
 
-def wide_costs_chain(seed, L):
-    """A chain whose cost bound L sum(u_f) + sum(u_b) exceeds 2^30, so the
-    solver takes its 64-bit value path."""
+def cost_bound(p):
+    """sum_l P[l] + sum u_b = sum_j (L - j + 1) u_f^j + sum u_b: no stage runs
+    forward more often than the stages after it plus one, so every finite cost
+    is at most this; the library picks its value path from it."""
+    return int(np.cumsum(p[0].astype(object)).sum() + p[1].astype(object).sum())
+
+
+def scaled_chain(seed, L, shift):
     p = chaingen.random_chains(1, L, seed=seed)
-    p[0, 0] *= 1 << 22
-    p[0, 1] *= 1 << 22
-    assert L * p[0, 0].sum() + p[0, 1].sum() >= 1 << 30
+    p[0, 0] *= 1 << shift
+    p[0, 1] *= 1 << shift
+    return p
+
+
+def wide_costs_chain(seed, L):
+    """A chain whose cost bound exceeds 2^30, so the solver takes its 64-bit
+    value path."""
+    p = scaled_chain(seed, L, 22)
+    assert cost_bound(p[0]) >= 1 << 30
     return p
 
 
@@ -274,12 +286,28 @@ def test_wide_value_path(L, M, seed):
     assert_same(p, M, cost, dec)
 
 
+@pytest.mark.parametrize("L,M,seed", [(70, 300, 5), (90, 200, 6)])
+def test_narrow_chain_beyond_packed_keys(L, M, seed):
+    # costs below 2^30 (compact copy) but too large to leave the split field
+    # room once the middle range has 16 splits or more: the first
+    # block-diagonal takes packed keys, the later ones the (value, split) pairs
+    p = scaled_chain(seed, L, 12)
+    v = cost_bound(p[0])
+    assert (1 << 26) < v < (1 << 30)
+    say(f"narrow beyond packed L={L} M={M} bound={v}")
+    _, cost, dec = solve_on_gpu(p, M)
+    assert_same(p, M, cost, dec)
+
+
 def test_batch_mixing_value_paths():
     # chains of one call may take different value paths
     params = chaingen.random_chains(6, 37, seed=21)
     for c in (1, 4):
         params[c, 0] *= 1 << 22
         params[c, 1] *= 1 << 22
+    params[2, 0] *= 1 << 13
+    params[2, 1] *= 1 << 13
+    assert cost_bound(params[1]) >= 1 << 30 and (1 << 27) < cost_bound(params[2]) < (1 << 30)
     M = 200
     _, cost, dec = solve_on_gpu(params, M)
     for c in range(6):
