@@ -65,6 +65,16 @@ def cpu_baseline(params, M, stages):
     }
 
 
+def arithmetic_type(params):
+    """The integer type the fill computes in: uint32 with saturation when every
+    chain's cost bound sum_j (L - j + 1) u_f^j + sum_j u_b^j is below 2^30 (the
+    library makes the same test on the device), else int64."""
+    import numpy as np
+    p = params if params.ndim == 3 else params[None]
+    bound = max(int(np.cumsum(c[0].astype(object)).sum() + c[1].astype(object).sum()) for c in p)
+    return "u32" if bound < (1 << 30) else "int64"
+
+
 def traffic_if_current(kernel_class):
     """Measured HBM bytes per launch of a kernel class from the committed
     counter summary, if it was taken on the current kernel source."""
@@ -188,7 +198,7 @@ def main():
         "higher_is_better": True,
         "scaling": "strong",
         "vs_baseline": None,
-        "dtype": "int64",
+        "dtype": arithmetic_type(params),
         "data": "synthetic",
         "config": {"workload": name, "L": L, "M": M, "n_chains": n_chains, "candidates_per_step": R,
                    "alg_bytes_per_step": alg_bytes},
