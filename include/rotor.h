@@ -211,6 +211,50 @@ ROTOR_API int32_t rotor_reconstruct(const int64_t *d_params, int32_t n_chains, i
                           int32_t chain, int32_t n_budgets, const int64_t *d_budgets, int64_t cap, rotor_op *d_ops,
                           int64_t *d_count, int32_t *d_status, void *stream);
 
+/* ---- front end: from measured sizes to budgets (host only) --------------- */
+
+/* Discretisation of Section 5.2: for a memory limit of mem_bytes and S slots,
+ * every memory size becomes a whole number of slots of mem_bytes / S bytes,
+ * rounded up: ceil(v * S / mem_bytes).  The DP then runs with the budget
+ * M = S, whatever the limit, and each size is overestimated by less than one
+ * slot.
+ *
+ *   h_params     HOST, read only: [n_chains][6][L] int64 in the layout above,
+ *                except that the rows ROTOR_ROW_WA, _WABAR, _OF and _OB hold
+ *                sizes in bytes (or any unit of mem_bytes).
+ *   h_mem_bytes  HOST, read only: [n_chains] the memory limit of each chain,
+ *                > 0; a batch may give the same chain several limits.
+ *   slots        S, 1 <= S < 2^28.
+ *   h_out        HOST, written: [n_chains][6][L], the time rows copied, the
+ *                four size rows in slots.  May be h_params itself.
+ * Returns ROTOR_OK; ROTOR_EINVAL for a null pointer, sizes out of range, a
+ * limit <= 0 or S out of range; ROTOR_EDOMAIN if an input is negative or a
+ * size comes to 2^30 slots or more.  Nothing is written unless ROTOR_OK. */
+ROTOR_API int32_t rotor_discretize(const int64_t *h_params, int32_t n_chains, int32_t L, const int64_t *h_mem_bytes,
+                                   int64_t slots, int64_t *h_out);
+
+/* Peak memory of the schedule that recomputes nothing -- F_all^1 ..
+ * F_all^L, then B^L .. B^1 -- under the memory accounting of Theorem 1
+ * (Section 4.2): the chain input is not counted, delta^l has the size of a^l,
+ * and during F_all^j the gradient delta^L, abar^1 .. abar^j and o_f^j are
+ * live, during B^j delta^j, abar^1 .. abar^j and o_b^j.  This is the memory
+ * of the store-everything strategy the experiments of Section 5.3 compare
+ * against; every budget at or above it gives the time sum(u_f + u_b).
+ *
+ *   h_params  HOST, read only: [6][L] int64, one chain (any size unit).
+ *   peak      HOST, written.
+ * Returns ROTOR_OK, ROTOR_EINVAL (null pointer, L out of range) or
+ * ROTOR_EDOMAIN (a negative value). */
+ROTOR_API int32_t rotor_store_all_peak(const int64_t *h_params, int32_t L, int64_t *peak);
+
+/* The n budgets equally spaced between 0 (excluded) and top (included), as
+ * the experiments of Section 5.3 take 10 limits up to the store-everything
+ * memory: budgets[i-1] = floor(i * top / n), i = 1..n.  One rotor_reconstruct
+ * call then walks all of them in the same table.
+ *   top >= 0, 1 <= n <= 2^20, budgets HOST [n] written.
+ * Returns ROTOR_OK or ROTOR_EINVAL. */
+ROTOR_API int32_t rotor_even_budgets(int64_t top, int32_t n, int64_t *budgets);
+
 #ifdef __cplusplus
 }
 #endif

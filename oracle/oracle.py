@@ -59,6 +59,12 @@ def lib():
         l.oracle_reconstruct.restype = ctypes.c_int64
         l.oracle_reconstruct.argtypes = [ctypes.c_int, ctypes.c_int64, i64p, i64p, ctypes.c_int64, i32p,
                                          ctypes.c_int64]
+        l.oracle_slots.restype = ctypes.c_int64
+        l.oracle_slots.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64]
+        l.oracle_discretize.restype = None
+        l.oracle_discretize.argtypes = [ctypes.c_int, i64p, ctypes.c_int64, ctypes.c_int64, i64p]
+        l.oracle_store_all_peak.restype = ctypes.c_int64
+        l.oracle_store_all_peak.argtypes = [ctypes.c_int, i64p]
         _lib = l
     return _lib
 
@@ -141,3 +147,22 @@ def reconstruct(params, M: int, C, m: int):
 def table_view(C, L: int):
     """Dict-free accessor: ``get(s, t)`` returns the row of (s, t)."""
     return lambda s, t: C[row(L, s, t)]
+
+
+def slots(v: int, mem: int, S: int) -> int:
+    """Slots of a size v for the limit mem split into S slots (Section 5.2)."""
+    return lib().oracle_slots(v, mem, S)
+
+
+def discretize(params, mem: int, S: int):
+    """One chain [6, L] with its four size rows converted to slots."""
+    p = _chain(params)
+    out = np.empty_like(p)
+    lib().oracle_discretize(p.shape[1], _p64(p), mem, S, _p64(out))
+    return out
+
+
+def store_all_peak(params) -> int:
+    """Peak memory of F_all^1..F_all^L, B^L..B^1 (no recomputation)."""
+    p = _chain(params)
+    return lib().oracle_store_all_peak(p.shape[1], _p64(p))

@@ -316,3 +316,55 @@ int64_t oracle_reconstruct(int L, int64_t M, const int64_t *p, const int64_t *C,
     opt_rec(&r, 1, L, m);
     return r.err ? -1 : r.n;
 }
+
+/* ---- front end: discretisation and the store-everything memory ----------- */
+
+/* Section 5.2: with a memory limit mem and S slots of mem / S each, a size v
+ * takes the smallest whole number of slots q with q * (mem / S) >= v, that
+ * is q * mem >= v * S. */
+int64_t oracle_slots(int64_t v, int64_t mem, int64_t S)
+{
+    const unsigned __int128 need = (unsigned __int128)v * (unsigned __int128)S;
+    unsigned __int128 q = need / (unsigned __int128)mem;
+    if (q * (unsigned __int128)mem < need)
+        q += 1;
+    return (int64_t)q;
+}
+
+/* p_out[6][L] = p_in with the four size rows (omega_a, omega_abar, o_f, o_b)
+ * in slots; the time rows are copied. */
+void oracle_discretize(int L, const int64_t *p_in, int64_t mem, int64_t S, int64_t *p_out)
+{
+    for (int row = 0; row < 6; ++row)
+        for (int l = 0; l < L; ++l) {
+            const int64_t v = p_in[(int64_t)row * L + l];
+            const int size_row = row == R_WA || row == R_WAB || row == R_OF || row == R_OB;
+            p_out[(int64_t)row * L + l] = size_row ? oracle_slots(v, mem, S) : v;
+        }
+}
+
+/* Peak memory of F_all^1 .. F_all^L, B^L .. B^1, replayed with the
+ * accounting of Theorem 1: the chain input a^0 is not counted, delta^L is
+ * stored from the start, an operation's peak is what is stored plus its
+ * output and overhead, and B^j's output delta^{j-1} is not counted while B^j
+ * runs (the m_all backward term). */
+int64_t oracle_store_all_peak(int L, const int64_t *p)
+{
+    orc_chain ch = {L, 0, p};
+    int64_t stored = wd(&ch, L); /* delta^L */
+    int64_t peak = 0;
+    for (int j = 1; j <= L; ++j) {
+        /* F_all^j reads a^{j-1} (inside abar^{j-1}, or a^0) and writes abar^j */
+        peak = max64(peak, stored + wab(&ch, j) + of(&ch, j));
+        stored += wab(&ch, j);
+    }
+    for (int j = L; j >= 1; --j) {
+        /* B^j reads delta^j and abar^j, both stored */
+        peak = max64(peak, stored + ob(&ch, j));
+        /* then abar^j and delta^j are freed and delta^{j-1} is stored */
+        stored -= wab(&ch, j) + wd(&ch, j);
+        if (j > 1)
+            stored += wd(&ch, j - 1);
+    }
+    return peak;
+}

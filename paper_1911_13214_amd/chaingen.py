@@ -67,6 +67,24 @@ def random_chains(n_chains: int, L: int, seed: int, wa_hi: int = 10) -> np.ndarr
     return out
 
 
+def byte_sized_chain(L: int, seed: int) -> np.ndarray:
+    """A chain [6, L] whose sizes are in bytes, as measured before the
+    discretisation into slots: per stage u_f = U{1..100}, u_b = max(1, 2 u_f +
+    U{-5..5}), omega_a = U{2^10..2^27} bytes, omega_abar = omega_a U{1..4},
+    o_f, o_b = U{0..2^24} bytes (drawn in that order)."""
+    rng = SplitMix64(seed)
+    out = np.zeros((6, L), dtype=np.int64)
+    for l in range(L):
+        uf = rng.uniform(1, 100)
+        ub = max(1, 2 * uf + rng.uniform(-5, 5))
+        wa = rng.uniform(1 << 10, 1 << 27)
+        wabar = wa * rng.uniform(1, 4)
+        of = rng.uniform(0, 1 << 24)
+        ob = rng.uniform(0, 1 << 24)
+        out[:, l] = (uf, ub, wa, wabar, of, ob)
+    return out
+
+
 def homogeneous_chain(L: int, uf=10, ub=20, wa=5, wabar=15, of=0, ob=0) -> np.ndarray:
     out = np.zeros((1, 6, L), dtype=np.int64)
     for r, v in enumerate((uf, ub, wa, wabar, of, ob)):

@@ -1,0 +1,90 @@
+// Front end of the solver (host only): discretisation of memory sizes into
+// slots (Section 5.2), the memory of the schedule that stores everything, and
+// equally spaced budgets (the experimental setting of Section 5.3).
+#include <stdint.h>
+
+#include "rotor_internal.h"
+
+namespace {
+
+constexpr int64_t kMaxSlots = (int64_t)1 << 28;
+constexpr int64_t kMaxSize = (int64_t)1 << 30;
+
+bool is_size_row(int row)
+{
+    return row == ROTOR_ROW_WA || row == ROTOR_ROW_WABAR || row == ROTOR_ROW_OF || row == ROTOR_ROW_OB;
+}
+
+// ceil(v * slots / mem) in 128-bit arithmetic (v, slots, mem >= 0, mem > 0).
+int64_t slots_of(int64_t v, int64_t slots, int64_t mem)
+{
+    const unsigned __int128 num = (unsigned __int128)(uint64_t)v * (uint64_t)slots;
+    const unsigned __int128 q = (num + (uint64_t)mem - 1) / (uint64_t)mem;
+    return q >= (unsigned __int128)kMaxSize ? kMaxSize : (int64_t)q;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t rotor_discretize(const int64_t *h_params, int32_t n_chains, int32_t L, const int64_t *h_mem_bytes,
+                         int64_t slots, int64_t *h_out)
+{
+    if (!h_params || !h_mem_bytes || !h_out || n_chains < 1 || n_chains > ROTOR_MAX_CHAINS || L < 1 ||
+        L > ROTOR_MAX_L || slots < 1 || slots >= kMaxSlots)
+        return ROTOR_EINVAL;
+    for (int32_t c = 0; c < n_chains; ++c)
+        if (h_mem_bytes[c] <= 0)
+            return ROTOR_EINVAL;
+    const int64_t n = (int64_t)n_chains * ROTOR_N_ROWS * L;
+    for (int64_t i = 0; i < n; ++i) {
+        const int64_t v = h_params[i];
+        if (v < 0)
+            return ROTOR_EDOMAIN;
+        const int row = (int)((i / L) % ROTOR_N_ROWS);
+        if (is_size_row(row) && slots_of(v, slots, h_mem_bytes[i / ((int64_t)ROTOR_N_ROWS * L)]) >= kMaxSize)
+            return ROTOR_EDOMAIN;
+    }
+    for (int64_t i = 0; i < n; ++i) {
+        const int row = (int)((i / L) % ROTOR_N_ROWS);
+        const int64_t mem = h_mem_bytes[i / ((int64_t)ROTOR_N_ROWS * L)];
+        h_out[i] = is_size_row(row) ? slots_of(h_params[i], slots, mem) : h_params[i];
+    }
+    return ROTOR_OK;
+}
+
+int32_t rotor_store_all_peak(const int64_t *h_params, int32_t L, int64_t *peak)
+{
+    if (!h_params || !peak || L < 1 || L > ROTOR_MAX_L)
+        return ROTOR_EINVAL;
+    for (int64_t i = 0; i < (int64_t)ROTOR_N_ROWS * L; ++i)
+        if (h_params[i] < 0)
+            return ROTOR_EDOMAIN;
+    const int64_t *wa = h_params + (int64_t)ROTOR_ROW_WA * L;
+    const int64_t *wabar = h_params + (int64_t)ROTOR_ROW_WABAR * L;
+    const int64_t *of = h_params + (int64_t)ROTOR_ROW_OF * L;
+    const int64_t *ob = h_params + (int64_t)ROTOR_ROW_OB * L;
+    // values are < 2^63 / (3L + 2) in any sane input; saturate otherwise
+    auto add = [](int64_t a, int64_t b) { return a > INT64_MAX - b ? INT64_MAX : a + b; };
+    int64_t best = 0, kept = 0;  // kept: abar^1 .. abar^{j-1}
+    for (int32_t j = 1; j <= L; ++j) {
+        const int64_t fwd = add(add(add(wa[L - 1], kept), wabar[j - 1]), of[j - 1]);
+        kept = add(kept, wabar[j - 1]);
+        const int64_t bwd = add(add(wa[j - 1], kept), ob[j - 1]);
+        best = fwd > best ? fwd : best;
+        best = bwd > best ? bwd : best;
+    }
+    *peak = best;
+    return ROTOR_OK;
+}
+
+int32_t rotor_even_budgets(int64_t top, int32_t n, int64_t *budgets)
+{
+    if (!budgets || top < 0 || n < 1 || n > (1 << 20))
+        return ROTOR_EINVAL;
+    for (int32_t i = 1; i <= n; ++i)
+        budgets[i - 1] = (int64_t)((unsigned __int128)(uint64_t)top * (uint64_t)i / (uint64_t)n);
+    return ROTOR_OK;
+}
+
+}  // extern "C"

@@ -40,6 +40,9 @@ SIGNATURES = {
     "rotor_solve": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp, _u64, _vp]),
     "rotor_reconstruct": (_i32, [_vp, _i32, _i32, _i64, _vp, _i32, _i32, _vp, _i64, _vp, _vp, _vp, _vp]),
     "rotor_solve_timed": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp, _u64, _vp, _vp]),
+    "rotor_discretize": (_i32, [_vp, _i32, _i32, _vp, _i64, _vp]),
+    "rotor_store_all_peak": (_i32, [_vp, _i32, _P(_i64)]),
+    "rotor_even_budgets": (_i32, [_i64, _i32, _vp]),
 }
 
 KERNEL_CLASSES = ("leaf", "diag", "middle", "edge", "prep")
@@ -178,6 +181,42 @@ def rotor_reconstruct(d_params, n_chains: int, L: int, M: int, d_dec, chain: int
                                    _stream_ptr(stream)), "rotor_reconstruct")
 
 
+def rotor_discretize(params: np.ndarray, mem_bytes, slots: int) -> np.ndarray:
+    """Sizes in bytes -> slots of mem_bytes / slots each, rounded up
+    (Section 5.2).  ``params`` [n_chains, 6, L] (or [6, L]); ``mem_bytes`` one
+    limit or one per chain.  Returns the converted array (same shape)."""
+    p = np.ascontiguousarray(params, dtype=np.int64)
+    squeeze = p.ndim == 2
+    if squeeze:
+        p = p[None]
+    if p.ndim != 3 or p.shape[1] != N_ROWS:
+        raise ValueError("params must be [n_chains, 6, L]")
+    mem = np.ascontiguousarray(np.broadcast_to(np.asarray(mem_bytes, dtype=np.int64), (p.shape[0],)))
+    out = np.empty_like(p)
+    _check(lib().rotor_discretize(p.ctypes.data, p.shape[0], p.shape[2], mem.ctypes.data, slots, out.ctypes.data),
+           "rotor_discretize")
+    return out[0] if squeeze else out
+
+
+def rotor_store_all_peak(params: np.ndarray) -> int:
+    """Memory of the schedule that recomputes nothing, for one chain [6, L]."""
+    p = np.ascontiguousarray(params, dtype=np.int64)
+    if p.ndim == 3 and p.shape[0] == 1:
+        p = p[0]
+    if p.ndim != 2 or p.shape[0] != N_ROWS:
+        raise ValueError("params must be one chain [6, L]")
+    peak = ctypes.c_int64()
+    _check(lib().rotor_store_all_peak(p.ctypes.data, p.shape[1], ctypes.byref(peak)), "rotor_store_all_peak")
+    return peak.value
+
+
+def rotor_even_budgets(top: int, n: int) -> np.ndarray:
+    """floor(i * top / n) for i = 1..n."""
+    out = np.empty(n, dtype=np.int64) if n > 0 else np.empty(1, dtype=np.int64)
+    _check(lib().rotor_even_budgets(top, n, out.ctypes.data), "rotor_even_budgets")
+    return out
+
+
 # ---- conveniences (allocation and host copies only) -------------------------
 
 def upload_params(params: np.ndarray, M: int, device="cuda"):
@@ -250,3 +289,26 @@ def reconstruct(d_params, n_chains: int, L: int, M: int, d_dec, chain: int, budg
         _check(int(status[b]), "rotor_reconstruct")
         out.append([(int(k), int(s)) for k, s in ops[b, :count[b]]])
     return out
+
+
+def plan(params_bytes: np.ndarray, slots: int = 500, n_budgets: int = 10, top_bytes=None, device="cuda"):
+    """The paper's use of the solver (Sections 5.2 and 5.3) for one chain
+    whose sizes are in bytes: discretise with respect to ``top_bytes``
+    (default: the memory of the store-everything schedule) into ``slots``
+    slots, fill one table with M = slots, and walk it at ``n_budgets``
+    budgets equally spaced up to the top in one call.  Returns a dict with
+    the slot parameters, the budgets (slots), their times C(1, L, budget)
+    (None where infeasible) and the sequences."""
+    p = np.ascontiguousarray(params_bytes, dtype=np.int64)
+    if p.ndim == 3:
+        p = p[0]
+    L = p.shape[1]
+    top = rotor_store_all_peak(p) if top_bytes is None else int(top_bytes)
+    ps = rotor_discretize(p, max(top, 1), slots)
+    d_params, cost, dec = solve(ps, slots, device=device)
+    budgets = rotor_even_budgets(slots, n_budgets)
+    seqs = reconstruct(d_params, 1, L, slots, dec, 0, budgets)
+    top_row = cost[0, rotor_row_index(L, 1, L)].cpu().numpy()
+    times = [None if top_row[b] == ROTOR_INF else int(top_row[b]) for b in budgets]
+    return {"params_slots": ps, "top_bytes": top, "budgets": [int(b) for b in budgets], "times": times,
+            "sequences": seqs}

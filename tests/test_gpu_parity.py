@@ -209,6 +209,50 @@ def test_reconstruct_large_chain_replays():
         assert time == g["top_cost"][m] and peak <= m
 
 
+@pytest.mark.parametrize("L,seed", [(40, 1), (77, 2)])
+def test_plan_discretise_solve_and_walk_ten_budgets(L, seed):
+    # Sections 5.2 and 5.3: sizes in bytes -> 500 slots of the store-everything
+    # memory, one table, ten equally spaced budgets walked in one call
+    from paper_1911_13214_amd import rotor
+    p = chaingen.byte_sized_chain(L, seed=seed)
+    say(f"plan bytes L={L}")
+    S = 500
+    res = rotor.plan(p, slots=S, n_budgets=10)
+    ps = res["params_slots"]
+    assert res["top_bytes"] == orc.store_all_peak(p)
+    assert np.array_equal(ps, orc.discretize(p, orc.store_all_peak(p), S))
+    assert res["budgets"] == [S * i // 10 for i in range(1, 11)]
+    C, _ = orc.solve(ps, S)
+    top = orc.table_view(C, L)(1, L)
+    ch = model.Chain(ps)
+    feasible = 0
+    for b, t, seq in zip(res["budgets"], res["times"], res["sequences"]):
+        if top[b] == orc.INF:
+            assert t is None and seq is None
+            continue
+        feasible += 1
+        assert t == top[b] and seq == orc.reconstruct(ps, S, C, b)
+        time, peak = model.simulate(ch, 1, L, seq)
+        assert time == t and peak <= b
+    assert feasible >= 3
+
+
+def test_discretise_one_limit_per_chain_of_a_batch():
+    # the paper's reading: every memory limit gets its own slot size; a batch
+    # of ten copies of a chain with ten limits is filled in one call
+    from paper_1911_13214_amd import rotor
+    p = chaingen.byte_sized_chain(30, seed=9)
+    top = orc.store_all_peak(p)
+    limits = np.array([top * i // 10 for i in range(1, 11)], dtype=np.int64)
+    S = 200
+    ps = rotor.rotor_discretize(np.repeat(p[None], 10, axis=0), limits, S)
+    for c in range(10):
+        assert np.array_equal(ps[c], orc.discretize(p, int(limits[c]), S))
+    _, cost, dec = solve_on_gpu(ps, S)
+    for c in range(10):
+        assert_same(ps, S, cost, dec, c)
+
+
 def test_reconstruct_status_codes():
     import torch
 

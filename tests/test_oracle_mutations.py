@@ -93,3 +93,48 @@ def test_mutation_is_caught(tmp_path, name):
     old, new = MUTATIONS[name]
     lib = _build_mutant(tmp_path, name, old, new)
     assert not _pins_pass(lambda params, M: _mutant_solve(lib, params, M)), f"mutation '{name}' went unnoticed"
+
+
+# the front end: a plausible mistake in the discretisation or in the
+# store-everything memory is caught by the pins of test_frontend.py
+FRONT_MUTATIONS = {
+    "slots rounded down": ("if (q * (unsigned __int128)mem < need)\n        q += 1;", ""),
+    "slots of the limit, not of S": ("(unsigned __int128)v * (unsigned __int128)S;", "(unsigned __int128)v;"),
+    "store-all peak drops delta^L": ("int64_t stored = wd(&ch, L); /* delta^L */", "int64_t stored = 0;"),
+    "store-all peak drops o_b": ("peak = max64(peak, stored + ob(&ch, j));", "peak = max64(peak, stored);"),
+    "store-all peak keeps the freed gradient": ("stored -= wab(&ch, j) + wd(&ch, j);", "stored -= wab(&ch, j);"),
+}
+
+
+def _front_pins_pass(lib):
+    import random
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    lib.oracle_slots.restype = ctypes.c_int64
+    lib.oracle_slots.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64]
+    lib.oracle_store_all_peak.restype = ctypes.c_int64
+    lib.oracle_store_all_peak.argtypes = [ctypes.c_int, i64p]
+    rng = random.Random(5)
+    for _ in range(300):
+        mem, S = rng.randint(1, 1 << 30), rng.choice([1, 500, rng.randint(1, 1 << 16)])
+        v = rng.randint(0, 3 * mem)
+        q = lib.oracle_slots(v, mem, S)
+        if not (q * mem >= v * S and (q == 0 or (q - 1) * mem < v * S)):
+            return False
+    for seed in range(12):
+        p = np.ascontiguousarray(chaingen.byte_sized_chain(1 + seed, seed=seed))
+        if lib.oracle_store_all_peak(p.shape[1], p.ctypes.data_as(i64p)) != \
+                model.all_fall_peak(model.Chain(p), 1, p.shape[1]):
+            return False
+    return True
+
+
+def test_unmutated_front_end_passes(tmp_path):
+    lib = _build_mutant(tmp_path, "none", "#include <stdint.h>", "#include <stdint.h>")
+    assert _front_pins_pass(lib)
+
+
+@pytest.mark.parametrize("name", sorted(FRONT_MUTATIONS))
+def test_front_end_mutation_is_caught(tmp_path, name):
+    old, new = FRONT_MUTATIONS[name]
+    lib = _build_mutant(tmp_path, name, old, new)
+    assert not _front_pins_pass(lib), f"mutation '{name}' went unnoticed"
