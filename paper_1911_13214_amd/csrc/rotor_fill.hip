@@ -335,45 +335,72 @@ __global__ __launch_bounds__(256) void leaf_kernel(const int64_t *__restrict__ p
         cw.shadow[idx] = ok ? (uint32_t)v : kInf32;
 }
 
-// Relax the consecutive splits k = k0 .. k0 + n - 1 (n <= kT - 1, uniform)
-// of the pair (s, t): X rows (s, k) are consecutive from xrow, the Y row of
-// (k+1, t) starts at yrow and advances L - k - 1 rows per k.  All loads are
-// issued before the first relaxation so their latencies overlap.
-template <class P>
-__device__ inline void relax_run(typename P::Acc &acc, const ChainRows &r, const int64_t *tab,
-                                 const uint32_t *shadow, int L, int m, int64_t pitch, int k0, int n, int64_t xrow,
-                                 int64_t yrow, uint64_t &prefix)
+// Relax the N consecutive splits k = k0 .. k0 + N - 1 of the pair (s, t):
+// X rows (s, k) are consecutive from xrow, the Y row of (k+1, t) starts at
+// yrow and advances L - k - 1 rows per k.  Straight-line code: every load is
+// issued before the first relaxation, so their latencies overlap.
+template <class P, int N>
+__device__ __forceinline__ void relax_fixed(typename P::Acc &acc, const ChainRows &r, const int64_t *tab,
+                                            const uint32_t *shadow, int L, int m, int64_t pitch, int k0,
+                                            int64_t xrow, int64_t yrow, uint64_t &prefix)
 {
-    typename P::Raw rx[kT - 1], ry[kT - 1];
-    int ri[kT - 1];
+    typename P::Raw rx[N], ry[N];
+    int ri[N];
 #pragma unroll
-    for (int i = 0; i < kT - 1; ++i) {
-        if (i < n) {
-            const int k = k0 + i;
-            ri[i] = m - (int)r.wa[k - 1];
-            rx[i] = P::load(tab + xrow, shadow + xrow, m);
-            // a budget shifted below 0 reads the lane's own budget (in bounds);
-            // xop discards the candidate
-            ry[i] = P::load(tab + yrow, shadow + yrow, ri[i] >= 0 ? ri[i] : m);
-            xrow += pitch;
-            yrow += (int64_t)(L - k - 1) * pitch;
-        }
+    for (int i = 0; i < N; ++i) {
+        const int k = k0 + i;
+        ri[i] = m - (int)r.wa[k - 1];
+        rx[i] = P::load(tab + xrow, shadow + xrow, m);
+        // a budget shifted below 0 reads the lane's own budget (in bounds);
+        // xop discards the candidate
+        ry[i] = P::load(tab + yrow, shadow + yrow, ri[i] >= 0 ? ri[i] : m);
+        xrow += pitch;
+        yrow += (int64_t)(L - k - 1) * pitch;
     }
 #pragma unroll
-    for (int i = 0; i < kT - 1; ++i) {
-        if (i < n) {
-            const int k = k0 + i;
-            prefix += (uint64_t)r.uf[k - 1];
-            P::relax(acc, P::xop(rx[i], prefix, (uint32_t)(k + 1), ri[i] >= 0), P::yop(ry[i]), (uint32_t)(k + 1));
-        }
+    for (int i = 0; i < N; ++i) {
+        const int k = k0 + i;
+        prefix += (uint64_t)r.uf[k - 1];
+        P::relax(acc, P::xop(rx[i], prefix, (uint32_t)(k + 1), ri[i] >= 0), P::yop(ry[i]), (uint32_t)(k + 1));
     }
+}
+
+// The same for a run of n <= N splits (n uniform): one branch picks the
+// straight-line body of that length.
+template <class P, int N>
+struct RelaxRun {
+    __device__ __forceinline__ static void go(int n, typename P::Acc &acc, const ChainRows &r, const int64_t *tab,
+                                              const uint32_t *shadow, int L, int m, int64_t pitch, int k0,
+                                              int64_t xrow, int64_t yrow, uint64_t &prefix)
+    {
+        if (n == N)
+            relax_fixed<P, N>(acc, r, tab, shadow, L, m, pitch, k0, xrow, yrow, prefix);
+        else
+            RelaxRun<P, N - 1>::go(n, acc, r, tab, shadow, L, m, pitch, k0, xrow, yrow, prefix);
+    }
+};
+template <class P>
+struct RelaxRun<P, 0> {
+    __device__ __forceinline__ static void go(int, typename P::Acc &, const ChainRows &, const int64_t *,
+                                              const uint32_t *, int, int, int64_t, int, int64_t, int64_t,
+                                              uint64_t &)
+    {
+    }
+};
+
+template <class P>
+__device__ __forceinline__ void relax_run(typename P::Acc &acc, const ChainRows &r, const int64_t *tab,
+                                          const uint32_t *shadow, int L, int m, int64_t pitch, int k0, int n,
+                                          int64_t xrow, int64_t yrow, uint64_t &prefix)
+{
+    RelaxRun<P, kT - 1>::go(n, acc, r, tab, shadow, L, m, pitch, k0, xrow, yrow, prefix);
 }
 
 // Eq. (DP:mainrec) for the pairs (s, s + d) inside one diagonal block, all
 // splits in one pass.  Rows (s, s'-1) are consecutive; the row of (s'+1, t)
 // is L - s' rows after the row of (s', t).
 template <class P>
-__device__ inline void diag_body(const ChainRows &r, const ChainWork &cw, int L, int m, int64_t pitch, int s,
+__device__ __forceinline__ void diag_body(const ChainRows &r, const ChainWork &cw, int L, int m, int64_t pitch, int s,
                                  int t, int64_t *tab, int16_t *dtab)
 {
     const int64_t cell = row_of(L, s, t);
@@ -674,7 +701,7 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
 // Splits are met in increasing order: low, then the stored middle partial,
 // then high.
 template <class P>
-__device__ inline void edge_body(const ChainRows &r, const ChainWork &cw, int L, int m, int64_t pitch, int s,
+__device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &cw, int L, int m, int64_t pitch, int s,
                                  int t, int k_lo, int k_hi, int64_t *tab, int16_t *dtab)
 {
     const int64_t cell = row_of(L, s, t);
