@@ -404,20 +404,19 @@ __device__ __forceinline__ void diag_body(const ChainRows &r, const ChainWork &c
                                  int t, int64_t *tab, int16_t *dtab)
 {
     const int64_t cell = row_of(L, s, t);
+    // the C_2 operand first (the lane's own budget when it is out of reach)
+    const int ri = m - (int)r.wabar[s - 1];
+    const bool all_ok = m >= cw.gall[cell] && ri >= 0;
+    const int64_t below = row_of(L, s + 1, t) * pitch;
+    const typename P::Raw c2 = P::load(tab + below, cw.shadow + below, all_ok ? ri : m);
     typename P::Acc acc;
     P::init(acc);
     uint64_t prefix = 0;
-    relax_run<P>(acc, r, tab, cw.shadow, L, m, pitch, s, t - s, row_of(L, s, s) * pitch,
-                 row_of(L, s + 1, t) * pitch, prefix);
+    relax_run<P>(acc, r, tab, cw.shadow, L, m, pitch, s, t - s, row_of(L, s, s) * pitch, below, prefix);
     if (m < cw.gnone[cell])
         P::init(acc);
-    if (m >= cw.gall[cell]) {
-        const int ri = m - (int)r.wabar[s - 1];
-        if (ri >= 0) {
-            const int64_t below = row_of(L, s + 1, t) * pitch;
-            P::relax_all(acc, P::load(tab + below, cw.shadow + below, ri), (uint64_t)(r.uf[s - 1] + r.ub[s - 1]));
-        }
-    }
+    if (all_ok)
+        P::relax_all(acc, c2, (uint64_t)(r.uf[s - 1] + r.ub[s - 1]));
     store_cell<P>(tab, dtab, cw.shadow, cell * pitch + m, acc);
 }
 
@@ -701,32 +700,32 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
 // Splits are met in increasing order: low, then the stored middle partial,
 // then high.
 template <class P>
-__device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &cw, int L, int m, int64_t pitch, int s,
-                                 int t, int k_lo, int k_hi, int64_t *tab, int16_t *dtab)
+__device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &cw, int L, int m, int64_t pitch,
+                                          int s, int t, int k_lo, int k_hi, int64_t *tab, int16_t *dtab)
 {
     const int64_t cell = row_of(L, s, t);
+    // loads that depend on nothing go first: the stored middle partial and
+    // the C_2 operand (the lane's own budget when C_2 is out of reach)
+    const int64_t stored = load64(tab + cell * pitch, m);
+    const int ri = m - (int)r.wabar[s - 1];
+    const bool all_ok = m >= cw.gall[cell] && ri >= 0;
+    const int64_t below = row_of(L, s + 1, t) * pitch;
+    const typename P::Raw c2 = P::load(tab + below, cw.shadow + below, all_ok ? ri : m);
     typename P::Acc acc;
     P::init(acc);
     // low splits k = s .. k_lo - 1: X from block (I, I), Y from this block
     uint64_t prefix = 0;
-    relax_run<P>(acc, r, tab, cw.shadow, L, m, pitch, s, k_lo - s, row_of(L, s, s) * pitch,
-                 row_of(L, s + 1, t) * pitch, prefix);
+    relax_run<P>(acc, r, tab, cw.shadow, L, m, pitch, s, k_lo - s, row_of(L, s, s) * pitch, below, prefix);
     // middle splits: the stored partial counts u_f from k_lo on
-    P::merge_stored(acc, load64(tab + cell * pitch, m), prefix);
+    P::merge_stored(acc, stored, prefix);
     // high splits k = 16J + 1 .. t - 1: X from this block, Y from block (J, J)
     prefix += (uint64_t)(cw.pre[k_hi] - cw.pre[k_lo - 1]);
-    if (t > k_hi + 1)
-        relax_run<P>(acc, r, tab, cw.shadow, L, m, pitch, k_hi + 1, t - k_hi - 1, row_of(L, s, k_hi + 1) * pitch,
-                     row_of(L, k_hi + 2, t) * pitch, prefix);
+    relax_run<P>(acc, r, tab, cw.shadow, L, m, pitch, k_hi + 1, t - k_hi - 1, row_of(L, s, k_hi + 1) * pitch,
+                 row_of(L, k_hi + 2, t) * pitch, prefix);
     if (m < cw.gnone[cell])
         P::init(acc);
-    if (m >= cw.gall[cell]) {
-        const int ri = m - (int)r.wabar[s - 1];
-        if (ri >= 0) {
-            const int64_t below = row_of(L, s + 1, t) * pitch;
-            P::relax_all(acc, P::load(tab + below, cw.shadow + below, ri), (uint64_t)(r.uf[s - 1] + r.ub[s - 1]));
-        }
-    }
+    if (all_ok)
+        P::relax_all(acc, c2, (uint64_t)(r.uf[s - 1] + r.ub[s - 1]));
     store_cell<P>(tab, dtab, cw.shadow, cell * pitch + m, acc);
 }
 
