@@ -42,7 +42,7 @@
  * (s, t), 1 <= s <= t <= L, are stored s-major (by s, then t):
  *   row(s, t) = (s-1)*L - (s-1)*(s-2)/2 + (t-s)
  * Each row holds `pitch` elements, pitch = M+1 rounded up to a multiple of
- * 16 (128 bytes of costs); only columns 0..M are written.  The cost table is
+ * 32 (256 bytes of costs); only columns 0..M are written.  The cost table is
  * int64 and the decision table int16, with the same indexing:
  *   element(c, s, t, m) = (c * rows + row(s, t)) * pitch + m,
  *   rows = L(L+1)/2.

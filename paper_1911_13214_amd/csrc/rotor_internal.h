@@ -17,7 +17,10 @@ __host__ __device__ inline int64_t row_of(int L, int s, int t)
     return (int64_t)(s - 1) * L - (int64_t)(s - 1) * (s - 2) / 2 + (t - s);
 }
 
-__host__ __device__ inline int64_t pitch_of(int64_t M) { return (M + 1 + 15) / 16 * 16; }
+// Row pitch: M + 1 rounded up to 32 elements, so that every row of the int64
+// table starts 256 bytes and every row of the 4-byte compact copy 128 bytes
+// (one cache line) after an aligned table base.
+__host__ __device__ inline int64_t pitch_of(int64_t M) { return (M + 1 + 31) / 32 * 32; }
 
 // Everything one fill launch needs to address a batch of tables.
 struct Tables {

@@ -46,7 +46,7 @@ def test_status_strings():
 @pytest.mark.parametrize("n_chains,L,M", [(1, 1, 0), (1, 10, 100), (256, 64, 640), (1, 500, 5000), (3, 7, 15)])
 def test_layout(n_chains, L, M):
     pitch, rows, cb, db = rotor.rotor_layout(n_chains, L, M)
-    assert pitch >= M + 1 and pitch % 16 == 0 and pitch - (M + 1) < 16
+    assert pitch >= M + 1 and pitch % 32 == 0 and pitch - (M + 1) < 32
     assert rows == L * (L + 1) // 2
     assert cb == n_chains * rows * pitch * 8 and db == n_chains * rows * pitch * 2
 
