@@ -75,15 +75,16 @@ def arithmetic_type(params):
     return "u32" if bound < (1 << 30) else "int64"
 
 
-def traffic_if_current(kernel_class):
+def traffic_if_current(kernel_class, workload):
     """Measured HBM bytes per launch of a kernel class from the committed
-    counter summary, if it was taken on the current kernel source."""
+    counter summary, if it was taken on this workload and on the current
+    kernel source."""
     path = os.path.join(ROOT, "profiles", f"traffic_{kernel_class}_kernel.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
     sha = hashlib.sha256(open(FILL_SOURCE, "rb").read()).hexdigest()
-    if rec.get("fill_source_sha256") != sha:
+    if rec.get("fill_source_sha256") != sha or rec.get("bench_workload") != workload:
         return None
     return rec.get("bytes_per_launch")
 
@@ -203,7 +204,7 @@ def main():
         "config": {"workload": name, "L": L, "M": M, "n_chains": n_chains, "candidates_per_step": R,
                    "alg_bytes_per_step": alg_bytes},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic_if_current(dom),
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic_if_current(dom, name),
                      "kernel": f"{dom}_kernel", "launches_per_step": kd["launches"],
                      "avg_launch_us": kd["avg_launch_us"]},
         "kernels": kernels,

@@ -358,6 +358,36 @@ def test_batch_mixing_value_paths():
         assert_same(params, M, cost, dec, c)
 
 
+def test_fill_replays_from_a_captured_graph():
+    # the fill only enqueues kernels (no allocation, no memset, no host wait),
+    # so a caller may capture it; every replay, with eager work in between,
+    # must rebuild the same tables
+    import torch
+    from paper_1911_13214_amd import rotor
+    params, L, M, n, _ = chaingen.config(3)
+    say("graph replay resnet-like L=100 M=1000")
+    d_params = rotor.upload_params(params, M)
+    cost, dec = rotor.alloc_tables(n, L, M)
+    work = rotor.alloc_workspace(n, L, M)
+    st = torch.cuda.Stream()
+    st.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(st):
+        rotor.rotor_solve(d_params, n, L, M, cost, dec, work, st)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=st):
+        rotor.rotor_solve(d_params, n, L, M, cost, dec, work, st)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        cost.fill_(-7)
+        dec.fill_(-7)
+        work.fill_(-7)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert_same(params, M, cost, dec)
+
+
 def test_workspace_too_small_is_rejected():
     import torch
     from paper_1911_13214_amd import rotor
