@@ -85,6 +85,7 @@ extern "C" {
 #define ROTOR_INFEASIBLE (-4)   /* no sequence fits the budget: C(1, L, m) is infinite */
 #define ROTOR_ECAPACITY (-5)    /* the output array is too small; the count holds the size needed */
 #define ROTOR_ECORRUPT (-6)     /* the decision table is not one this library wrote */
+#define ROTOR_ESEQUENCE (-7)    /* an operation sequence is not valid (rotor_sequence_cost) */
 
 /* Rows of the packed parameter array. */
 #define ROTOR_ROW_UF 0
@@ -254,6 +255,30 @@ ROTOR_API int32_t rotor_store_all_peak(const int64_t *h_params, int32_t L, int64
  *   top >= 0, 1 <= n <= 2^20, budgets HOST [n] written.
  * Returns ROTOR_OK or ROTOR_EINVAL. */
 ROTOR_API int32_t rotor_even_budgets(int64_t top, int32_t n, int64_t *budgets);
+
+/* Time and peak memory of an operation sequence on the whole chain [1, L],
+ * replayed with the operation semantics of Table 1 (Section 3.1) and the
+ * memory accounting of Theorem 1 (Section 4.2): at the start the chain input
+ * a^0 (not counted) and the gradient delta^L are stored; a forward operation
+ * of stage l needs a^{l-1} (F_ck and F_all also accept abar^{l-1}), and F_none
+ * replaces a^{l-1} by its output; the peak of a forward is what is stored
+ * plus its output (abar^l for F_all, a^l otherwise) plus o_f^l; B^l needs
+ * delta^l, abar^l and a^{l-1} or abar^{l-1}, peaks at what is stored plus
+ * o_b^l, frees delta^l and abar^l (and a plain a^{l-1}) and stores
+ * delta^{l-1}; a^l and delta^l have size w_a^l, abar^l size w_abar^l, and the
+ * sequence must end with exactly delta^0 stored.  This is the prediction the
+ * DP makes for a sequence, e.g. one rotor_reconstruct returned, in the units
+ * of the parameters.
+ *
+ *   h_params  HOST, read only: [6][L] int64, one chain.
+ *   h_ops     HOST, read only: [n_ops] operations.
+ *   time, peak  HOST, written: sum of the operations' times, peak memory.
+ * Returns ROTOR_OK; ROTOR_EINVAL (null pointer, L out of range, n_ops < 0,
+ * an unknown kind or a stage outside 1..L); ROTOR_EDOMAIN (a negative
+ * parameter); ROTOR_ESEQUENCE if an operation's input is missing, a value is
+ * stored twice or anything but delta^0 is left at the end. */
+ROTOR_API int32_t rotor_sequence_cost(const int64_t *h_params, int32_t L, const rotor_op *h_ops, int64_t n_ops,
+                                      int64_t *time, int64_t *peak);
 
 #ifdef __cplusplus
 }

@@ -125,6 +125,7 @@ const char *rotor_status_string(int32_t status)
     case ROTOR_INFEASIBLE: return "no sequence fits the memory budget";
     case ROTOR_ECAPACITY: return "output array too small";
     case ROTOR_ECORRUPT: return "decision table inconsistent";
+    case ROTOR_ESEQUENCE: return "operation sequence not valid";
     default: return "unknown status";
     }
 }

@@ -1,7 +1,10 @@
 // Front end of the solver (host only): discretisation of memory sizes into
-// slots (Section 5.2), the memory of the schedule that stores everything, and
-// equally spaced budgets (the experimental setting of Section 5.3).
+// slots (Section 5.2), the memory of the schedule that stores everything,
+// equally spaced budgets (the experimental setting of Section 5.3), and the
+// time and memory the model predicts for an operation sequence.
 #include <stdint.h>
+
+#include <vector>
 
 #include "rotor_internal.h"
 
@@ -84,6 +87,68 @@ int32_t rotor_even_budgets(int64_t top, int32_t n, int64_t *budgets)
         return ROTOR_EINVAL;
     for (int32_t i = 1; i <= n; ++i)
         budgets[i - 1] = (int64_t)((unsigned __int128)(uint64_t)top * (uint64_t)i / (uint64_t)n);
+    return ROTOR_OK;
+}
+
+int32_t rotor_sequence_cost(const int64_t *h_params, int32_t L, const rotor_op *h_ops, int64_t n_ops,
+                            int64_t *time, int64_t *peak)
+{
+    if (!h_params || !time || !peak || L < 1 || L > ROTOR_MAX_L || n_ops < 0 || (n_ops > 0 && !h_ops))
+        return ROTOR_EINVAL;
+    for (int64_t i = 0; i < (int64_t)ROTOR_N_ROWS * L; ++i)
+        if (h_params[i] < 0)
+            return ROTOR_EDOMAIN;
+    for (int64_t i = 0; i < n_ops; ++i)
+        if (h_ops[i].kind < ROTOR_F_CK || h_ops[i].kind > ROTOR_B || h_ops[i].stage < 1 || h_ops[i].stage > L)
+            return ROTOR_EINVAL;
+    auto row = [&](int r, int l) { return h_params[(int64_t)r * L + (l - 1)]; };
+    // what is stored, per index l = 0..L; index 0 (a^0, delta^0) is not counted
+    std::vector<char> a(L + 1, 0), abar(L + 1, 0), delta(L + 1, 0);
+    auto size_a = [&](int l) { return l == 0 ? (int64_t)0 : row(ROTOR_ROW_WA, l); };
+    auto size_abar = [&](int l) { return row(ROTOR_ROW_WABAR, l); };
+    a[0] = 1;
+    delta[L] = 1;
+    int64_t mem = size_a(L), t_sum = 0, p_max = 0;
+    for (int64_t i = 0; i < n_ops; ++i) {
+        const int kind = h_ops[i].kind, l = h_ops[i].stage;
+        if (kind == ROTOR_B) {
+            if (!delta[l] || !abar[l] || !(a[l - 1] || abar[l - 1]))
+                return ROTOR_ESEQUENCE;
+            p_max = p_max > mem + row(ROTOR_ROW_OB, l) ? p_max : mem + row(ROTOR_ROW_OB, l);
+            t_sum += row(ROTOR_ROW_UB, l);
+            delta[l] = 0;
+            abar[l] = 0;
+            mem -= size_a(l) + size_abar(l);
+            if (!abar[l - 1] && a[l - 1]) {  // a plain input is consumed
+                a[l - 1] = 0;
+                mem -= size_a(l - 1);
+            }
+            if (delta[l - 1])
+                return ROTOR_ESEQUENCE;
+            delta[l - 1] = 1;
+            mem += size_a(l - 1);
+            continue;
+        }
+        const bool has_input = a[l - 1] || (kind != ROTOR_F_NONE && abar[l - 1]);
+        const bool all = kind == ROTOR_F_ALL;
+        if (!has_input || (all ? abar[l] : a[l]))
+            return ROTOR_ESEQUENCE;
+        const int64_t out = all ? size_abar(l) : size_a(l);
+        const int64_t here = mem + out + row(ROTOR_ROW_OF, l);
+        p_max = p_max > here ? p_max : here;
+        t_sum += row(ROTOR_ROW_UF, l);
+        if (kind == ROTOR_F_NONE) {
+            a[l - 1] = 0;
+            mem -= size_a(l - 1);
+        }
+        (all ? abar[l] : a[l]) = 1;
+        mem += out;
+    }
+    for (int l = 0; l <= L; ++l)
+        if (a[l] || abar[l] || delta[l] != (l == 0))
+            return ROTOR_ESEQUENCE;
+    *time = t_sum;
+    *peak = p_max;
     return ROTOR_OK;
 }
 

@@ -21,6 +21,7 @@ ROTOR_EDEVICE = -3
 ROTOR_INFEASIBLE = -4
 ROTOR_ECAPACITY = -5
 ROTOR_ECORRUPT = -6
+ROTOR_ESEQUENCE = -7
 ROTOR_INF = np.iinfo(np.int64).max
 F_CK, F_NONE, F_ALL, B = 0, 1, 2, 3
 N_ROWS = 6
@@ -43,6 +44,7 @@ SIGNATURES = {
     "rotor_discretize": (_i32, [_vp, _i32, _i32, _vp, _i64, _vp]),
     "rotor_store_all_peak": (_i32, [_vp, _i32, _P(_i64)]),
     "rotor_even_budgets": (_i32, [_i64, _i32, _vp]),
+    "rotor_sequence_cost": (_i32, [_vp, _i32, _vp, _i64, _P(_i64), _P(_i64)]),
 }
 
 KERNEL_CLASSES = ("leaf", "diag", "middle", "edge", "prep")
@@ -215,6 +217,21 @@ def rotor_even_budgets(top: int, n: int) -> np.ndarray:
     out = np.empty(n, dtype=np.int64) if n > 0 else np.empty(1, dtype=np.int64)
     _check(lib().rotor_even_budgets(top, n, out.ctypes.data), "rotor_even_budgets")
     return out
+
+
+def rotor_sequence_cost(params: np.ndarray, ops) -> tuple:
+    """(time, peak memory) the model predicts for the sequence ``ops`` (a list
+    of (kind, stage)) on one chain [6, L]."""
+    p = np.ascontiguousarray(params, dtype=np.int64)
+    if p.ndim == 3 and p.shape[0] == 1:
+        p = p[0]
+    if p.ndim != 2 or p.shape[0] != N_ROWS:
+        raise ValueError("params must be one chain [6, L]")
+    o = np.ascontiguousarray(np.asarray(ops, dtype=np.int32).reshape(-1, 2))
+    t, pk = ctypes.c_int64(), ctypes.c_int64()
+    _check(lib().rotor_sequence_cost(p.ctypes.data, p.shape[1], o.ctypes.data, o.shape[0], ctypes.byref(t),
+                                     ctypes.byref(pk)), "rotor_sequence_cost")
+    return t.value, pk.value
 
 
 # ---- conveniences (allocation and host copies only) -------------------------

@@ -38,7 +38,7 @@ def test_internal_symbols_are_hidden():
 
 
 def test_status_strings():
-    for code in (0, -1, -2, -3, -4, -5, -6):
+    for code in (0, -1, -2, -3, -4, -5, -6, -7):
         assert rotor.status_string(code) != "unknown status"
     assert rotor.status_string(42) == "unknown status"
 

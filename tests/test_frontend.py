@@ -123,3 +123,55 @@ def test_front_end_rejects_bad_input():
     for top, n in ((-1, 3), (5, 0), (5, (1 << 20) + 1)):
         with pytest.raises(rotor.RotorError):
             rotor.rotor_even_budgets(top, n)
+
+
+# ---- the model's prediction for a sequence (Table 1, Theorem 1) -----------
+
+def test_sequence_cost_matches_the_simulator_on_every_persistent_schedule():
+    # model.simulate is the independent Table-1 replay the brute-force pins use
+    rng = random.Random(3)
+    for L in range(1, 7):
+        for seed in range(4):
+            p = chaingen.random_chains(1, L, seed=rng.randint(0, 1 << 20))[0]
+            ch = model.Chain(p)
+            for _, ops in model.persistent_schedules(1, L):
+                assert rotor.rotor_sequence_cost(p, ops) == model.simulate(ch, 1, L, ops)
+
+
+def test_sequence_cost_of_reconstructed_sequences_is_the_table():
+    # the sequence Algorithm 2 rebuilds costs C(1, L, m) and fits in m
+    for seed in range(5):
+        L = 4 + seed
+        p = chaingen.random_chains(1, L, seed=seed)[0]
+        M = 60
+        C, _ = orc.solve(p, M)
+        top = orc.table_view(C, L)(1, L)
+        for m in range(0, M + 1, 7):
+            if top[m] == orc.INF:
+                continue
+            time, peak = rotor.rotor_sequence_cost(p, orc.reconstruct(p, M, C, m))
+            assert time == top[m] and peak <= m
+
+
+def test_sequence_cost_rejects_invalid_sequences():
+    p = chaingen.random_chains(1, 3, seed=1)[0]
+    F_CK, F_NONE, F_ALL, B = 0, 1, 2, 3
+    good = [(F_ALL, 1), (F_ALL, 2), (F_ALL, 3), (B, 3), (B, 2), (B, 1)]
+    assert rotor.rotor_sequence_cost(p, good) == model.simulate(model.Chain(p), 1, 3, good)
+    bad = [
+        good[:-1],                                                   # delta^1 left over
+        [(F_ALL, 2)] + good[1:],                                     # forward without its input
+        [(F_NONE, 1), (F_ALL, 1)] + good[1:],                        # a^0 consumed, then needed
+        [(F_ALL, 1), (F_ALL, 1)] + good[1:],                         # abar^1 stored twice
+        [(F_CK, 1), (F_ALL, 2), (F_ALL, 3), (B, 3), (B, 2), (B, 1)],  # B^1 without abar^1
+    ]
+    for ops in bad:
+        with pytest.raises(model.InvalidSequence):
+            model.simulate(model.Chain(p), 1, 3, ops)
+        with pytest.raises(rotor.RotorError) as e:
+            rotor.rotor_sequence_cost(p, ops)
+        assert e.value.status == rotor.ROTOR_ESEQUENCE
+    for ops in ([(4, 1)], [(F_ALL, 0)], [(F_ALL, 4)]):
+        with pytest.raises(rotor.RotorError) as e:
+            rotor.rotor_sequence_cost(p, ops)
+        assert e.value.status == rotor.ROTOR_EINVAL

@@ -1,0 +1,26 @@
+"""The executor on the GPU (Sections 5.1-5.4): parameters estimated from a
+synthetic chain, one table filled by the library, the sequences of ten
+budgets run through autograd.  Each sequence reproduces the plain gradients
+bit for bit, its measured peak memory stays within its budget and matches
+the model's prediction closely; the measured time follows the prediction."""
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+
+def test_sequences_run_within_budget_and_as_predicted():
+    from paper_1911_13214_amd import executor as ex
+    print("executor validate L=12 width=512 batch=2048", flush=True)
+    res = ex.validate(L=12, seed=3, width=512, batch=2048, slots=500, n_budgets=10, repeats=3)
+    ok = [r for r in res["rows"] if r["feasible"]]
+    assert len(ok) >= 4
+    assert res["all_gradients_equal"]
+    for r in ok:
+        assert r["predicted_bytes"] <= r["budget_bytes"]
+        # allocator slack: blocks are rounded to 512 bytes, plus the input gradient at the end
+        assert r["measured_bytes"] <= r["budget_bytes"] * 1.02 + (8 << 20), r
+    assert res["mape_memory"] < 0.03, res["mape_memory"]
+    assert res["mape_time"] < 0.30, res["mape_time"]
+    # less memory, more recomputation: the measured time never drops as the budget shrinks by much
+    times = [r["measured_us"] for r in ok]
+    assert times[0] >= times[-1] * 0.98
