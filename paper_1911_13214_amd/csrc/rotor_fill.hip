@@ -37,7 +37,8 @@
 // ...), the split points of a block fall in three ranges:
 //   middle  k in [16(I+1), 16J]: X in blocks (I, K) and Y in blocks (K, J)
 //           of smaller D -- all finished, the same range for every cell of
-//           the block: a register-tiled min-plus product (middle_kernel);
+//           the block: a register-tiled min-plus product (middle_packed_kernel,
+//           or middle_kernel for chains outside the packed keys);
 //   low     k in [s, 16(I+1) - 1]: Y is a cell of the same block further down;
 //   high    k in [16J + 1, t - 1]: X is a cell of the same block to the left.
 // The low and high ranges hold at most 30 splits per cell and are taken by

@@ -358,6 +358,36 @@ def test_batch_mixing_value_paths():
         assert_same(params, M, cost, dec, c)
 
 
+@pytest.mark.parametrize("L,M", [(5, (1 << 28) - 1), (20, (1 << 24) + 3)])
+def test_largest_budgets(L, M):
+    # M at the domain's limit: C(s, t, m) depends only on budgets up to m, and
+    # from the store-everything peak on it no longer changes, so the oracle
+    # at a small budget range gives every column exactly
+    import torch
+    from paper_1911_13214_amd import rotor
+    p = chaingen.random_chains(1, L, seed=L)
+    small = 2000
+    assert orc.store_all_peak(p[0]) < small
+    say(f"largest budgets L={L} M={M}")
+    d_params = rotor.upload_params(p, M)
+    cost, dec = rotor.alloc_tables(1, L, M)
+    work = rotor.alloc_workspace(1, L, M)
+    rotor.rotor_solve(d_params, 1, L, M, cost, dec, work)
+    torch.cuda.synchronize()
+    del work
+    C, D = orc.solve(p, small)
+    order = torch.as_tensor(gpu_rows_in_oracle_order(L), device="cuda")
+    g = torch.Generator().manual_seed(L)
+    cols = torch.cat([torch.arange(small + 1), torch.randint(small + 1, M + 1, (4000,), generator=g),
+                      torch.tensor([M - 1, M])]).cuda()
+    gc = cost[0][:, cols][order].cpu().numpy()
+    gd = dec[0][:, cols][order].cpu().numpy()
+    want = np.minimum(cols.cpu().numpy(), small)
+    assert np.array_equal(gc, C[:, want]) and np.array_equal(gd, D[:, want])
+    del cost, dec
+    torch.cuda.empty_cache()
+
+
 def test_fill_replays_from_a_captured_graph():
     # the fill only enqueues kernels (no allocation, no memset, no host wait),
     # so a caller may capture it; every replay, with eager work in between,
