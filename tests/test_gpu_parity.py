@@ -388,6 +388,33 @@ def test_largest_budgets(L, M):
     torch.cuda.empty_cache()
 
 
+def test_long_chain_windows():
+    # L = 4000: 8 million pairs, 250 blocks a side.  Small sizes keep the
+    # costs near 4e8, too large for packed keys once the middle range passes
+    # 8 splits, so the (value, split) middle path runs at scale.  Windows of
+    # 36 stages are solved by the oracle: C(s, t, .) depends on s..t only.
+    import torch
+    from paper_1911_13214_amd import rotor
+    L, M = 4000, 63
+    p = chaingen.random_chains(1, L, seed=11, wa_hi=1)
+    assert (1 << 26) < cost_bound(p[0]) < (1 << 30)
+    say(f"long chain L={L} M={M}")
+    _, cost, dec = solve_on_gpu(p, M)
+    for a in (1, 1983, 3965):
+        b = a + 35
+        C, D = orc.solve(np.ascontiguousarray(p[:, :, a - 1:b]), M)
+        pairs = [(s, t) for s in range(1, 37) for t in range(s, 37)]
+        rows = torch.tensor([rotor.rotor_row_index(L, s + a - 1, t + a - 1) for s, t in pairs], device="cuda")
+        gc = cost[0][rows][:, :M + 1].cpu().numpy()
+        gd = dec[0][rows][:, :M + 1].cpu().numpy().astype(np.int64)
+        want_c = np.stack([C[orc.row(36, s, t)] for s, t in pairs])
+        want_d = np.stack([D[orc.row(36, s, t)] for s, t in pairs]).astype(np.int64)
+        np.testing.assert_array_equal(gc, want_c)
+        np.testing.assert_array_equal(gd, np.where(want_d > 0, want_d + a - 1, want_d))
+    top = cost[0, rotor.rotor_row_index(L, 1, L), :M + 1].cpu().numpy()
+    assert np.all(top[1:] <= top[:-1]) and top[M] != orc.INF
+
+
 def test_fill_replays_from_a_captured_graph():
     # the fill only enqueues kernels (no allocation, no memset, no host wait),
     # so a caller may capture it; every replay, with eager work in between,
