@@ -53,6 +53,7 @@ namespace {
 constexpr int64_t kInf = INT64_MAX;
 constexpr int kT = 16;   // block side, in stages
 constexpr int kSub = 8;  // per-wave register tile side
+constexpr int kEdgeThreads = 128;  // budgets per edge workgroup (measured best of 64..512)
 constexpr uint32_t kAllSplit = 0xFFFF;  // split field of a C_2 candidate
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
 constexpr uint64_t kNarrowBound = 1ull << 30;
@@ -697,7 +698,7 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
 }
 
 // Edge splits, C_2 and the gates for the cells a + b = q of every block
-// (I, I + D) of one block-diagonal; a workgroup is one cell at 256 budgets.
+// (I, I + D) of one block-diagonal; a workgroup is one cell at 128 budgets.
 // Splits are met in increasing order: low, then the stored middle partial,
 // then high.
 template <class P>
@@ -730,7 +731,7 @@ __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &c
     store_cell<P>(tab, dtab, cw.shadow, cell * pitch + m, acc);
 }
 
-__global__ __launch_bounds__(256) void edge_kernel(const int64_t *__restrict__ params, int L, int M,
+__global__ __launch_bounds__(kEdgeThreads) void edge_kernel(const int64_t *__restrict__ params, int L, int M,
                                                    int64_t pitch, int64_t rows, int delta, int q, int a_min,
                                                    int n_q, int64_t *__restrict__ cost, int16_t *__restrict__ dec,
                                                    Work w)
@@ -742,7 +743,7 @@ __global__ __launch_bounds__(256) void edge_kernel(const int64_t *__restrict__ p
     const int J = I + delta;
     const int s = (I + 1) * kT - a;
     const int t = J * kT + 1 + (q - a);
-    const int m = blockIdx.x * 256 + threadIdx.x;
+    const int m = blockIdx.x * kEdgeThreads + threadIdx.x;
     if (t > L || m > M)
         return;
     const ChainRows r = chain_rows(params, L, c);
@@ -805,6 +806,7 @@ hipError_t launch_fill(const Tables &tb, const Work &w, hipStream_t stream, Laun
     const uint64_t nc = (uint64_t)tb.n_chains;
     const unsigned mb256 = (unsigned)((tb.M + 1 + 255) / 256);
     const unsigned mb64 = (unsigned)((tb.M + 1 + 63) / 64);
+    const unsigned mb_edge = (unsigned)((tb.M + kEdgeThreads) / kEdgeThreads);
     auto launched = [&](KernelClass k, uint64_t c1, uint64_t c2, uint64_t cells) -> hipError_t {
         hipError_t e = check();
         if (e == hipSuccess && obs)
@@ -864,7 +866,7 @@ hipError_t launch_fill(const Tables &tb, const Work &w, hipStream_t stream, Laun
                     cells += ((I + delta) * kT + 1 + (q - a) <= L) ? 1 : 0;
             if ((e = before(kEdge)) != hipSuccess)
                 return e;
-            edge_kernel<<<dim3(mb256, (nb - delta) * n_q, tb.n_chains), 256, 0, stream>>>(
+            edge_kernel<<<dim3(mb_edge, (nb - delta) * n_q, tb.n_chains), kEdgeThreads, 0, stream>>>(
                 tb.params, L, tb.M, tb.pitch, tb.rows, delta, q, a_min, n_q, tb.cost, tb.dec, w);
             if ((e = launched(kEdge, cells * (uint64_t)q, cells, cells)) != hipSuccess)
                 return e;
