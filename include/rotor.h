@@ -162,6 +162,26 @@ ROTOR_API int32_t rotor_workspace_bytes(int32_t n_chains, int32_t L, int64_t M, 
 ROTOR_API int32_t rotor_solve(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
                               int16_t *d_dec, void *d_work, uint64_t work_bytes, void *stream);
 
+/* Fill orders of rotor_solve_schedule.  Both fill the same tables, bit for
+ * bit; they differ in speed.
+ *   ROTOR_SCHEDULE_BLOCKED   16 x 16 blocks of pairs: register-tiled min-plus
+ *                            products for the splits that reach across
+ *                            blocks, 31 short launches per block-diagonal for
+ *                            the others; the fast order for large tables.
+ *   ROTOR_SCHEDULE_DIAGONAL  one launch per t - s, every split of a pair in
+ *                            one pass (the wavefront the recurrence allows);
+ *                            fewer launches, the fast order for small tables.
+ *   ROTOR_SCHEDULE_AUTO      DIAGONAL when L <= 112 and the table has at most
+ *                            3e8 candidates, BLOCKED otherwise (rotor_solve). */
+#define ROTOR_SCHEDULE_AUTO 0
+#define ROTOR_SCHEDULE_BLOCKED 1
+#define ROTOR_SCHEDULE_DIAGONAL 2
+
+/* rotor_solve with an explicit fill order; ROTOR_EINVAL for an unknown one. */
+ROTOR_API int32_t rotor_solve_schedule(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M,
+                                       int64_t *d_cost, int16_t *d_dec, void *d_work, uint64_t work_bytes,
+                                       void *stream, int32_t schedule);
+
 /* Kernel classes of the fill, for rotor_solve_timed. */
 #define ROTOR_KERNEL_LEAF 0   /* single-stage cells, Eq. (DP:Init) */
 #define ROTOR_KERNEL_DIAG 1   /* pairs inside one 16-stage diagonal block, all splits */

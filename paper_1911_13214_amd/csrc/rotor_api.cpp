@@ -200,7 +200,18 @@ int32_t rotor_solve(const int64_t *d_params, int32_t n_chains, int32_t L, int64_
         return ROTOR_EINVAL;
     const Tables tb = make_tables(d_params, n_chains, L, M, d_cost, d_dec);
     const Work w = work_view(d_work, n_chains, L, tb.pitch);
-    return launch_fill(tb, w, (hipStream_t)stream) == hipSuccess ? ROTOR_OK : ROTOR_EDEVICE;
+    return launch_fill(tb, w, ROTOR_SCHEDULE_AUTO, (hipStream_t)stream) == hipSuccess ? ROTOR_OK : ROTOR_EDEVICE;
+}
+
+int32_t rotor_solve_schedule(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
+                             int16_t *d_dec, void *d_work, uint64_t work_bytes, void *stream, int32_t schedule)
+{
+    if (schedule < ROTOR_SCHEDULE_AUTO || schedule > ROTOR_SCHEDULE_DIAGONAL ||
+        !solve_args_ok(d_params, n_chains, L, M, d_cost, d_dec, d_work, work_bytes))
+        return ROTOR_EINVAL;
+    const Tables tb = make_tables(d_params, n_chains, L, M, d_cost, d_dec);
+    const Work w = work_view(d_work, n_chains, L, tb.pitch);
+    return launch_fill(tb, w, schedule, (hipStream_t)stream) == hipSuccess ? ROTOR_OK : ROTOR_EDEVICE;
 }
 
 int32_t rotor_solve_timed(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
@@ -212,7 +223,7 @@ int32_t rotor_solve_timed(const int64_t *d_params, int32_t n_chains, int32_t L, 
     const Tables tb = make_tables(d_params, n_chains, L, M, d_cost, d_dec);
     const Work w = work_view(d_work, n_chains, L, tb.pitch);
     TimingObserver obs(stats);
-    hipError_t e = launch_fill(tb, w, (hipStream_t)stream, &obs);
+    hipError_t e = launch_fill(tb, w, ROTOR_SCHEDULE_AUTO, (hipStream_t)stream, &obs);
     const hipError_t f = obs.finish((hipStream_t)stream);
     return (e == hipSuccess && f == hipSuccess) ? ROTOR_OK : ROTOR_EDEVICE;
 }

@@ -54,6 +54,10 @@ constexpr int64_t kInf = INT64_MAX;
 constexpr int kT = 16;   // block side, in stages
 constexpr int kSub = 8;  // per-wave register tile side
 constexpr int kEdgeThreads = 128;  // budgets per edge workgroup (measured best of 64..512)
+// The automatic schedule fills small tables diagonal by diagonal (measured
+// on MI355X: faster up to about these sizes, slower beyond).
+constexpr int kStreamMaxL = 112;
+constexpr uint64_t kStreamMaxCandidates = 300000000ull;
 constexpr uint32_t kAllSplit = 0xFFFF;  // split field of a C_2 candidate
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
 constexpr uint64_t kNarrowBound = 1ull << 30;
@@ -398,12 +402,12 @@ __device__ __forceinline__ void relax_run(typename P::Acc &acc, const ChainRows 
     RelaxRun<P, kT - 1>::go(n, acc, r, tab, shadow, L, m, pitch, k0, xrow, yrow, prefix);
 }
 
-// Eq. (DP:mainrec) for the pairs (s, s + d) inside one diagonal block, all
-// splits in one pass.  Rows (s, s'-1) are consecutive; the row of (s'+1, t)
-// is L - s' rows after the row of (s', t).
+// Eq. (DP:mainrec) for one pair (s, t), all splits in straight-line runs of
+// up to kT - 1.  Rows (s, s'-1) are consecutive; the row of (s'+1, t) is
+// L - s' rows after the row of (s', t).
 template <class P>
-__device__ __forceinline__ void diag_body(const ChainRows &r, const ChainWork &cw, int L, int m, int64_t pitch, int s,
-                                 int t, int64_t *tab, int16_t *dtab)
+__device__ __forceinline__ void diag_body(const ChainRows &r, const ChainWork &cw, int L, int m, int64_t pitch,
+                                          int s, int t, int64_t *tab, int16_t *dtab)
 {
     const int64_t cell = row_of(L, s, t);
     // the C_2 operand first (the lane's own budget when it is out of reach)
@@ -414,7 +418,11 @@ __device__ __forceinline__ void diag_body(const ChainRows &r, const ChainWork &c
     typename P::Acc acc;
     P::init(acc);
     uint64_t prefix = 0;
-    relax_run<P>(acc, r, tab, cw.shadow, L, m, pitch, s, t - s, row_of(L, s, s) * pitch, below, prefix);
+    for (int k0 = s; k0 < t; k0 += kT - 1) {
+        const int n = min(kT - 1, t - k0);
+        relax_run<P>(acc, r, tab, cw.shadow, L, m, pitch, k0, n, row_of(L, s, k0) * pitch,
+                     row_of(L, k0 + 1, t) * pitch, prefix);
+    }
     if (m < cw.gnone[cell])
         P::init(acc);
     if (all_ok)
@@ -422,14 +430,16 @@ __device__ __forceinline__ void diag_body(const ChainRows &r, const ChainWork &c
     store_cell<P>(tab, dtab, cw.shadow, cell * pitch + m, acc);
 }
 
+// The pairs (s, s + d): inside the 16 x 16 diagonal blocks only (blocked
+// fill), or all of them (streamed fill of a small table, one launch per d).
 __global__ __launch_bounds__(256) void diag_kernel(const int64_t *__restrict__ params, int L, int M,
-                                                   int64_t pitch, int64_t rows, int d, int64_t *__restrict__ cost,
-                                                   int16_t *__restrict__ dec, Work w)
+                                                   int64_t pitch, int64_t rows, int d, int whole,
+                                                   int64_t *__restrict__ cost, int16_t *__restrict__ dec, Work w)
 {
     const int c = blockIdx.z;
     const int s = blockIdx.y + 1;
     const int t = s + d;
-    if ((s - 1) / kT != (t - 1) / kT)
+    if (!whole && (s - 1) / kT != (t - 1) / kT)
         return;
     const int m = blockIdx.x * 256 + threadIdx.x;
     if (m > M)
@@ -799,7 +809,7 @@ Work work_view(void *base, int n_chains, int L, int64_t pitch)
     return w;
 }
 
-hipError_t launch_fill(const Tables &tb, const Work &w, hipStream_t stream, LaunchObserver *obs)
+hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_t stream, LaunchObserver *obs)
 {
     const int L = tb.L;
     const uint64_t W = (uint64_t)tb.M + 1;
@@ -827,16 +837,22 @@ hipError_t launch_fill(const Tables &tb, const Work &w, hipStream_t stream, Laun
                                                                  tb.dec, w);
     if ((e = launched(kLeaf, 0, 0, (uint64_t)L)) != hipSuccess)
         return e;
-    // diagonal blocks
-    for (int d = 1; d < kT && d < L; ++d) {
+    // A small table goes diagonal by diagonal: its launches are few and
+    // short, and the blocked fill would need 33 per block-diagonal.
+    const uint64_t r_total = ((uint64_t)L * L * L / 6) * W * nc;
+    const bool streamed = schedule == ROTOR_SCHEDULE_DIAGONAL ||
+                          (schedule == ROTOR_SCHEDULE_AUTO && L <= kStreamMaxL && r_total <= kStreamMaxCandidates);
+    for (int d = 1; d < (streamed ? L : kT) && d < L; ++d) {
         if ((e = before(kDiag)) != hipSuccess)
             return e;
         diag_kernel<<<dim3(mb256, L - d, tb.n_chains), 256, 0, stream>>>(tb.params, L, tb.M, tb.pitch, tb.rows, d,
-                                                                         tb.cost, tb.dec, w);
-        const uint64_t pairs = in_block_pairs(L, d);
+                                                                         streamed ? 1 : 0, tb.cost, tb.dec, w);
+        const uint64_t pairs = streamed ? (uint64_t)(L - d) : in_block_pairs(L, d);
         if ((e = launched(kDiag, pairs * d, pairs, pairs)) != hipSuccess)
             return e;
     }
+    if (streamed)
+        return hipSuccess;
     const int nb = (L + kT - 1) / kT;
     for (int delta = 1; delta < nb; ++delta) {
         // pairs of the block-diagonal: full rows of 16, columns up to L

@@ -70,8 +70,10 @@ struct LaunchObserver {
     virtual ~LaunchObserver() {}
 };
 
-// Enqueue the whole table fill on `stream`.  Returns a HIP error code.
-hipError_t launch_fill(const Tables &tb, const Work &w, hipStream_t stream, LaunchObserver *obs = nullptr);
+// Enqueue the whole table fill on `stream` with one of the ROTOR_SCHEDULE_*
+// orders.  Returns a HIP error code.
+hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_t stream,
+                       LaunchObserver *obs = nullptr);
 
 // Enqueue the sequence walk (one workgroup per budget).
 hipError_t launch_reconstruct(const int64_t *params, int L, int M, int64_t pitch, int64_t rows,

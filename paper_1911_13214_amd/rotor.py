@@ -39,6 +39,7 @@ SIGNATURES = {
     "rotor_check_params": (_i32, [_vp, _i32, _i32, _i64]),
     "rotor_workspace_bytes": (_i32, [_i32, _i32, _i64, _P(_u64)]),
     "rotor_solve": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp, _u64, _vp]),
+    "rotor_solve_schedule": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp, _u64, _vp, _i32]),
     "rotor_reconstruct": (_i32, [_vp, _i32, _i32, _i64, _vp, _i32, _i32, _vp, _i64, _vp, _vp, _vp, _vp]),
     "rotor_solve_timed": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp, _u64, _vp, _vp]),
     "rotor_discretize": (_i32, [_vp, _i32, _i32, _vp, _i64, _vp]),
@@ -48,6 +49,7 @@ SIGNATURES = {
 }
 
 KERNEL_CLASSES = ("leaf", "diag", "middle", "edge", "prep")
+SCHEDULES = {"auto": 0, "blocked": 1, "diagonal": 2}
 
 
 class KernelStats(ctypes.Structure):
@@ -154,6 +156,15 @@ def rotor_solve(d_params, n_chains: int, L: int, M: int, d_cost, d_dec, d_work, 
     tensor of at least rotor_workspace_bytes."""
     p, c, d, w, wb = _solve_ptrs(d_params, n_chains, L, M, d_cost, d_dec, d_work)
     _check(lib().rotor_solve(p, n_chains, L, M, c, d, w, wb, _stream_ptr(stream)), "rotor_solve")
+
+
+def rotor_solve_schedule(d_params, n_chains: int, L: int, M: int, d_cost, d_dec, d_work, schedule: str,
+                         stream=None):
+    """rotor_solve with an explicit fill order: "auto", "blocked" or
+    "diagonal" (same tables, different speed)."""
+    p, c, d, w, wb = _solve_ptrs(d_params, n_chains, L, M, d_cost, d_dec, d_work)
+    _check(lib().rotor_solve_schedule(p, n_chains, L, M, c, d, w, wb, _stream_ptr(stream), SCHEDULES[schedule]),
+           "rotor_solve_schedule")
 
 
 def rotor_solve_timed(d_params, n_chains: int, L: int, M: int, d_cost, d_dec, d_work, stream=None):
@@ -263,7 +274,7 @@ def alloc_workspace(n_chains: int, L: int, M: int, device="cuda"):
     return torch.empty(((rotor_workspace_bytes(n_chains, L, M) + 7) // 8,), dtype=torch.int64, device=device)
 
 
-def solve(params: np.ndarray, M: int, device="cuda", stream=None):
+def solve(params: np.ndarray, M: int, device="cuda", stream=None, schedule: str = "auto"):
     """Upload, allocate and fill.  Returns (d_params, cost, dec) device
     tensors; the fill is enqueued on ``stream`` (the workspace is released to
     torch's caching allocator on that stream)."""
@@ -274,7 +285,7 @@ def solve(params: np.ndarray, M: int, device="cuda", stream=None):
     d_params = upload_params(p, M, device)
     cost, dec = alloc_tables(n_chains, L, M, device)
     work = alloc_workspace(n_chains, L, M, device)
-    rotor_solve(d_params, n_chains, L, M, cost, dec, work, stream)
+    rotor_solve_schedule(d_params, n_chains, L, M, cost, dec, work, schedule, stream)
     if stream is not None:
         work.record_stream(stream)
     return d_params, cost, dec

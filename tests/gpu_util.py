@@ -21,12 +21,12 @@ def gpu_rows_in_oracle_order(L: int) -> np.ndarray:
     return idx
 
 
-def solve_on_gpu(params, M, stream=None):
+def solve_on_gpu(params, M, stream=None, schedule="auto"):
     import torch
 
     from paper_1911_13214_amd import rotor
 
-    d_params, cost, dec = rotor.solve(params, M, device="cuda", stream=stream)
+    d_params, cost, dec = rotor.solve(params, M, device="cuda", stream=stream, schedule=schedule)
     torch.cuda.synchronize()
     return d_params, cost, dec
 

@@ -20,9 +20,24 @@ def say(msg):
     print(msg, flush=True)
 
 
+SCHEDULES = ["blocked", "diagonal"]
+_oracle_cache = {}
+
+
+def oracle_tables(params, M):
+    """The oracle's tables of one chain, kept for the next schedule's run of
+    the same case."""
+    key = (params.tobytes(), params.shape, M)
+    if key not in _oracle_cache:
+        if len(_oracle_cache) > 8:
+            _oracle_cache.clear()
+        _oracle_cache[key] = orc.solve(params, M)
+    return _oracle_cache[key]
+
+
 def assert_same(params, M, cost, dec, c=0, order=None):
     L = params.shape[-1]
-    C, D = orc.solve(params[c:c + 1] if params.ndim == 3 else params, M)
+    C, D = oracle_tables(params[c:c + 1] if params.ndim == 3 else params, M)
     gc, gd = chain_tables(cost, dec, c, L, M, order)
     if not np.array_equal(gc, C):
         bad = np.argwhere(gc != C)[0]
@@ -34,18 +49,20 @@ def assert_same(params, M, cost, dec, c=0, order=None):
                              f"oracle {D[tuple(bad)]}")
 
 
+@pytest.mark.parametrize("schedule", SCHEDULES)
 @pytest.mark.parametrize("cfg", [1, 2, 3])
-def test_parity_full_tables(cfg):
+def test_parity_full_tables(cfg, schedule):
     params, L, M, _, name = chaingen.config(cfg)
-    say(f"parity {name}")
-    _, cost, dec = solve_on_gpu(params, M)
+    say(f"parity {name} {schedule}")
+    _, cost, dec = solve_on_gpu(params, M, schedule=schedule)
     assert_same(params, M, cost, dec)
 
 
-def test_parity_batch_256_chains():
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_parity_batch_256_chains(schedule):
     params, L, M, n, name = chaingen.config(4)
-    say(f"parity {name}")
-    _, cost, dec = solve_on_gpu(params, M)
+    say(f"parity {name} {schedule}")
+    _, cost, dec = solve_on_gpu(params, M, schedule=schedule)
     order = gpu_rows_in_oracle_order(L)
     for c in list(range(0, n, 17)) + [n - 1]:
         assert_same(params, M, cost, dec, c, order)
@@ -54,11 +71,12 @@ def test_parity_batch_256_chains():
     assert hc == str(g["hash_cost"]) and hd == str(g["hash_dec"])
 
 
-def test_parity_large_chain():
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_parity_large_chain(schedule):
     params, L, M, _, name = chaingen.config(5)
-    say(f"parity {name}")
+    say(f"parity {name} {schedule}")
     g = np.load(os.path.join(GOLDEN, "random_L500_M5000.npz"))
-    _, cost, dec = solve_on_gpu(params, M)
+    _, cost, dec = solve_on_gpu(params, M, schedule=schedule)
     order = gpu_rows_in_oracle_order(L)
     top = order[orc.row(L, 1, L)]
     np.testing.assert_array_equal(cost[0, top, :M + 1].cpu().numpy(), g["top_cost"])
@@ -89,30 +107,33 @@ def test_parity_large_chain():
 
 @pytest.mark.parametrize("L,M,seed", [(1, 0, 1), (1, 37, 2), (2, 15, 3), (3, 16, 4), (5, 1, 9), (17, 255, 5),
                                       (33, 257, 6), (40, 1023, 7), (64, 300, 8)])
-def test_edge_shapes(L, M, seed):
-    say(f"edge L={L} M={M}")
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_edge_shapes(L, M, seed, schedule):
+    say(f"edge L={L} M={M} {schedule}")
     params = chaingen.random_chains(1, L, seed=seed)
-    _, cost, dec = solve_on_gpu(params, M)
+    _, cost, dec = solve_on_gpu(params, M, schedule=schedule)
     assert_same(params, M, cost, dec)
 
 
-def test_tiny_and_wide_chains():
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_tiny_and_wide_chains(schedule):
     for seed in range(40):
         p = tiny_chain(seed)
-        _, cost, dec = solve_on_gpu(p, TINY_M)
+        _, cost, dec = solve_on_gpu(p, TINY_M, schedule=schedule)
         assert_same(p, TINY_M, cost, dec)
     for seed in range(6):
         p = wide_chain(seed, L=12, size_hi=40, over_hi=30)
-        _, cost, dec = solve_on_gpu(p, 400)
+        _, cost, dec = solve_on_gpu(p, 400, schedule=schedule)
         assert_same(p, 400, cost, dec)
 
 
-def test_shifts_beyond_the_budget():
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_shifts_beyond_the_budget(schedule):
     # sizes larger than M: every shifted read falls below budget 0
     p = chaingen.random_chains(1, 9, seed=12)
     p[0, 2, ::2] += 300
     p[0, 3, ::3] += 500
-    _, cost, dec = solve_on_gpu(p, 200)
+    _, cost, dec = solve_on_gpu(p, 200, schedule=schedule)
     assert_same(p, 200, cost, dec)
 
 
@@ -322,11 +343,12 @@ def wide_costs_chain(seed, L):
     return p
 
 
+@pytest.mark.parametrize("schedule", SCHEDULES)
 @pytest.mark.parametrize("L,M,seed", [(5, 60, 1), (23, 230, 2), (40, 400, 3), (70, 300, 4)])
-def test_wide_value_path(L, M, seed):
+def test_wide_value_path(L, M, seed, schedule):
     p = wide_costs_chain(seed, L)
-    say(f"wide L={L} M={M}")
-    _, cost, dec = solve_on_gpu(p, M)
+    say(f"wide L={L} M={M} {schedule}")
+    _, cost, dec = solve_on_gpu(p, M, schedule=schedule)
     assert_same(p, M, cost, dec)
 
 
@@ -339,11 +361,12 @@ def test_narrow_chain_beyond_packed_keys(L, M, seed):
     v = cost_bound(p[0])
     assert (1 << 26) < v < (1 << 30)
     say(f"narrow beyond packed L={L} M={M} bound={v}")
-    _, cost, dec = solve_on_gpu(p, M)
+    _, cost, dec = solve_on_gpu(p, M, schedule="blocked")
     assert_same(p, M, cost, dec)
 
 
-def test_batch_mixing_value_paths():
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_batch_mixing_value_paths(schedule):
     # chains of one call may take different value paths
     params = chaingen.random_chains(6, 37, seed=21)
     for c in (1, 4):
@@ -353,7 +376,7 @@ def test_batch_mixing_value_paths():
     params[2, 1] *= 1 << 13
     assert cost_bound(params[1]) >= 1 << 30 and (1 << 27) < cost_bound(params[2]) < (1 << 30)
     M = 200
-    _, cost, dec = solve_on_gpu(params, M)
+    _, cost, dec = solve_on_gpu(params, M, schedule=schedule)
     for c in range(6):
         assert_same(params, M, cost, dec, c)
 
