@@ -601,8 +601,8 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
         middle_body<Wide>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, tab);
 }
 
-// Packed middle products (same blocks, workgroups and tiling as
-// middle_kernel).  With S the bit width of k - k_lo, a loaded value v becomes
+// Packed middle products (same blocks, workgroups and register tiles as
+// middle_kernel, operands staged in LDS).  With S the bit width of k - k_lo, a loaded value v becomes
 // v << S by a rotation that leaves 0xFFFFFFFF (infinity) unchanged; X also
 // gets (prefix << S) | (k - k_lo) by a saturating add, Y nothing more, so a
 // candidate is sat(x + y) and the minimum key is the smallest value with,
@@ -611,55 +611,134 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
 // format (value << 32) | s' that edge_kernel merges.
 __device__ inline uint32_t rot_left(uint32_t v, int S) { return __builtin_amdgcn_alignbit(v, v, (32 - S) & 31); }
 
-__device__ inline void packed_update(uint32_t (&acc)[kSub][kSub], const uint32_t (&rx)[kSub],
-                                     const uint32_t (&ry)[kSub], uint32_t add, int S)
+// Workgroups are handed to the 8 XCDs in turn (workgroup b of the grid, x
+// fastest, to XCD b mod 8), and each XCD has its own L2.  xcd_tile renumbers
+// them so that each XCD runs a contiguous range of tiles: neighbouring budget
+// chunks of one pair range, whose shifted reads share cache lines, then meet
+// in the same L2.
+constexpr int kXcds = 8;
+struct Tile {
+    int x, y, z;
+};
+__device__ inline Tile xcd_tile()
 {
-    uint32_t x[kSub], y[kSub];
-#pragma unroll
-    for (int i = 0; i < kSub; ++i)
-        x[i] = sat_add(rot_left(rx[i], S), add);
-#pragma unroll
-    for (int j = 0; j < kSub; ++j)
-        y[j] = rot_left(ry[j], S);
-#pragma unroll
-    for (int i = 0; i < kSub; ++i)
-#pragma unroll
-        for (int j = 0; j < kSub; ++j)
-            acc[i][j] = min(acc[i][j], sat_add(x[i], y[j]));
+    const int nx = gridDim.x, ny = gridDim.y;
+    const int n = nx * ny * gridDim.z;
+    const int b = (blockIdx.z * ny + blockIdx.y) * nx + blockIdx.x;
+    const int xcd = b % kXcds, slot = b / kXcds;
+    const int q = n / kXcds, r = n % kXcds;
+    const int id = xcd < r ? xcd * (q + 1) + slot : r * (q + 1) + (xcd - r) * q + slot;
+    return {id % nx, (id / nx) % ny, id / (nx * ny)};
+}
+
+// The packed kernel stages its operands in LDS.  A stage is kStage splits;
+// for each, a slot holds the block's 16 X rows and 16 Y rows at the
+// workgroup's 64 budgets (8 KB).  A ring of kRing stages keeps the next
+// stage in flight while the current one is relaxed.  Each wave copies 8 of
+// the 32 rows of a split straight from global memory into LDS
+// (global_load_lds_dword, no registers held), so each row is fetched once
+// per workgroup instead of once per wave that uses it; the waves read their
+// 8 + 8 operands from LDS.  Two splits per stage let one three-way unsigned
+// min fold two candidates into an accumulator.  Measured on MI355X: a ring
+// of two such stages (32 KB, four workgroups per CU) beats deeper rings and
+// single-split stages.
+constexpr int kStage = 2;
+constexpr int kRing = 2;
+constexpr int kSplitWords = 2 * kT * 64;
+constexpr int kDmaPerSplit = 8;  // row copies per wave and split
+constexpr int kDmaPerStage = kDmaPerSplit * kStage;
+static_assert(kRing >= 2 && (kRing - 2) * kDmaPerStage <= 63, "vmcnt holds at most 63");
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef const __attribute__((address_space(1))) void global_void;
+
+// Wait until at most N of this wave's vector memory operations are
+// outstanding and its LDS reads are done, then meet the workgroup.
+template <int N>
+__device__ __forceinline__ void ring_barrier()
+{
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
+// ring_barrier leaving the copies of the next `later` stages outstanding
+// (later uniform, at most kRing - 2)
+template <int A>
+__device__ __forceinline__ void ring_wait(int later)
+{
+    if constexpr (A == 0) {
+        ring_barrier<0>();
+    } else {
+        if (later >= A)
+            ring_barrier<A * kDmaPerStage>();
+        else
+            ring_wait<A - 1>(later);
+    }
 }
 
 __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__restrict__ params, int L, int M,
                                                             int64_t pitch, int64_t rows, int delta,
                                                             int64_t *__restrict__ cost, Work w)
 {
-    const int c = blockIdx.z;
-    const int I = blockIdx.y;
+    __shared__ uint32_t ring[kRing * kStage * kSplitWords];
+    const Tile tile = xcd_tile();
+    const int c = tile.z;
+    const int I = tile.y;
     const int J = I + delta;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int m = blockIdx.x * 64 + (threadIdx.x & 63);
-    const int s0 = I * kT + (wave >> 1) * kSub + 1;
-    const int t0 = J * kT + (wave & 1) * kSub + 1;
+    const int lane = threadIdx.x & 63;
+    const int m = tile.x * 64 + lane;
     const int k_lo = (I + 1) * kT;
     const int k_hi = J * kT;
-    if (t0 > L || !middle_packed(w.flags[c], k_hi - k_lo))
+    // uniform over the workgroup: every wave returns or none does
+    if (!middle_packed(w.flags[c], k_hi - k_lo))
         return;
-    const int nt = min(kSub, L - t0 + 1);
+    const int s0 = I * kT + (wave >> 1) * kSub + 1;
+    const int t0 = J * kT + (wave & 1) * kSub + 1;
+    const int nt = t0 <= L ? min(kSub, L - t0 + 1) : 0;
     const int S = k_hi > k_lo ? 32 - __clz(k_hi - k_lo) : 0;
     const ChainRows r = chain_rows(params, L, c);
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
+    const int mc = m <= M ? m : M;
+    const int n_stages = (k_hi - k_lo + kStage) / kStage;
 
-    MiddleTile<Narrow> tl;
+    // rows this wave copies: waves 0, 1 the X rows (s, k) of s = 16I+1+8w ..,
+    // waves 2, 3 the Y rows (k+1, t) of t = 16J+1+8(w-2) .. (past L: row L)
+    const bool copies_x = wave < 2;
+    const int first = copies_x ? I * kT + 1 + wave * kSub : J * kT + 1 + (wave - 2) * kSub;
+    const char *src[kDmaPerSplit];  // each copied row at the next split to copy
 #pragma unroll
-    for (int i = 0; i < kSub; ++i)
-        tl.xrow[i] = row_of(L, s0 + i, k_lo) * pitch;
+    for (int i = 0; i < kDmaPerSplit; ++i)
+        src[i] = (const char *)(cw.shadow + (copies_x ? row_of(L, first + i, k_lo) * pitch
+                                                      : row_of(L, k_lo + 1, min(first + i, L)) * pitch));
+    const int64_t row_bytes = pitch * 4;
+    int k_copy = k_lo;  // next split to copy
+    uint32_t *const dst0 = ring + (copies_x ? wave * kSub : kT + (wave - 2) * kSub) * 64;
+    int fill = 0;  // ring stage filled next
+    // copies of one stage; splits past k_hi copy split k_hi again, so every
+    // stage issues the same number of copies
+    auto issue = [&]() {
+        uint32_t *dst = dst0 + fill * (kStage * kSplitWords);
 #pragma unroll
-    for (int j = 0; j < kSub; ++j)
-        tl.ystep[j] = (int64_t)(j < nt ? j : nt - 1) * pitch;  // columns past L read the last one
-    tl.yrow = row_of(L, k_lo + 1, t0) * pitch;
-    tl.tab = tab;
-    tl.shadow = cw.shadow;
-    tl.mc = m <= M ? m : M;
+        for (int p = 0; p < kStage; ++p) {
+            const int k = k_copy;
+            const int ri = mc - (int)r.wa[k - 1];
+            const uint32_t off = 4u * (uint32_t)(copies_x ? mc : (ri >= 0 ? ri : mc));
+#pragma unroll
+            for (int i = 0; i < kDmaPerSplit; ++i)
+                __builtin_amdgcn_global_load_lds((global_void *)(src[i] + off),
+                                                 (lds_void *)(dst + p * kSplitWords + i * 64), 4, 0, 0);
+            if (k < k_hi) {
+                // to split k + 1: X rows advance one row, Y rows L - k - 1 rows
+                const int64_t step = copies_x ? row_bytes : (int64_t)(L - k - 1) * row_bytes;
+#pragma unroll
+                for (int i = 0; i < kDmaPerSplit; ++i)
+                    src[i] += step;
+                ++k_copy;
+            }
+        }
+        fill = fill + 1 == kRing ? 0 : fill + 1;
+    };
 
     uint32_t acc[kSub][kSub];
 #pragma unroll
@@ -668,31 +747,48 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
         for (int j = 0; j < kSub; ++j)
             acc[i][j] = kInf32;
 
+#pragma unroll
+    for (int st = 0; st < kRing - 1; ++st)
+        if (st < n_stages)
+            issue();
     uint32_t prefix = 0;  // sum of u_f from k_lo to k, at most V
-    uint32_t ax[kSub], ay[kSub], bx[kSub], by[kSub];
-    auto add_of = [&](int k, int ri) { return ri >= 0 ? (prefix << S) | (uint32_t)(k - k_lo) : kInf32; };
+    const uint32_t *const x_lds0 = ring + (wave >> 1) * kSub * 64 + lane;
+    const uint32_t *const y_lds0 = ring + (kT + (wave & 1) * kSub) * 64 + lane;
+    int read = 0;  // ring stage read next
     int k = k_lo;
-    int ra = tl.mc - (int)r.wa[k - 1];
-    tl.load(ra, ax, ay);
-    for (; k + 1 <= k_hi; k += 2) {
-        tl.advance(L, k, pitch);
-        const int rb = tl.mc - (int)r.wa[k];
-        tl.load(rb, bx, by);
-        prefix += (uint32_t)r.uf[k - 1];
-        packed_update(acc, ax, ay, add_of(k, ra), S);
-        if (k + 2 <= k_hi) {
-            tl.advance(L, k + 1, pitch);
-            ra = tl.mc - (int)r.wa[k + 1];
-            tl.load(ra, ax, ay);
+    for (int it = 0; it < n_stages; ++it) {
+        // this wave's copies of stage it have landed, and so (after the
+        // barrier) have every wave's; the stage refilled below was read by
+        // every wave before it reached the barrier
+        ring_wait<kRing - 2>(n_stages - 1 - it);
+        if (it + kRing - 1 < n_stages)
+            issue();
+        const uint32_t *x_lds = x_lds0 + read * (kStage * kSplitWords);
+        const uint32_t *y_lds = y_lds0 + read * (kStage * kSplitWords);
+        read = read + 1 == kRing ? 0 : read + 1;
+        uint32_t x[kStage][kSub], y[kStage][kSub];
+#pragma unroll
+        for (int p = 0; p < kStage; ++p, ++k) {
+            const bool real = k <= k_hi;
+            const int ri = mc - (int)r.wa[(real ? k : k_hi) - 1];
+            prefix += real ? (uint32_t)r.uf[k - 1] : 0u;
+            const uint32_t add = real && ri >= 0 ? (prefix << S) | (uint32_t)(k - k_lo) : kInf32;
+#pragma unroll
+            for (int i = 0; i < kSub; ++i)
+                x[p][i] = sat_add(rot_left(x_lds[p * kSplitWords + i * 64], S), add);
+#pragma unroll
+            for (int j = 0; j < kSub; ++j)
+                y[p][j] = rot_left(y_lds[p * kSplitWords + j * 64], S);
         }
-        prefix += (uint32_t)r.uf[k];
-        packed_update(acc, bx, by, add_of(k + 1, rb), S);
+#pragma unroll
+        for (int i = 0; i < kSub; ++i)
+#pragma unroll
+            for (int j = 0; j < kSub; ++j)
+#pragma unroll
+                for (int p = 0; p < kStage; ++p)
+                    acc[i][j] = min(acc[i][j], sat_add(x[p][i], y[p][j]));
     }
-    if (k == k_hi) {
-        prefix += (uint32_t)r.uf[k - 1];
-        packed_update(acc, ax, ay, add_of(k, ra), S);
-    }
-    if (m > M)
+    if (m > M || nt == 0)
         return;
     const uint32_t mask = (1u << S) - 1u;
 #pragma unroll
