@@ -136,6 +136,9 @@ struct Wide {
     };
     static constexpr bool kShadow = false;
     static constexpr uint64_t kShiftedOut = 1ull << 62;
+    static constexpr int kBytes = 8;  // bytes per cell of the table it reads
+    __device__ static const char *table(const int64_t *tab, const uint32_t *) { return (const char *)tab; }
+    __device__ static Raw load_at(const char *row, int m) { return *(global_c64)(row + (uint32_t)m * 8u); }
     __device__ static Raw load(const int64_t *crow, const uint32_t *, int m) { return load64(crow, m); }
     __device__ static void init(Acc &a) { a.key = ~0ull; }
     // ok = false: the budget of Y was shifted below 0, the candidate is infinite
@@ -169,6 +172,9 @@ struct Narrow {
         uint32_t sp;
     };
     static constexpr bool kShadow = true;
+    static constexpr int kBytes = 4;
+    __device__ static const char *table(const int64_t *, const uint32_t *shadow) { return (const char *)shadow; }
+    __device__ static Raw load_at(const char *row, int m) { return *(global_c32)(row + (uint32_t)m * 4u); }
     __device__ static Raw load(const int64_t *, const uint32_t *srow, int m) { return load32(srow, m); }
     __device__ static void init(Acc &a)
     {
@@ -341,27 +347,46 @@ __global__ __launch_bounds__(256) void leaf_kernel(const int64_t *__restrict__ p
         cw.shadow[idx] = ok ? (uint32_t)v : kInf32;
 }
 
-// Relax the N consecutive splits k = k0 .. k0 + N - 1 of the pair (s, t):
-// X rows (s, k) are consecutive from xrow, the Y row of (k+1, t) starts at
-// yrow and advances L - k - 1 rows per k.  Straight-line code: every load is
-// issued before the first relaxation, so their latencies overlap.
+// Row cursor of a run of splits of one pair (s, t): the X row (s, k) and the
+// Y row (k+1, t) of the next split k, as byte addresses in the table the
+// value path reads.  From split k to k + 1 the X row moves one row and the Y
+// row L - k - 1 rows; `ystep` holds the latter, in bytes, and shrinks by one
+// row per split.
+struct RowCursor {
+    const char *x;
+    const char *y;
+    int64_t ystep;
+    int64_t row_bytes;
+};
+
+template <class P>
+__device__ __forceinline__ RowCursor row_cursor(const int64_t *tab, const uint32_t *shadow, int L, int64_t pitch,
+                                                int s, int t, int k)
+{
+    const char *base = P::table(tab, shadow);
+    const int64_t rb = pitch * P::kBytes;
+    return {base + row_of(L, s, k) * rb, base + row_of(L, k + 1, t) * rb, (int64_t)(L - k - 1) * rb, rb};
+}
+
+// Relax the N consecutive splits k = k0 .. k0 + N - 1 at the cursor and
+// advance it.  Straight-line code: every load is issued before the first
+// relaxation, so their latencies overlap.
 template <class P, int N>
-__device__ __forceinline__ void relax_fixed(typename P::Acc &acc, const ChainRows &r, const int64_t *tab,
-                                            const uint32_t *shadow, int L, int m, int64_t pitch, int k0,
-                                            int64_t xrow, int64_t yrow, uint64_t &prefix)
+__device__ __forceinline__ void relax_fixed(typename P::Acc &acc, const ChainRows &r, int m, int k0, RowCursor &cur,
+                                            uint64_t &prefix)
 {
     typename P::Raw rx[N], ry[N];
     int ri[N];
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-        const int k = k0 + i;
-        ri[i] = m - (int)r.wa[k - 1];
-        rx[i] = P::load(tab + xrow, shadow + xrow, m);
+        ri[i] = m - (int)r.wa[k0 + i - 1];
+        rx[i] = P::load_at(cur.x, m);
         // a budget shifted below 0 reads the lane's own budget (in bounds);
         // xop discards the candidate
-        ry[i] = P::load(tab + yrow, shadow + yrow, ri[i] >= 0 ? ri[i] : m);
-        xrow += pitch;
-        yrow += (int64_t)(L - k - 1) * pitch;
+        ry[i] = P::load_at(cur.y, ri[i] >= 0 ? ri[i] : m);
+        cur.x += cur.row_bytes;
+        cur.y += cur.ystep;
+        cur.ystep -= cur.row_bytes;
     }
 #pragma unroll
     for (int i = 0; i < N; ++i) {
@@ -375,31 +400,28 @@ __device__ __forceinline__ void relax_fixed(typename P::Acc &acc, const ChainRow
 // straight-line body of that length.
 template <class P, int N>
 struct RelaxRun {
-    __device__ __forceinline__ static void go(int n, typename P::Acc &acc, const ChainRows &r, const int64_t *tab,
-                                              const uint32_t *shadow, int L, int m, int64_t pitch, int k0,
-                                              int64_t xrow, int64_t yrow, uint64_t &prefix)
+    __device__ __forceinline__ static void go(int n, typename P::Acc &acc, const ChainRows &r, int m, int k0,
+                                              RowCursor &cur, uint64_t &prefix)
     {
         if (n == N)
-            relax_fixed<P, N>(acc, r, tab, shadow, L, m, pitch, k0, xrow, yrow, prefix);
+            relax_fixed<P, N>(acc, r, m, k0, cur, prefix);
         else
-            RelaxRun<P, N - 1>::go(n, acc, r, tab, shadow, L, m, pitch, k0, xrow, yrow, prefix);
+            RelaxRun<P, N - 1>::go(n, acc, r, m, k0, cur, prefix);
     }
 };
 template <class P>
 struct RelaxRun<P, 0> {
-    __device__ __forceinline__ static void go(int, typename P::Acc &, const ChainRows &, const int64_t *,
-                                              const uint32_t *, int, int, int64_t, int, int64_t, int64_t,
+    __device__ __forceinline__ static void go(int, typename P::Acc &, const ChainRows &, int, int, RowCursor &,
                                               uint64_t &)
     {
     }
 };
 
 template <class P>
-__device__ __forceinline__ void relax_run(typename P::Acc &acc, const ChainRows &r, const int64_t *tab,
-                                          const uint32_t *shadow, int L, int m, int64_t pitch, int k0, int n,
-                                          int64_t xrow, int64_t yrow, uint64_t &prefix)
+__device__ __forceinline__ void relax_run(typename P::Acc &acc, const ChainRows &r, int m, int k0, int n,
+                                          RowCursor &cur, uint64_t &prefix)
 {
-    RelaxRun<P, kT - 1>::go(n, acc, r, tab, shadow, L, m, pitch, k0, xrow, yrow, prefix);
+    RelaxRun<P, kT - 1>::go(n, acc, r, m, k0, cur, prefix);
 }
 
 // Eq. (DP:mainrec) for one pair (s, t), all splits in straight-line runs of
@@ -418,11 +440,9 @@ __device__ __forceinline__ void diag_body(const ChainRows &r, const ChainWork &c
     typename P::Acc acc;
     P::init(acc);
     uint64_t prefix = 0;
-    for (int k0 = s; k0 < t; k0 += kT - 1) {
-        const int n = min(kT - 1, t - k0);
-        relax_run<P>(acc, r, tab, cw.shadow, L, m, pitch, k0, n, row_of(L, s, k0) * pitch,
-                     row_of(L, k0 + 1, t) * pitch, prefix);
-    }
+    RowCursor cur = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, s);
+    for (int k0 = s; k0 < t; k0 += kT - 1)
+        relax_run<P>(acc, r, m, k0, min(kT - 1, t - k0), cur, prefix);
     if (m < cw.gnone[cell])
         P::init(acc);
     if (all_ok)
@@ -823,13 +843,14 @@ __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &c
     P::init(acc);
     // low splits k = s .. k_lo - 1: X from block (I, I), Y from this block
     uint64_t prefix = 0;
-    relax_run<P>(acc, r, tab, cw.shadow, L, m, pitch, s, k_lo - s, row_of(L, s, s) * pitch, below, prefix);
+    RowCursor low = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, s);
+    relax_run<P>(acc, r, m, s, k_lo - s, low, prefix);
     // middle splits: the stored partial counts u_f from k_lo on
     P::merge_stored(acc, stored, prefix);
     // high splits k = 16J + 1 .. t - 1: X from this block, Y from block (J, J)
     prefix += (uint64_t)(cw.pre[k_hi] - cw.pre[k_lo - 1]);
-    relax_run<P>(acc, r, tab, cw.shadow, L, m, pitch, k_hi + 1, t - k_hi - 1, row_of(L, s, k_hi + 1) * pitch,
-                 row_of(L, k_hi + 2, t) * pitch, prefix);
+    RowCursor high = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, k_hi + 1);
+    relax_run<P>(acc, r, m, k_hi + 1, t - k_hi - 1, high, prefix);
     if (m < cw.gnone[cell])
         P::init(acc);
     if (all_ok)
