@@ -192,14 +192,15 @@ ROTOR_API int32_t rotor_solve_schedule(const int64_t *d_params, int32_t n_chains
 
 typedef struct {
     int32_t launches;          /* kernel launches of this class */
-    double ms;                 /* summed launch durations, from HIP events */
+    double ms;                 /* time of this class's launches, from HIP events */
     uint64_t split_candidates; /* C_1 candidates evaluated (split point x budget x pair) */
     uint64_t all_candidates;   /* C_2 candidates evaluated (budget x pair) */
     uint64_t cells;            /* final (cost, decision) cells written */
 } rotor_kernel_stats;
 
 /* rotor_solve, plus a breakdown of the fill by kernel class: a HIP event pair
- * is recorded on `stream` around every launch, and the call waits for the
+ * is recorded on `stream` around each run of consecutive launches of one
+ * class (the runs' times summed per class), and the call waits for the
  * stream.  stats: HOST array of ROTOR_N_KERNEL_CLASSES entries, overwritten.
  * Summed over the classes, split_candidates is (L^3 - L)/6 (M+1) n_chains and
  * all_candidates L(L-1)/2 (M+1) n_chains.  Same return codes as rotor_solve. */

@@ -54,12 +54,16 @@ Tables make_tables(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t
 }
 
 // Records an event pair around every launch and adds up the work counts.
+// Times each run of consecutive launches of one kernel class with one pair of
+// HIP events on the launch stream (about two runs per block-diagonal), so the
+// events add little to what they measure.
 struct TimingObserver : LaunchObserver {
-    struct Pair {
+    struct Run {
         hipEvent_t start, stop;
         KernelClass k;
     };
-    std::vector<Pair> pairs;
+    std::vector<Run> runs;
+    bool open = false;  // the last run has no stop recorded yet
     rotor_kernel_stats *stats;
 
     explicit TimingObserver(rotor_kernel_stats *st) : stats(st)
@@ -67,44 +71,58 @@ struct TimingObserver : LaunchObserver {
         for (int k = 0; k < ROTOR_N_KERNEL_CLASSES; ++k)
             stats[k] = rotor_kernel_stats{0, 0.0, 0, 0, 0};
     }
+    hipError_t close(hipStream_t s)
+    {
+        if (!open)
+            return hipSuccess;
+        open = false;
+        return hipEventRecord(runs.back().stop, s);
+    }
     hipError_t before(KernelClass k, hipStream_t s) override
     {
-        Pair p{nullptr, nullptr, k};
-        hipError_t e = hipEventCreate(&p.start);
+        if (open && runs.back().k == k)
+            return hipSuccess;
+        hipError_t e = close(s);
+        Run r{nullptr, nullptr, k};
         if (e == hipSuccess)
-            e = hipEventCreate(&p.stop);
+            e = hipEventCreate(&r.start);
         if (e == hipSuccess)
-            e = hipEventRecord(p.start, s);
-        pairs.push_back(p);
+            e = hipEventCreate(&r.stop);
+        if (e == hipSuccess)
+            e = hipEventRecord(r.start, s);
+        runs.push_back(r);
+        open = e == hipSuccess;
         return e;
     }
-    hipError_t after(KernelClass k, const LaunchWork &w, hipStream_t s) override
+    hipError_t after(KernelClass k, const LaunchWork &w, hipStream_t) override
     {
         rotor_kernel_stats &st = stats[k];
         st.launches += 1;
         st.split_candidates += w.split_candidates;
         st.all_candidates += w.all_candidates;
         st.cells += w.cells;
-        return hipEventRecord(pairs.back().stop, s);
+        return hipSuccess;
     }
     hipError_t finish(hipStream_t s)
     {
-        hipError_t e = hipStreamSynchronize(s);
-        for (Pair &p : pairs) {
+        hipError_t e = close(s);
+        if (e == hipSuccess)
+            e = hipStreamSynchronize(s);
+        for (Run &r : runs) {
             float ms = 0.f;
-            if (e == hipSuccess && p.start && p.stop)
-                e = hipEventElapsedTime(&ms, p.start, p.stop);
-            stats[p.k].ms += ms;
+            if (e == hipSuccess && r.start && r.stop)
+                e = hipEventElapsedTime(&ms, r.start, r.stop);
+            stats[r.k].ms += ms;
         }
         return e;
     }
     ~TimingObserver() override
     {
-        for (Pair &p : pairs) {
-            if (p.start)
-                (void)hipEventDestroy(p.start);
-            if (p.stop)
-                (void)hipEventDestroy(p.stop);
+        for (Run &r : runs) {
+            if (r.start)
+                (void)hipEventDestroy(r.start);
+            if (r.stop)
+                (void)hipEventDestroy(r.stop);
         }
     }
 };
