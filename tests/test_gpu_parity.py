@@ -304,15 +304,22 @@ def test_reconstruct_status_codes():
     assert status[0].item() == rotor.ROTOR_ECORRUPT
 
 
-@pytest.mark.parametrize("cfg", [2, 3])
+@pytest.mark.parametrize("cfg", [2, 3, 4])
 def test_timed_solve_matches_and_counts_the_work(cfg):
+    # random L=50 and ResNet-like L=100 take the streamed order, the batch
+    # workload the blocked one (middle and edge classes)
+    import torch
+
     from paper_1911_13214_amd import rotor
     params, L, M, n, _ = chaingen.config(cfg)
+    say(f"timed cfg {cfg}")
     d_params, cost, dec = solve_on_gpu(params, M)
     c2, d2 = rotor.alloc_tables(n, L, M)
     stats = rotor.rotor_solve_timed(d_params, n, L, M, c2, d2, rotor.alloc_workspace(n, L, M))
-    assert np.array_equal(cost[..., :M + 1].cpu().numpy(), c2[..., :M + 1].cpu().numpy())
-    assert np.array_equal(dec[..., :M + 1].cpu().numpy(), d2[..., :M + 1].cpu().numpy())
+    torch.cuda.synchronize()
+    assert torch.equal(cost[..., :M + 1], c2[..., :M + 1]) and torch.equal(dec[..., :M + 1], d2[..., :M + 1])
+    blocked = cfg == 4
+    assert (stats["middle"]["launches"] > 0) == blocked and (stats["edge"]["launches"] > 0) == blocked
     W = M + 1
     assert sum(s["split_candidates"] for s in stats.values()) == (L ** 3 - L) // 6 * W * n
     assert sum(s["all_candidates"] for s in stats.values()) == L * (L - 1) // 2 * W * n
