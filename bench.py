@@ -10,6 +10,7 @@ Only one GPU is supported: --gpus N with N > 1 exits with a message.
 """
 import argparse
 import hashlib
+import re
 import json
 import os
 import platform
@@ -75,16 +76,24 @@ def arithmetic_type(params):
     return "u32" if bound < (1 << 30) else "int64"
 
 
+def kernel_code_digest(path=None):
+    """sha256 of the fill kernels' source with comments and whitespace
+    removed: it changes when the code changes, not when a comment does."""
+    text = open(path or FILL_SOURCE).read()
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return hashlib.sha256("".join(text.split()).encode()).hexdigest()
+
+
 def traffic_if_current(kernel_class, workload):
     """Measured HBM bytes per launch of a kernel class from the committed
     counter summary, if it was taken on this workload and on the current
-    kernel source."""
+    kernel code."""
     path = os.path.join(ROOT, "profiles", f"traffic_{kernel_class}_kernel.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    sha = hashlib.sha256(open(FILL_SOURCE, "rb").read()).hexdigest()
-    if rec.get("fill_source_sha256") != sha or rec.get("bench_workload") != workload:
+    if rec.get("fill_code_digest") != kernel_code_digest() or rec.get("bench_workload") != workload:
         return None
     return rec.get("bytes_per_launch")
 
@@ -103,8 +112,8 @@ def main():
                          "counter run can scale FETCH_SIZE / WRITE_SIZE by a kernel of known traffic")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: the solver has no multi-GPU path (see the sharding note "
-              "in the design document)", file=sys.stderr)
+        print("bench.py runs on one GPU only: the solver has no multi-GPU path (a batch of chains would "
+              "shard by chain, a single chain over its budget range)", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

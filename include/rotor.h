@@ -229,9 +229,10 @@ ROTOR_API int32_t rotor_solve_timed(const int64_t *d_params, int32_t n_chains, i
  * Asynchronous.  Returns ROTOR_OK once enqueued, ROTOR_EINVAL for bad
  * arguments (including L > ROTOR_MAX_L_RECONSTRUCT), ROTOR_EDEVICE if the
  * launch fails.  Allocates nothing. */
-ROTOR_API int32_t rotor_reconstruct(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, const int16_t *d_dec,
-                          int32_t chain, int32_t n_budgets, const int64_t *d_budgets, int64_t cap, rotor_op *d_ops,
-                          int64_t *d_count, int32_t *d_status, void *stream);
+ROTOR_API int32_t rotor_reconstruct(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M,
+                                    const int16_t *d_dec, int32_t chain, int32_t n_budgets,
+                                    const int64_t *d_budgets, int64_t cap, rotor_op *d_ops, int64_t *d_count,
+                                    int32_t *d_status, void *stream);
 
 /* ---- front end: from measured sizes to budgets (host only) --------------- */
 

@@ -38,13 +38,15 @@
 //   middle  k in [16(I+1), 16J]: X in blocks (I, K) and Y in blocks (K, J)
 //           of smaller D -- all finished, the same range for every cell of
 //           the block: a register-tiled min-plus product (middle_packed_kernel,
-//           or middle_kernel for chains outside the packed keys);
+//           operands staged in LDS, or middle_kernel for chains outside the
+//           packed keys);
 //   low     k in [s, 16(I+1) - 1]: Y is a cell of the same block further down;
 //   high    k in [16J + 1, t - 1]: X is a cell of the same block to the left.
 // The low and high ranges hold at most 30 splits per cell and are taken by
 // edge_kernel in 31 steps over the block's anti-diagonals a + b = q
 // (a = 16(I+1) - s low splits, b = t - 16J - 1 high splits), each step
-// reading only finished cells.
+// reading only finished cells.  A small table is instead filled in the
+// streamed order: one diag_kernel launch per diagonal d over all its pairs.
 #include "rotor_internal.h"
 
 namespace rotor {
@@ -622,13 +624,14 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
 }
 
 // Packed middle products (same blocks, workgroups and register tiles as
-// middle_kernel, operands staged in LDS).  With S the bit width of k - k_lo, a loaded value v becomes
-// v << S by a rotation that leaves 0xFFFFFFFF (infinity) unchanged; X also
-// gets (prefix << S) | (k - k_lo) by a saturating add, Y nothing more, so a
-// candidate is sat(x + y) and the minimum key is the smallest value with,
-// among equal values, the smallest split.  A budget shifted below 0 turns the
-// X term of that lane into infinity.  The partial is stored in the narrow
-// format (value << 32) | s' that edge_kernel merges.
+// middle_kernel, operands staged in LDS).  With S the bit width of
+// k - k_lo, a loaded value v becomes v << S by a rotation that leaves
+// 0xFFFFFFFF (infinity) unchanged; X also gets (prefix << S) | (k - k_lo) by
+// a saturating add, Y nothing more, so a candidate is sat(x + y) and the
+// minimum key is the smallest value with, among equal values, the smallest
+// split.  A budget shifted below 0 turns the X term of that lane into
+// infinity.  The partial is stored in the narrow format (value << 32) | s'
+// that edge_kernel merges.
 __device__ inline uint32_t rot_left(uint32_t v, int S) { return __builtin_amdgcn_alignbit(v, v, (32 - S) & 31); }
 
 // Workgroups are handed to the 8 XCDs in turn (workgroup b of the grid, x

@@ -175,3 +175,14 @@ def test_sequence_cost_rejects_invalid_sequences():
         with pytest.raises(rotor.RotorError) as e:
             rotor.rotor_sequence_cost(p, ops)
         assert e.value.status == rotor.ROTOR_EINVAL
+
+
+def test_kernel_code_digest_ignores_comments_only(tmp_path):
+    import bench
+    src = tmp_path / "k.hip"
+    src.write_text("// header\nint f(int a) { return a + 1; } /* block\n comment */\n")
+    d0 = bench.kernel_code_digest(str(src))
+    src.write_text("// other header\nint f(int a)\n{\n    return a + 1;  // trailing\n}\n")
+    assert bench.kernel_code_digest(str(src)) == d0
+    src.write_text("int f(int a) { return a + 2; }\n")
+    assert bench.kernel_code_digest(str(src)) != d0
