@@ -104,6 +104,7 @@ struct ChainWork {
     const int32_t *gall;   // [rows] m_all(s, t)
     uint32_t *shadow;      // [rows][pitch] compact copy of the costs
     bool narrow;
+    int32_t mode;          // the chain's mode word
 };
 
 __device__ inline ChainWork chain_work(const Work &w, int L, int64_t rows, int64_t pitch, int c)
@@ -113,7 +114,8 @@ __device__ inline ChainWork chain_work(const Work &w, int L, int64_t rows, int64
     cw.gnone = w.gnone + (int64_t)c * rows;
     cw.gall = w.gall + (int64_t)c * rows;
     cw.shadow = w.shadow + (int64_t)c * rows * pitch;
-    cw.narrow = (w.flags[c] & kModeNarrow) != 0;
+    cw.mode = w.flags[c];
+    cw.narrow = (cw.mode & kModeNarrow) != 0;
     return cw;
 }
 
@@ -630,8 +632,8 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
 // a saturating add, Y nothing more, so a candidate is sat(x + y) and the
 // minimum key is the smallest value with, among equal values, the smallest
 // split.  A budget shifted below 0 turns the X term of that lane into
-// infinity.  The partial is stored in the narrow format (value << 32) | s'
-// that edge_kernel merges.
+// infinity.  The partial key is left in the compact copy of the cell for
+// edge_kernel to merge.
 __device__ inline uint32_t rot_left(uint32_t v, int S) { return __builtin_amdgcn_alignbit(v, v, (32 - S) & 31); }
 
 // Workgroups are handed to the 8 XCDs in turn (workgroup b of the grid, x
@@ -699,8 +701,7 @@ __device__ __forceinline__ void ring_wait(int later)
 }
 
 __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__restrict__ params, int L, int M,
-                                                            int64_t pitch, int64_t rows, int delta,
-                                                            int64_t *__restrict__ cost, Work w)
+                                                            int64_t pitch, int64_t rows, int delta, Work w)
 {
     __shared__ uint32_t ring[kRing * kStage * kSplitWords];
     const Tile tile = xcd_tile();
@@ -721,7 +722,6 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     const int S = k_hi > k_lo ? 32 - __clz(k_hi - k_lo) : 0;
     const ChainRows r = chain_rows(params, L, c);
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
-    int64_t *tab = cost + (int64_t)c * rows * pitch;
     const int mc = m <= M ? m : M;
     const int n_stages = (k_hi - k_lo + kStage) / kStage;
 
@@ -813,17 +813,14 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     }
     if (m > M || nt == 0)
         return;
-    const uint32_t mask = (1u << S) - 1u;
+    // the partial stays a packed key, in the cell's compact copy, which
+    // edge_kernel reads once and then overwrites with the final value
 #pragma unroll
     for (int i = 0; i < kSub; ++i)
 #pragma unroll
         for (int j = 0; j < kSub; ++j)
-            if (j < nt) {
-                const uint32_t v = acc[i][j];
-                const uint64_t stored = v == kInf32 ? (uint64_t)kInf32 << 32
-                                                    : ((uint64_t)(v >> S) << 32) | (uint32_t)(k_lo + 1 + (v & mask));
-                tab[row_of(L, s0 + i, t0 + j) * pitch + m] = (int64_t)stored;
-            }
+            if (j < nt)
+                cw.shadow[row_of(L, s0 + i, t0 + j) * pitch + m] = acc[i][j];
 }
 
 // Edge splits, C_2 and the gates for the cells a + b = q of every block
@@ -835,9 +832,13 @@ __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &c
                                           int s, int t, int k_lo, int k_hi, int64_t *tab, int16_t *dtab)
 {
     const int64_t cell = row_of(L, s, t);
-    // loads that depend on nothing go first: the stored middle partial and
-    // the C_2 operand (the lane's own budget when C_2 is out of reach)
-    const int64_t stored = load64(tab + cell * pitch, m);
+    // loads that depend on nothing go first: the stored middle partial (a
+    // packed key in the compact copy, or (value << 32) | s' in the cost
+    // table) and the C_2 operand (the lane's own budget when C_2 is out of
+    // reach)
+    const bool packed_partial = P::kShadow && middle_packed(cw.mode, k_hi - k_lo);
+    const uint32_t key = packed_partial ? load32(cw.shadow + cell * pitch, m) : 0u;
+    const int64_t stored64 = packed_partial ? 0 : load64(tab + cell * pitch, m);
     const int ri = m - (int)r.wabar[s - 1];
     const bool all_ok = m >= cw.gall[cell] && ri >= 0;
     const int64_t below = row_of(L, s + 1, t) * pitch;
@@ -849,6 +850,12 @@ __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &c
     RowCursor low = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, s);
     relax_run<P>(acc, r, m, s, k_lo - s, low, prefix);
     // middle splits: the stored partial counts u_f from k_lo on
+    int64_t stored = stored64;
+    if (packed_partial) {
+        const int S = k_hi > k_lo ? 32 - __clz(k_hi - k_lo) : 0;
+        const uint32_t split = (uint32_t)(k_lo + 1) + (key & ((1u << S) - 1u));
+        stored = key == kInf32 ? (int64_t)((uint64_t)kInf32 << 32) : (int64_t)(((uint64_t)(key >> S) << 32) | split);
+    }
     P::merge_stored(acc, stored, prefix);
     // high splits k = 16J + 1 .. t - 1: X from this block, Y from block (J, J)
     prefix += (uint64_t)(cw.pre[k_hi] - cw.pre[k_lo - 1]);
@@ -983,7 +990,7 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
             return e;
         // each chain is taken by one of the two kernels, the other returns at once
         middle_packed_kernel<<<dim3(mb64, nb - delta, tb.n_chains), 256, 0, stream>>>(
-            tb.params, L, tb.M, tb.pitch, tb.rows, delta, tb.cost, w);
+            tb.params, L, tb.M, tb.pitch, tb.rows, delta, w);
         if ((e = launched(kMiddle, pairs * (uint64_t)((delta - 1) * kT + 1), 0, 0)) != hipSuccess)
             return e;
         if ((e = before(kMiddle)) != hipSuccess)
