@@ -168,11 +168,14 @@ ROTOR_API int32_t rotor_solve(const int64_t *d_params, int32_t n_chains, int32_t
  *                            products for the splits that reach across
  *                            blocks, 31 short launches per block-diagonal for
  *                            the others; the fast order for large tables.
- *   ROTOR_SCHEDULE_DIAGONAL  one launch per t - s, every split of a pair in
- *                            one pass (the wavefront the recurrence allows);
+ *   ROTOR_SCHEDULE_DIAGONAL  one launch per t - s over all pairs (the
+ *                            wavefront the recurrence allows), the splits of
+ *                            a pair spread over four waves from t - s = 16 on;
  *                            fewer launches, the fast order for small tables.
- *   ROTOR_SCHEDULE_AUTO      DIAGONAL when L <= 112 and the table has at most
- *                            3e8 candidates, BLOCKED otherwise (rotor_solve). */
+ *   ROTOR_SCHEDULE_AUTO      DIAGONAL when the table has at most 2e9 split
+ *                            candidates (L^3/6 (M+1)) for one chain, or 4e8
+ *                            summed over a batch; BLOCKED otherwise (the
+ *                            order rotor_solve uses). */
 #define ROTOR_SCHEDULE_AUTO 0
 #define ROTOR_SCHEDULE_BLOCKED 1
 #define ROTOR_SCHEDULE_DIAGONAL 2

@@ -46,7 +46,8 @@
 // edge_kernel in 31 steps over the block's anti-diagonals a + b = q
 // (a = 16(I+1) - s low splits, b = t - 16J - 1 high splits), each step
 // reading only finished cells.  A small table is instead filled in the
-// streamed order: one diag_kernel launch per diagonal d over all its pairs.
+// streamed order: one launch per diagonal d over all its pairs (diag_kernel,
+// or diag_split_kernel with the splits of a pair spread over four waves).
 #include "rotor_internal.h"
 
 namespace rotor {
@@ -56,10 +57,12 @@ constexpr int64_t kInf = INT64_MAX;
 constexpr int kT = 16;   // block side, in stages
 constexpr int kSub = 8;  // per-wave register tile side
 constexpr int kEdgeThreads = 128;  // budgets per edge workgroup (measured best of 64..512)
-// The automatic schedule fills small tables diagonal by diagonal (measured
-// on MI355X: faster up to about these sizes, slower beyond).
-constexpr int kStreamMaxL = 112;
-constexpr uint64_t kStreamMaxCandidates = 300000000ull;
+// The automatic schedule fills small tables diagonal by diagonal: measured on
+// MI355X, that is faster up to about 2e9 split candidates for one chain
+// (L = 250 at M = 500) and 4e8 for a batch, whose blocked launches are wider.
+constexpr uint64_t kStreamMaxCandidates1 = 2000000000ull;
+constexpr uint64_t kStreamMaxCandidatesN = 400000000ull;
+constexpr int kSplitMinD = 16;  // streamed diagonals from this length spread their splits over four waves
 constexpr uint32_t kAllSplit = 0xFFFF;  // split field of a C_2 candidate
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
 constexpr uint64_t kNarrowBound = 1ull << 30;
@@ -162,6 +165,8 @@ struct Wide {
         a.key = umin(a.key, key_of(y) + ((ufub << 16) | kAllSplit));
     }
     __device__ static int64_t stored(const Acc &a) { return (int64_t)a.key; }
+    // fold in the stored() form of a result over larger splits
+    __device__ static void merge_later(Acc &a, int64_t later) { a.key = umin(a.key, (uint64_t)later); }
     __device__ static bool finite(const Acc &a) { return a.key < (1ull << 62); }
     __device__ static int64_t value(const Acc &a) { return (int64_t)(a.key >> 16); }
     __device__ static uint32_t split(const Acc &a) { return (uint32_t)(a.key & 0xFFFF); }
@@ -213,6 +218,14 @@ struct Narrow {
         a.sp = b ? kAllSplit : a.sp;
     }
     __device__ static int64_t stored(const Acc &a) { return (int64_t)(((uint64_t)a.val << 32) | a.sp); }
+    // fold in the stored() form of a result over larger splits: strict <
+    __device__ static void merge_later(Acc &a, int64_t later)
+    {
+        const uint32_t v = (uint32_t)((uint64_t)later >> 32);
+        const bool b = v < a.val;
+        a.val = b ? v : a.val;
+        a.sp = b ? (uint32_t)later : a.sp;
+    }
     __device__ static bool finite(const Acc &a) { return a.val != kInf32; }
     __device__ static int64_t value(const Acc &a) { return (int64_t)a.val; }
     __device__ static uint32_t split(const Acc &a) { return a.sp; }
@@ -476,6 +489,71 @@ __global__ __launch_bounds__(256) void diag_kernel(const int64_t *__restrict__ p
         diag_body<Narrow>(r, cw, L, m, pitch, s, t, tab, dtab);
     else
         diag_body<Wide>(r, cw, L, m, pitch, s, t, tab, dtab);
+}
+
+// Streamed order for the longer diagonals: the d splits of each pair are
+// spread over the four waves of a workgroup (one pair, 64 budgets), wave w
+// taking the w-th quarter in increasing order; wave 0 then folds the four
+// results in split order (so ties still go to the smallest split), adds C_2
+// and the gates, and writes the cell.  Four times the waves of diag_kernel,
+// each with a quarter of the dependent loads.
+template <class P>
+__device__ __forceinline__ void diag_split_body(const ChainRows &r, const ChainWork &cw, int L, int M, int m,
+                                                int64_t pitch, int s, int t, int wave, int64_t (*part)[64],
+                                                int64_t *tab, int16_t *dtab)
+{
+    const int mc = m <= M ? m : M;  // lanes past M load in bounds and store nothing
+    const int lane = threadIdx.x & 63;
+    const int d = t - s;
+    const int chunk = (d + 3) / 4;
+    const int k0 = s + wave * chunk;
+    const int k1 = min(t - 1, k0 + chunk - 1);
+    typename P::Acc acc;
+    P::init(acc);
+    if (k0 <= k1) {
+        uint64_t prefix = (uint64_t)(cw.pre[k0 - 1] - cw.pre[s - 1]);
+        RowCursor cur = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, k0);
+        for (int kk = k0; kk <= k1; kk += kT - 1)
+            relax_run<P>(acc, r, mc, kk, min(kT - 1, k1 - kk + 1), cur, prefix);
+    }
+    part[wave][lane] = P::stored(acc);
+    __syncthreads();
+    if (wave != 0 || m > M)
+        return;
+#pragma unroll
+    for (int v = 1; v < 4; ++v)
+        P::merge_later(acc, part[v][lane]);
+    const int64_t cell = row_of(L, s, t);
+    const int ri = m - (int)r.wabar[s - 1];
+    const bool all_ok = m >= cw.gall[cell] && ri >= 0;
+    const int64_t below = row_of(L, s + 1, t) * pitch;
+    const typename P::Raw c2 = P::load(tab + below, cw.shadow + below, all_ok ? ri : m);
+    if (m < cw.gnone[cell])
+        P::init(acc);
+    if (all_ok)
+        P::relax_all(acc, c2, (uint64_t)(r.uf[s - 1] + r.ub[s - 1]));
+    store_cell<P>(tab, dtab, cw.shadow, cell * pitch + m, acc);
+}
+
+__global__ __launch_bounds__(256) void diag_split_kernel(const int64_t *__restrict__ params, int L, int M,
+                                                         int64_t pitch, int64_t rows, int d,
+                                                         int64_t *__restrict__ cost, int16_t *__restrict__ dec,
+                                                         Work w)
+{
+    __shared__ int64_t part[4][64];
+    const int c = blockIdx.z;
+    const int s = blockIdx.y + 1;
+    const int t = s + d;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int m = blockIdx.x * 64 + (threadIdx.x & 63);
+    const ChainRows r = chain_rows(params, L, c);
+    const ChainWork cw = chain_work(w, L, rows, pitch, c);
+    int64_t *tab = cost + (int64_t)c * rows * pitch;
+    int16_t *dtab = dec + (int64_t)c * rows * pitch;
+    if (cw.narrow)
+        diag_split_body<Narrow>(r, cw, L, M, m, pitch, s, t, wave, part, tab, dtab);
+    else
+        diag_split_body<Wide>(r, cw, L, M, m, pitch, s, t, wave, part, tab, dtab);
 }
 
 // Whether the middle products of a chain whose middle split range has
@@ -968,12 +1046,17 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
     // short, and the blocked fill would need 33 per block-diagonal.
     const uint64_t r_total = ((uint64_t)L * L * L / 6) * W * nc;
     const bool streamed = schedule == ROTOR_SCHEDULE_DIAGONAL ||
-                          (schedule == ROTOR_SCHEDULE_AUTO && L <= kStreamMaxL && r_total <= kStreamMaxCandidates);
+                          (schedule == ROTOR_SCHEDULE_AUTO &&
+                           r_total <= (nc == 1 ? kStreamMaxCandidates1 : kStreamMaxCandidatesN));
     for (int d = 1; d < (streamed ? L : kT) && d < L; ++d) {
         if ((e = before(kDiag)) != hipSuccess)
             return e;
-        diag_kernel<<<dim3(mb256, L - d, tb.n_chains), 256, 0, stream>>>(tb.params, L, tb.M, tb.pitch, tb.rows, d,
-                                                                         streamed ? 1 : 0, tb.cost, tb.dec, w);
+        if (streamed && d >= kSplitMinD)
+            diag_split_kernel<<<dim3(mb64, L - d, tb.n_chains), 256, 0, stream>>>(tb.params, L, tb.M, tb.pitch,
+                                                                                  tb.rows, d, tb.cost, tb.dec, w);
+        else
+            diag_kernel<<<dim3(mb256, L - d, tb.n_chains), 256, 0, stream>>>(tb.params, L, tb.M, tb.pitch, tb.rows,
+                                                                             d, streamed ? 1 : 0, tb.cost, tb.dec, w);
         const uint64_t pairs = streamed ? (uint64_t)(L - d) : in_block_pairs(L, d);
         if ((e = launched(kDiag, pairs * d, pairs, pairs)) != hipSuccess)
             return e;
