@@ -5,6 +5,7 @@ synthetic workload, inputs already resident in device memory.
 Prints ONE JSON line on stdout.  Everything else goes to stderr.
 
   python bench.py [--steps K] [--warmup W] [--workload 1..5] [--no-cpu-baseline]
+  python bench.py --shape L,M[,N]   # N seeded random chains (the L=50 recipe) of any size
 
 Only one GPU is supported: --gpus N with N > 1 exits with a message.
 """
@@ -104,6 +105,8 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", type=int, default=5)
+    ap.add_argument("--shape", default=None, metavar="L,M[,N]",
+                    help="instead of a preset workload: N (default 1) random chains of L stages, budgets 0..M")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-stages", type=int, default=300)
     ap.add_argument("--profile-steps", type=int, default=2)
@@ -121,7 +124,15 @@ def main():
 
     from paper_1911_13214_amd import chaingen, rotor
 
-    params, L, M, n_chains, name = chaingen.config(args.workload)
+    if args.shape:
+        dims = [int(v) for v in args.shape.split(",")]
+        L, M = dims[0], dims[1]
+        n_chains = dims[2] if len(dims) > 2 else 1
+        params = chaingen.random_chains(n_chains, L, seed=L + M)
+        name = f"random L={L} M={M}" + (f" x {n_chains}" if n_chains > 1 else "")
+        args.workload = 0
+    else:
+        params, L, M, n_chains, name = chaingen.config(args.workload)
     r_ck, r_all, cells, alg_bytes, diag_bytes = work_counts(n_chains, L, M)
     R = r_ck + r_all
     dev = torch.device("cuda:0")
