@@ -445,6 +445,39 @@ def test_long_chain_windows():
     assert np.all(top[1:] <= top[:-1]) and top[M] != orc.INF
 
 
+def test_orders_agree_on_a_table_beyond_4_gb():
+    # L = 1000, M = 4000: 500,500 pairs, a 16 GB cost table and an 8 GB
+    # compact copy, so row offsets pass 32 bits; the cost bound (~2.5e7)
+    # leaves 7 bits of split field, so block-diagonals up to 8 take packed
+    # middle keys and the later ones the (value, split) middle kernel.  The
+    # blocked and the streamed order share no kernel beyond the leaves and
+    # the in-block diagonals; every cell must agree, and 36-stage windows
+    # must equal the oracle's tables.
+    import torch
+    from paper_1911_13214_amd import rotor
+    L, M = 1000, 4000
+    p = chaingen.random_chains(1, L, seed=1000)
+    assert (1 << 24) < cost_bound(p[0]) < (1 << 25)
+    say(f"orders at scale L={L} M={M}")
+    _, c1, d1 = solve_on_gpu(p, M, schedule="blocked")
+    _, c2, d2 = solve_on_gpu(p, M, schedule="diagonal")
+    assert torch.equal(c1[..., :M + 1], c2[..., :M + 1]) and torch.equal(d1[..., :M + 1], d2[..., :M + 1])
+    del c2, d2
+    torch.cuda.empty_cache()
+    for a in (1, 483, 965):
+        b = a + 35
+        C, D = oracle_tables(np.ascontiguousarray(p[:, :, a - 1:b]), M)
+        pairs = [(s, t) for s in range(1, 37) for t in range(s, 37)]
+        rows = torch.tensor([rotor.rotor_row_index(L, s + a - 1, t + a - 1) for s, t in pairs], device="cuda")
+        gc = c1[0][rows][:, :M + 1].cpu().numpy()
+        gd = d1[0][rows][:, :M + 1].cpu().numpy().astype(np.int64)
+        np.testing.assert_array_equal(gc, np.stack([C[orc.row(36, s, t)] for s, t in pairs]))
+        want_d = np.stack([D[orc.row(36, s, t)] for s, t in pairs]).astype(np.int64)
+        np.testing.assert_array_equal(gd, np.where(want_d > 0, want_d + a - 1, want_d))
+    top = c1[0, rotor.rotor_row_index(L, 1, L), :M + 1].cpu().numpy()
+    assert np.all(top[1:] <= top[:-1]) and top[M] != orc.INF
+
+
 def test_fill_replays_from_a_captured_graph():
     # the fill only enqueues kernels (no allocation, no memset, no host wait),
     # so a caller may capture it; every replay, with eager work in between,
