@@ -53,10 +53,10 @@ Tables make_tables(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t
     return tb;
 }
 
-// Records an event pair around every launch and adds up the work counts.
-// Times each run of consecutive launches of one kernel class with one pair of
-// HIP events on the launch stream (about two runs per block-diagonal), so the
-// events add little to what they measure.
+// Adds up the work counts of every launch and times each run of consecutive
+// launches of one kernel class with one pair of HIP events on the launch
+// stream (about two runs per block-diagonal), so the events add little to
+// what they measure.
 struct TimingObserver : LaunchObserver {
     struct Run {
         hipEvent_t start, stop;
