@@ -254,13 +254,14 @@ __device__ inline void store_cell(int64_t *cost, int16_t *dec, uint32_t *shadow,
 // ---------------------------------------------------------------------------
 
 // Gates of every pair, prefix sums and value path of every chain.
-// Workgroups 0 .. G-2 of a chain write the gate rows of 64 consecutive s:
-// m_all(s, t) (peak of F_all^s with delta^t stored, and of B^s with delta^s
-// stored) and m_none(s, t) (peak of F_ck^s and F_none^{s+1..t-1} with delta^t
-// stored), Section 4.2; delta has the size of a.  The per-t terms are staged
-// in LDS 64 stages at a time.  Gates above INT32_MAX are clamped: any gate
-// above M < 2^28 is never met.  The last workgroup of a chain scans u_f with
-// one wave.
+// Workgroup s - 1 of a chain writes the gate row of s, 64 consecutive t per
+// step: m_all(s, t) (peak of F_all^s with delta^t stored, and of B^s with
+// delta^s stored) and m_none(s, t) (peak of F_ck^s and F_none^{s+1..t-1} with
+// delta^t stored), Section 4.2; delta has the size of a.  The maximum over
+// s < j < t in m_none is a running maximum along t: a wave prefix maximum
+// per step plus the carry of the steps before.  Gates above INT32_MAX are
+// clamped: any gate above M < 2^28 is never met.  The last workgroup of a
+// chain scans u_f with one wave.
 __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ params, int L, int64_t rows, Work w)
 {
     const int c = blockIdx.y;
@@ -307,38 +308,30 @@ __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ pa
         }
         return;
     }
-    __shared__ int64_t lwa[64], lv[64];
-    const int s0 = blockIdx.x * 64 + 1;
-    const int s = s0 + lane;
+    const int s = blockIdx.x + 1;
     int32_t *gn = w.gnone + (int64_t)c * rows;
     int32_t *ga = w.gall + (int64_t)c * rows;
-    int64_t first = 0, bwd = 0, fpart = 0;
-    if (s <= L) {
-        first = r.wa[s - 1] + r.of[s - 1];
-        bwd = r.wa[s - 1] + r.wabar[s - 1] + r.ob[s - 1];
-        fpart = r.wabar[s - 1] + r.of[s - 1];
-    }
-    int64_t jmax = 0;  // max over s < j < t of w_a^{j-1} + w_a^j + o_f^j
-    int64_t row = s <= L ? row_of(L, s, s) : 0;
-    for (int t0 = s0; t0 <= L; t0 += 64) {
-        __syncthreads();
-        const int tt = t0 + lane;
-        if (tt <= L) {
-            lwa[lane] = r.wa[tt - 1];
-            lv[lane] = tt >= 3 ? r.wa[tt - 3] + r.wa[tt - 2] + r.of[tt - 2] : 0;  // the term of j = tt - 1
+    const int64_t first = r.wa[s - 1] + r.of[s - 1];
+    const int64_t bwd = r.wa[s - 1] + r.wabar[s - 1] + r.ob[s - 1];
+    const int64_t fpart = r.wabar[s - 1] + r.of[s - 1];
+    int64_t carry = 0;  // max over s < j < t0 of w_a^{j-1} + w_a^j + o_f^j
+    int64_t row = row_of(L, s, s);
+    for (int t0 = s; t0 <= L; t0 += 64, row += 64) {
+        const int t = t0 + lane;
+        // the term of j = t - 1, which m_none(s, t) includes when s < t - 1
+        int64_t incl = t <= L && t >= s + 2 ? r.wa[t - 3] + r.wa[t - 2] + r.of[t - 2] : 0;
+        for (int off = 1; off < 64; off *= 2) {
+            const int64_t v = __shfl_up(incl, off);
+            if (lane >= off)
+                incl = max(incl, v);
         }
-        __syncthreads();
-        if (s > L)
-            continue;
-        const int n = min(64, L - t0 + 1);
-        for (int i = max(0, s - t0); i < n; ++i) {
-            const int t = t0 + i;
-            ga[row] = clamp32(max(lwa[i] + fpart, bwd));
-            if (t >= s + 2)
-                jmax = max(jmax, lv[i]);
-            gn[row] = t > s ? clamp32(lwa[i] + max(first, jmax)) : 0;
-            ++row;
+        const int64_t jmax = max(carry, incl);
+        if (t <= L) {
+            const int64_t wt = r.wa[t - 1];
+            ga[row + lane] = clamp32(max(wt + fpart, bwd));
+            gn[row + lane] = t > s ? clamp32(wt + max(first, jmax)) : 0;
         }
+        carry = max(carry, __shfl(incl, 63));
     }
 }
 
@@ -1033,7 +1026,7 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
 
     if ((e = before(kPrep)) != hipSuccess)
         return e;
-    prep_kernel<<<dim3((L + 63) / 64 + 1, tb.n_chains), 64, 0, stream>>>(tb.params, L, tb.rows, w);
+    prep_kernel<<<dim3(L + 1, tb.n_chains), 64, 0, stream>>>(tb.params, L, tb.rows, w);
     if ((e = launched(kPrep, 0, 0, 0)) != hipSuccess)
         return e;
     if ((e = before(kLeaf)) != hipSuccess)
