@@ -478,6 +478,23 @@ def test_orders_agree_on_a_table_beyond_4_gb():
     assert np.all(top[1:] <= top[:-1]) and top[M] != orc.INF
 
 
+@pytest.mark.parametrize("n,L,M", [(65535, 3, 4), (8192, 40, 20)])
+def test_largest_batches(n, L, M):
+    # the chain index rides on the grid's z dimension (65535 at most): the two
+    # fill orders agree on every chain, and sampled chains equal the oracle
+    import torch
+    params = chaingen.random_chains(n, L, seed=n + L)
+    say(f"batch n={n} L={L} M={M}")
+    _, c1, d1 = solve_on_gpu(params, M, schedule="blocked")
+    _, c2, d2 = solve_on_gpu(params, M, schedule="diagonal")
+    assert torch.equal(c1[..., :M + 1], c2[..., :M + 1]) and torch.equal(d1[..., :M + 1], d2[..., :M + 1])
+    del c2, d2
+    order = gpu_rows_in_oracle_order(L)
+    rng = np.random.default_rng(n)
+    for c in sorted({0, 1, n // 2, n - 1, *rng.integers(0, n, 24).tolist()}):
+        assert_same(params, M, c1, d1, c, order)
+
+
 def test_fill_replays_from_a_captured_graph():
     # the fill only enqueues kernels (no allocation, no memset, no host wait),
     # so a caller may capture it; every replay, with eager work in between,
