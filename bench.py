@@ -99,6 +99,26 @@ def traffic_if_current(kernel_class, workload):
     return rec.get("bytes_per_launch")
 
 
+def copy_bandwidth(dev, mib=1024, reps=5):
+    """What the part delivers to a plain stream: GB/s (read + write) of a
+    device-to-device copy of ``mib`` MiB, HIP events around ``reps`` copies."""
+    import torch
+    src = torch.ones(mib << 17, dtype=torch.int64, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    b.synchronize()
+    gbps = 2 * (mib << 20) * reps / (a.elapsed_time(b) * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return round(gbps, 1)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -231,6 +251,14 @@ def main():
         "solve_alg_GBps": round(alg_bytes / (ms * 1e-3) / 1e9, 1),
         "check": check,
     }
+    # the same kernel against what a plain copy reaches on this part, on the
+    # measured traffic (when the committed counter record is current)
+    copy = copy_bandwidth(dev)
+    traffic = out["roofline"]["traffic"]
+    measured = round(traffic / (kd["avg_launch_us"] * 1e-6) / 1e9, 1) if traffic else None
+    out["copy_roofline"] = {"kernel": f"{dom}_kernel", "copy_GBps": copy, "measured_GBps": measured,
+                            "frac": round(measured / copy, 4) if measured else None,
+                            "copy": "device-to-device copy of 1 GiB, read + write, HIP events, mean of 5"}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(params, M, min(args.cpu_stages, L)) if n_chains == 1 else None
     print(json.dumps(out), flush=True)
