@@ -5,7 +5,7 @@ synthetic workload, inputs already resident in device memory.
 Prints ONE JSON line on stdout.  Everything else goes to stderr.
 
   python bench.py [--steps K] [--warmup W] [--workload 1..5] [--no-cpu-baseline]
-  python bench.py --shape L,M[,N]   # N seeded random chains (the L=50 recipe) of any size
+  python bench.py --shape L,M[,N] [--cost-shift B]   # N seeded random chains of any size
 
 Only one GPU is supported: --gpus N with N > 1 exits with a message.
 """
@@ -127,6 +127,8 @@ def main():
     ap.add_argument("--workload", type=int, default=5)
     ap.add_argument("--shape", default=None, metavar="L,M[,N]",
                     help="instead of a preset workload: N (default 1) random chains of L stages, budgets 0..M")
+    ap.add_argument("--cost-shift", type=int, default=0, metavar="B",
+                    help="with --shape: multiply u_f and u_b by 2^B (B = 10 puts L=500 on the 64-bit path)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-stages", type=int, default=300)
     ap.add_argument("--profile-steps", type=int, default=2)
@@ -149,7 +151,9 @@ def main():
         L, M = dims[0], dims[1]
         n_chains = dims[2] if len(dims) > 2 else 1
         params = chaingen.random_chains(n_chains, L, seed=L + M)
-        name = f"random L={L} M={M}" + (f" x {n_chains}" if n_chains > 1 else "")
+        params[:, :2] <<= args.cost_shift
+        name = f"random L={L} M={M}" + (f" x {n_chains}" if n_chains > 1 else "") + \
+            (f" costs x 2^{args.cost_shift}" if args.cost_shift else "")
         args.workload = 0
     else:
         params, L, M, n_chains, name = chaingen.config(args.workload)
