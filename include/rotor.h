@@ -174,8 +174,9 @@ ROTOR_API int32_t rotor_solve(const int64_t *d_params, int32_t n_chains, int32_t
  *                            fewer launches, the fast order for small tables.
  *   ROTOR_SCHEDULE_AUTO      DIAGONAL when the table has at most 2e9 split
  *                            candidates (L^3/6 (M+1)) for one chain, or 4e8
- *                            summed over a batch; BLOCKED otherwise (the
- *                            order rotor_solve uses). */
+ *                            summed over a batch, or when one chain has
+ *                            M < 63; BLOCKED otherwise (the order rotor_solve
+ *                            uses). */
 #define ROTOR_SCHEDULE_AUTO 0
 #define ROTOR_SCHEDULE_BLOCKED 1
 #define ROTOR_SCHEDULE_DIAGONAL 2

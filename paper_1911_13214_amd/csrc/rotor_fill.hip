@@ -59,9 +59,13 @@ constexpr int kSub = 8;  // per-wave register tile side
 constexpr int kEdgeThreads = 128;  // budgets per edge workgroup (measured best of 64..512)
 // The automatic schedule fills small tables diagonal by diagonal: measured on
 // MI355X, that is faster up to about 2e9 split candidates for one chain
-// (L = 250 at M = 500) and 4e8 for a batch, whose blocked launches are wider.
+// (L = 250 at M = 500) and 4e8 for a batch, whose blocked launches are wider,
+// and for any single chain with fewer than 64 budgets, which leave most lanes
+// of the blocked kernels' 64-budget chunks idle (L = 3000, M = 31: 229
+// against 269 ms).
 constexpr uint64_t kStreamMaxCandidates1 = 2000000000ull;
 constexpr uint64_t kStreamMaxCandidatesN = 400000000ull;
+constexpr int kStreamBelowBudgets = 64;
 constexpr int kSplitMinD = 16;  // streamed diagonals from this length spread their splits over four waves
 constexpr uint32_t kAllSplit = 0xFFFF;  // split field of a C_2 candidate
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
@@ -1040,7 +1044,8 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
     const uint64_t r_total = ((uint64_t)L * L * L / 6) * W * nc;
     const bool streamed = schedule == ROTOR_SCHEDULE_DIAGONAL ||
                           (schedule == ROTOR_SCHEDULE_AUTO &&
-                           r_total <= (nc == 1 ? kStreamMaxCandidates1 : kStreamMaxCandidatesN));
+                           (nc == 1 ? r_total <= kStreamMaxCandidates1 || W < (uint64_t)kStreamBelowBudgets
+                                    : r_total <= kStreamMaxCandidatesN));
     for (int d = 1; d < (streamed ? L : kT) && d < L; ++d) {
         if ((e = before(kDiag)) != hipSuccess)
             return e;

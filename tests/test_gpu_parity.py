@@ -137,13 +137,14 @@ def test_shifts_beyond_the_budget(schedule):
     assert_same(p, 200, cost, dec)
 
 
-def test_zero_sizes_any_length():
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_zero_sizes_any_length(schedule):
     # no memory needed anywhere: with u_f >= 1 the no-recomputation schedule
     # is optimal for every budget, F_all first everywhere
     L, M = 700, 3
     p = chaingen.random_chains(1, L, seed=13)
     p[0, 2:] = 0
-    d_params, cost, dec = solve_on_gpu(p, M)
+    d_params, cost, dec = solve_on_gpu(p, M, schedule=schedule)
     pre = np.concatenate([[0], np.cumsum(p[0, 0] + p[0, 1])])
     gc = cost[0].cpu().numpy()
     gd = dec[0].cpu().numpy()
