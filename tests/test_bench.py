@@ -1,0 +1,58 @@
+"""The bench's host side: the work it credits to one solve, the arithmetic
+type it reports, and its refusal of more than one GPU.  No GPU needed."""
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+import bench
+from paper_1911_13214_amd import chaingen
+
+
+def brute_counts(n_chains, L, M):
+    # one C_1 candidate per split s' in (s, t], one C_2 candidate per pair
+    # s < t, one cell per pair s <= t; each per budget 0..M and per chain
+    r_ck = sum(t - s for s in range(1, L + 1) for t in range(s, L + 1))
+    r_all = sum(1 for s in range(1, L + 1) for t in range(s + 1, L + 1))
+    cells = L * (L + 1) // 2
+    W = (M + 1) * n_chains
+    return r_ck * W, r_all * W, cells * W
+
+
+@pytest.mark.parametrize("n,L,M", [(1, 1, 0), (1, 2, 3), (3, 17, 40), (2, 64, 640), (1, 100, 1000)])
+def test_work_counts_match_the_enumerated_candidates(n, L, M):
+    r_ck, r_all, cells, alg, diag = bench.work_counts(n, L, M)
+    assert (r_ck, r_all, cells) == brute_counts(n, L, M)
+    assert alg == 16 * r_ck + 8 * r_all + 10 * cells
+    assert diag == alg - 10 * L * (M + 1) * n
+
+
+def test_work_counts_of_the_large_and_batch_workloads():
+    # the figures the roofline is priced on
+    assert bench.work_counts(1, 500, 5000)[:3] == (104_187_083_250, 623_874_750, 626_375_250)
+    assert bench.work_counts(256, 64, 640)[:3] == (7_167_713_280, 330_817_536, 341_319_680)
+    alg = bench.work_counts(1, 500, 5000)[3]
+    assert alg / 8e12 * 1e3 == pytest.approx(209.8, abs=0.05)  # ms at the 8 TB/s HBM peak
+
+
+def test_arithmetic_type_follows_the_cost_bound():
+    assert bench.arithmetic_type(chaingen.random_chains(1, 500, seed=5, wa_hi=20)) == "u32"
+    p = chaingen.random_chains(1, 500, seed=5, wa_hi=20)
+    p[:, chaingen.UF] <<= 10
+    p[:, chaingen.UB] <<= 10
+    assert bench.arithmetic_type(p) == "int64"
+    # the bound sum_l P[l] + sum u_b just below and at 2^30
+    L = 4
+    p = np.zeros((1, 6, L), dtype=np.int64)
+    p[0, chaingen.UF, 0] = ((1 << 30) - 1) // L
+    assert bench.arithmetic_type(p) == "u32"
+    p[0, chaingen.UB, 0] = (1 << 30) - L * p[0, chaingen.UF, 0]
+    assert bench.arithmetic_type(p) == "int64"
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    r = subprocess.run([sys.executable, bench.__file__, "--gpus", "2"], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 2
+    assert r.stdout == ""
+    assert "one GPU" in r.stderr
