@@ -18,11 +18,12 @@
 //    the table (INT64_MAX stored as 0xFFFFFFFF) and added with unsigned
 //    saturation; the best value and its split are kept side by side and
 //    splits are visited in increasing s' with a strict <;
-//  - packed (middle products of narrow chains, when (V + 1) << S fits below
-//    2^32 - 1 for the S bits of the block's middle split range): a candidate
-//    is one uint32 key (value << S) | (s' - first middle split), so one
-//    saturating add and one unsigned min relax it, ties going to the smaller
-//    split;
+//  - packed (middle products of narrow chains, when (V_D + 1) << S fits
+//    below 2^32 - 1 for the S bits of the block's middle split range, V_D
+//    being the same bound for the longest sub-chains of the block-diagonal):
+//    a candidate is one uint32 key (value << S) | (s' - first middle split),
+//    so one saturating add and one unsigned min relax it, ties going to the
+//    smaller split;
 //  - wide, otherwise: operands are the int64 cells and a candidate is one
 //    64-bit key (value << 16) | s', so one unsigned min keeps the smallest
 //    value and, among equal values, the smallest split.  Finite values are
@@ -99,10 +100,8 @@ __device__ inline uint32_t load32(const uint32_t *row, int m)
 __device__ inline uint32_t sat_add(uint32_t a, uint32_t b) { return __builtin_elementwise_add_sat(a, b); }
 __device__ inline uint64_t umin(uint64_t a, uint64_t b) { return b < a ? b : a; }
 
-// Per-chain mode word written by prep_kernel: bit 0 narrow path, bits 8..15
-// the largest S with (V + 1) << S <= 2^32 - 1 (packed middle keys).
+// Per-chain mode word written by prep_kernel: bit 0 narrow path.
 constexpr int32_t kModeNarrow = 1;
-__host__ __device__ inline int packed_bits(int32_t mode) { return (mode >> 8) & 0xFF; }
 
 // Per-chain views of the workspace.
 struct ChainWork {
@@ -110,8 +109,8 @@ struct ChainWork {
     const int32_t *gnone;  // [rows] m_none(s, t), t > s
     const int32_t *gall;   // [rows] m_all(s, t)
     uint32_t *shadow;      // [rows][pitch] compact copy of the costs
+    const int32_t *pbits;  // [nb] largest S with (V_D + 1) << S <= 2^32 - 1, per block-diagonal D
     bool narrow;
-    int32_t mode;          // the chain's mode word
 };
 
 __device__ inline ChainWork chain_work(const Work &w, int L, int64_t rows, int64_t pitch, int c)
@@ -121,8 +120,8 @@ __device__ inline ChainWork chain_work(const Work &w, int L, int64_t rows, int64
     cw.gnone = w.gnone + (int64_t)c * rows;
     cw.gall = w.gall + (int64_t)c * rows;
     cw.shadow = w.shadow + (int64_t)c * rows * pitch;
-    cw.mode = w.flags[c];
-    cw.narrow = (cw.mode & kModeNarrow) != 0;
+    cw.pbits = w.pbits + (int64_t)c * ((L + kT - 1) / kT);
+    cw.narrow = (w.flags[c] & kModeNarrow) != 0;
     return cw;
 }
 
@@ -298,17 +297,78 @@ __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ pa
             sb += __shfl_xor(sb, off);
             sp += __shfl_xor(sp, off);
         }
+        // V = sum_l P[l] + sum_j u_b^j = sum_j (L - j + 1) u_f^j + sum_j u_b^j
+        // (below 2^60 in the domain)
+        const uint64_t bound = sp + sb;
         if (lane == 63) {
             pre[0] = 0;
-            // V = sum_l P[l] + sum_j u_b^j = sum_j (L - j + 1) u_f^j + sum_j u_b^j
-            // (below 2^60 in the domain)
-            const uint64_t bound = sp + sb;
-            int32_t mode = 0;
-            if (bound < kNarrowBound) {
-                const uint64_t q = 0xFFFFFFFFull / (bound + 1);  // >= 4
-                mode = kModeNarrow | ((63 - __clzll((long long)q)) << 8);
+            w.flags[c] = bound < kNarrowBound ? kModeNarrow : 0;
+        }
+        // Packed middle keys, per block-diagonal D: every candidate of a block
+        // (I, I + D) is the time of a schedule of one of its pairs (s, t), so
+        // at most V(s, t) = sum_{l=s}^{t} (P[l] - P[s-1]) + sum_{j=s}^{t} u_b^j,
+        // which grows with t - s: the block's bound is V over [16I + 1,
+        // min(16(I + D + 1), L)], and V_D the largest over I.  With PP and B
+        // the sums of P and of u_b up to a stage,
+        // V(x + 1, y) = PP[y] - PP[x] - (y - x) P[x] + B[y] - B[x];
+        // bsum keeps PP and B at the block ends min(16b, L), b = 0..nb.
+        const int nb = (L + kT - 1) / kT;
+        if (nb < 2)
+            return;
+        int32_t *pb = w.pbits + (int64_t)c * nb;
+        if (bound >= kNarrowBound) {
+            for (int D = lane; D < nb; D += 64)
+                pb[D] = 0;
+            return;
+        }
+        int64_t *ppb = w.bsum + (int64_t)c * 2 * (nb + 1);
+        int64_t *bb = ppb + (nb + 1);
+        __syncthreads();  // pre[] of every lane written
+        for (int b = 1 + lane; b <= nb; b += 64) {
+            const int hi = min(b * kT, L);
+            int64_t sP = 0, sB = 0;
+            for (int l = (b - 1) * kT + 1; l <= hi; ++l) {
+                sP += pre[l];
+                sB += r.ub[l - 1];
             }
-            w.flags[c] = mode;
+            ppb[b] = sP;
+            bb[b] = sB;
+        }
+        __syncthreads();
+        // block sums -> sums up to the block ends, 64 blocks per step
+        int64_t carry_p = 0, carry_b = 0;
+        for (int b0 = 1; b0 <= nb; b0 += 64) {
+            const int b = b0 + lane;
+            int64_t vp = b <= nb ? ppb[b] : 0, vb = b <= nb ? bb[b] : 0;
+            for (int off = 1; off < 64; off *= 2) {
+                const int64_t up = __shfl_up(vp, off), ub = __shfl_up(vb, off);
+                if (lane >= off) {
+                    vp += up;
+                    vb += ub;
+                }
+            }
+            vp += carry_p;
+            vb += carry_b;
+            if (b <= nb) {
+                ppb[b] = vp;
+                bb[b] = vb;
+            }
+            carry_p = __shfl(vp, 63);
+            carry_b = __shfl(vb, 63);
+        }
+        if (lane == 0) {
+            ppb[0] = 0;
+            bb[0] = 0;
+        }
+        __syncthreads();
+        for (int D = lane; D < nb; D += 64) {
+            int64_t vmax = 0;
+            for (int I = 0; I + D < nb; ++I) {
+                const int x = I * kT, yb = I + D + 1, y = min(yb * kT, L);
+                vmax = max(vmax, ppb[yb] - ppb[I] - (int64_t)(y - x) * pre[x] + bb[yb] - bb[I]);
+            }
+            const uint64_t q = 0xFFFFFFFFull / ((uint64_t)vmax + 1);  // >= 4: vmax <= V < 2^30
+            pb[D] = 63 - __clzll((long long)q);
         }
         return;
     }
@@ -553,12 +613,12 @@ __global__ __launch_bounds__(256) void diag_split_kernel(const int64_t *__restri
         diag_split_body<Wide>(r, cw, L, M, m, pitch, s, t, wave, part, tab, dtab);
 }
 
-// Whether the middle products of a chain whose middle split range has
-// span + 1 splits use packed keys.
-__device__ inline bool middle_packed(int32_t mode, int span)
+// Whether the middle products of block-diagonal D of a chain, whose middle
+// split range has span + 1 splits, use packed keys.
+__device__ inline bool middle_packed(const ChainWork &cw, int D, int span)
 {
     const int S = span > 0 ? 32 - __clz(span) : 0;
-    return (mode & kModeNarrow) && S <= packed_bits(mode);
+    return cw.narrow && S <= cw.pbits[D];
 }
 
 // Middle splits of every block (I, I + D) of one block-diagonal.  A workgroup
@@ -692,7 +752,7 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     const int k_lo = (I + 1) * kT;
     const int k_hi = J * kT;
-    if (middle_packed(w.flags[c], k_hi - k_lo))
+    if (middle_packed(cw, delta, k_hi - k_lo))
         return;  // middle_packed_kernel takes this chain
     if (cw.narrow)
         middle_body<Narrow>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, tab);
@@ -788,15 +848,15 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     const int m = tile.x * 64 + lane;
     const int k_lo = (I + 1) * kT;
     const int k_hi = J * kT;
+    const ChainWork cw = chain_work(w, L, rows, pitch, c);
     // uniform over the workgroup: every wave returns or none does
-    if (!middle_packed(w.flags[c], k_hi - k_lo))
+    if (!middle_packed(cw, delta, k_hi - k_lo))
         return;
     const int s0 = I * kT + (wave >> 1) * kSub + 1;
     const int t0 = J * kT + (wave & 1) * kSub + 1;
     const int nt = t0 <= L ? min(kSub, L - t0 + 1) : 0;
     const int S = k_hi > k_lo ? 32 - __clz(k_hi - k_lo) : 0;
     const ChainRows r = chain_rows(params, L, c);
-    const ChainWork cw = chain_work(w, L, rows, pitch, c);
     const int mc = m <= M ? m : M;
     const int n_stages = (k_hi - k_lo + kStage) / kStage;
 
@@ -911,7 +971,7 @@ __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &c
     // packed key in the compact copy, or (value << 32) | s' in the cost
     // table) and the C_2 operand (the lane's own budget when C_2 is out of
     // reach)
-    const bool packed_partial = P::kShadow && middle_packed(cw.mode, k_hi - k_lo);
+    const bool packed_partial = P::kShadow && middle_packed(cw, (k_hi - k_lo) / kT + 1, k_hi - k_lo);
     const uint32_t key = packed_partial ? load32(cw.shadow + cell * pitch, m) : 0u;
     const int64_t stored64 = packed_partial ? 0 : load64(tab + cell * pitch, m);
     const int ri = m - (int)r.wabar[s - 1];
@@ -990,8 +1050,11 @@ WorkLayout work_layout(int n_chains, int L, int64_t pitch)
     const uint64_t rows = (uint64_t)L * (L + 1) / 2;
     WorkLayout wl;
     wl.flags = 0;
+    const uint64_t nb = (uint64_t)((L + kT - 1) / kT);
     wl.pre = align(wl.flags + 4ull * n_chains);
-    wl.gnone = align(wl.pre + 8ull * n_chains * (L + 1));
+    wl.pbits = align(wl.pre + 8ull * n_chains * (L + 1));
+    wl.bsum = align(wl.pbits + 4ull * n_chains * nb);
+    wl.gnone = align(wl.bsum + 16ull * n_chains * (nb + 1));
     wl.gall = align(wl.gnone + 4ull * n_chains * rows);
     wl.shadow = align(wl.gall + 4ull * n_chains * rows);
     wl.total = align(wl.shadow + 4ull * n_chains * rows * (uint64_t)pitch);
@@ -1005,6 +1068,8 @@ Work work_view(void *base, int n_chains, int L, int64_t pitch)
     Work w;
     w.flags = (int32_t *)(b + wl.flags);
     w.pre = (int64_t *)(b + wl.pre);
+    w.pbits = (int32_t *)(b + wl.pbits);
+    w.bsum = (int64_t *)(b + wl.bsum);
     w.gnone = (int32_t *)(b + wl.gnone);
     w.gall = (int32_t *)(b + wl.gall);
     w.shadow = (uint32_t *)(b + wl.shadow);

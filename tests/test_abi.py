@@ -72,9 +72,12 @@ def test_layout_rejects_bad_sizes(args):
 def test_workspace_size(n_chains, L, M):
     pitch, rows, cb, db = rotor.rotor_layout(n_chains, L, M)
     ws = rotor.rotor_workspace_bytes(n_chains, L, M)
-    # a 4-byte copy of every cell plus per-pair gates and per-stage prefixes
-    assert ws >= n_chains * rows * (4 * pitch + 8) + n_chains * 8 * (L + 1)
-    assert ws <= n_chains * rows * (4 * pitch + 8) + n_chains * 8 * (L + 1) + 5 * 256 + 4 * n_chains
+    # a 4-byte copy of every cell plus per-pair gates and per-stage prefixes,
+    # and per block of 16 stages a key width and two sums
+    nb = (L + 15) // 16
+    need = n_chains * rows * (4 * pitch + 8) + n_chains * 8 * (L + 1) + n_chains * (4 * nb + 16 * (nb + 1))
+    assert ws >= need
+    assert ws <= need + 7 * 256 + 4 * n_chains
     assert ws % 256 == 0
 
 

@@ -365,10 +365,47 @@ def test_narrow_chain_beyond_packed_keys(L, M, seed):
     # costs below 2^30 (compact copy) but too large to leave the split field
     # room once the middle range has 16 splits or more: the first
     # block-diagonal takes packed keys, the later ones the (value, split) pairs
+    # (their own bounds too leave too few bits)
     p = scaled_chain(seed, L, 12)
     v = cost_bound(p[0])
     assert (1 << 26) < v < (1 << 30)
     say(f"narrow beyond packed L={L} M={M} bound={v}")
+    _, cost, dec = solve_on_gpu(p, M, schedule="blocked")
+    assert_same(p, M, cost, dec)
+
+
+def key_bits(v):
+    """Largest S with (v + 1) << S <= 2^32 - 1: the split bits a packed key
+    has left beside a value of at most v."""
+    return (((1 << 32) - 1) // (v + 1)).bit_length() - 1
+
+
+def block_diagonal_bounds(p, L):
+    """cost_bound of the longest pairs of each block-diagonal D of 16-stage
+    blocks: the pairs of the blocks (I, I + D) lie within the stages
+    [16I + 1, min(16(I + D + 1), L)]."""
+    nb = (L + 15) // 16
+    return {D: max(cost_bound(p[:, 16 * I:min(16 * (I + D + 1), L)]) for I in range(nb - D)) for D in range(1, nb)}
+
+
+@pytest.mark.parametrize("seed,shift", [(8, 7), (8, 8), (8, 9), (7, 6)])
+def test_packed_keys_per_block_diagonal(seed, shift):
+    # The packed middle keys of block-diagonal D need (V_D + 1) << S to fit
+    # in 32 bits, with S the bits of its split range and V_D the bound of its
+    # longest pairs.  At these cost scales some block-diagonals fit with no
+    # bit to spare, others miss by one, and the whole chain's bound would
+    # have packed fewer of them.
+    L, M = 160, 240
+    p = scaled_chain(seed, L, shift)
+    v = cost_bound(p[0])
+    assert v < 1 << 30
+    vd = block_diagonal_bounds(p[0], L)
+    span_bits = {D: (16 * (D - 1)).bit_length() for D in vd}
+    packed = {D for D in vd if span_bits[D] <= key_bits(vd[D])}
+    assert {D for D in vd if span_bits[D] <= key_bits(v)} < packed
+    assert any(span_bits[D] == key_bits(vd[D]) for D in packed)
+    assert any(span_bits[D] == key_bits(vd[D]) + 1 for D in vd)
+    say(f"packed per block-diagonal seed={seed} shift={shift} bound={v} packed={sorted(packed)}")
     _, cost, dec = solve_on_gpu(p, M, schedule="blocked")
     assert_same(p, M, cost, dec)
 
