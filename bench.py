@@ -68,13 +68,24 @@ def cpu_baseline(params, M, stages):
 
 
 def arithmetic_type(params):
-    """The integer type the fill computes in: uint32 with saturation when every
-    chain's cost bound sum_j (L - j + 1) u_f^j + sum_j u_b^j is below 2^30 (the
-    library makes the same test on the device), else int64."""
+    """The integer types the fill computes in.  The library takes uint32 with
+    saturation for the pairs whose block-diagonal of 16-stage blocks has a cost
+    bound below 2^30 (the bound of a sub-chain [s, t] is
+    sum_{j=s}^{t} (t - j + 1) u_f^j + sum_{j=s}^{t} u_b^j, and it grows with the
+    sub-chain), int64 for the others: "u32" when that holds for the whole
+    chain, "int64" when not even for one block, else "u32+int64"."""
     import numpy as np
     p = params if params.ndim == 3 else params[None]
-    bound = max(int(np.cumsum(c[0].astype(object)).sum() + c[1].astype(object).sum()) for c in p)
-    return "u32" if bound < (1 << 30) else "int64"
+
+    def bound(c, lo, hi):
+        return int(np.cumsum(c[0, lo:hi].astype(object)).sum() + c[1, lo:hi].astype(object).sum())
+
+    L = p.shape[-1]
+    whole = max(bound(c, 0, L) for c in p)
+    block = max(bound(c, b, min(b + 16, L)) for c in p for b in range(0, L, 16))
+    if whole < (1 << 30):
+        return "u32"
+    return "int64" if block >= (1 << 30) else "u32+int64"
 
 
 def kernel_code_digest(path=None):

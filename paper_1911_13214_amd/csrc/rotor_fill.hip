@@ -9,18 +9,22 @@
 // u_f^s + u_b^s + C(s+1, t, m - w_abar^s).  Every term lies on a strictly
 // shorter sub-chain.  Ties go to the smallest s', then to C_1 over C_2.
 //
-// Value paths, chosen per chain by prep_kernel from a bound V on every
-// finite cost: stage j runs forward at most L - j + 1 times in any schedule of
-// the family (induction on the recurrence), so V = sum_j (L - j + 1) u_f^j +
-// sum_j u_b^j, and every C_1 or C_2 candidate, being the time of such a
-// schedule of its sub-chain, is at most V.
-//  - narrow, when V < 2^30: operands are read from a compact uint32 copy of
-//    the table (INT64_MAX stored as 0xFFFFFFFF) and added with unsigned
-//    saturation; the best value and its split are kept side by side and
-//    splits are visited in increasing s' with a strict <;
-//  - packed (middle products of narrow chains, when (V_D + 1) << S fits
-//    below 2^32 - 1 for the S bits of the block's middle split range, V_D
-//    being the same bound for the longest sub-chains of the block-diagonal):
+// Value paths, chosen per block-diagonal by prep_kernel from a bound on
+// every finite cost: stage j runs forward at most t - j + 1 times in any
+// schedule of the family for [s, t] (induction on the recurrence), so
+// V(s, t) = sum_{j=s}^{t} (t - j + 1) u_f^j + sum_{j=s}^{t} u_b^j bounds
+// every C_1 or C_2 candidate of the pair, being the time of such a schedule.
+// V grows with the sub-chain, so V_D, V over the longest sub-chains of the
+// 16 x 16 blocks of block-diagonal D (D = 0: within one block), bounds every
+// pair of the block-diagonal and grows with D; a pair's operands are
+// sub-chains of it, of block-diagonals up to its own.
+//  - narrow, when V_D < 2^30: operands are read from a compact uint32 copy of
+//    the table (INT64_MAX stored as 0xFFFFFFFF), which the pairs of narrow
+//    block-diagonals write, and added with unsigned saturation; the best
+//    value and its split are kept side by side and splits are visited in
+//    increasing s' with a strict <;
+//  - packed (middle products of narrow block-diagonals, when (V_D + 1) << S
+//    fits below 2^32 - 1 for the S bits of the block's middle split range):
 //    a candidate is one uint32 key (value << S) | (s' - first middle split),
 //    so one saturating add and one unsigned min relax it, ties going to the
 //    smaller split;
@@ -100,18 +104,20 @@ __device__ inline uint32_t load32(const uint32_t *row, int m)
 __device__ inline uint32_t sat_add(uint32_t a, uint32_t b) { return __builtin_elementwise_add_sat(a, b); }
 __device__ inline uint64_t umin(uint64_t a, uint64_t b) { return b < a ? b : a; }
 
-// Per-chain mode word written by prep_kernel: bit 0 narrow path.
-constexpr int32_t kModeNarrow = 1;
-
 // Per-chain views of the workspace.
 struct ChainWork {
     const int64_t *pre;    // [L+1] prefix sums of u_f
     const int32_t *gnone;  // [rows] m_none(s, t), t > s
     const int32_t *gall;   // [rows] m_all(s, t)
-    uint32_t *shadow;      // [rows][pitch] compact copy of the costs
-    const int32_t *pbits;  // [nb] largest S with (V_D + 1) << S <= 2^32 - 1, per block-diagonal D
-    bool narrow;
+    uint32_t *shadow;      // [rows][pitch] compact copy of the costs (narrow block-diagonals)
+    const int32_t *pbits;  // [nb] per block-diagonal D: the largest S with (V_D + 1) << S <= 2^32 - 1,
+                           // or -1 if V_D >= 2^30 (64-bit path)
+    // whether the pairs of block-diagonal D take the narrow path
+    __device__ bool narrow(int D) const { return pbits[D] >= 0; }
 };
+
+// Block-diagonal of the pair (s, t): D = J - I for s in block I, t in block J.
+__device__ inline int block_diag(int s, int t) { return (t - 1) / kT - (s - 1) / kT; }
 
 __device__ inline ChainWork chain_work(const Work &w, int L, int64_t rows, int64_t pitch, int c)
 {
@@ -121,7 +127,6 @@ __device__ inline ChainWork chain_work(const Work &w, int L, int64_t rows, int64
     cw.gall = w.gall + (int64_t)c * rows;
     cw.shadow = w.shadow + (int64_t)c * rows * pitch;
     cw.pbits = w.pbits + (int64_t)c * ((L + kT - 1) / kT);
-    cw.narrow = (w.flags[c] & kModeNarrow) != 0;
     return cw;
 }
 
@@ -256,7 +261,8 @@ __device__ inline void store_cell(int64_t *cost, int16_t *dec, uint32_t *shadow,
 
 // ---------------------------------------------------------------------------
 
-// Gates of every pair, prefix sums and value path of every chain.
+// Gates of every pair, prefix sums of u_f, and the value path and packed key
+// width of every block-diagonal.
 // Workgroup s - 1 of a chain writes the gate row of s, 64 consecutive t per
 // step: m_all(s, t) (peak of F_all^s with delta^t stored, and of B^s with
 // delta^s stored) and m_none(s, t) (peak of F_ck^s and F_none^{s+1..t-1} with
@@ -264,7 +270,7 @@ __device__ inline void store_cell(int64_t *cost, int16_t *dec, uint32_t *shadow,
 // s < j < t in m_none is a running maximum along t: a wave prefix maximum
 // per step plus the carry of the steps before.  Gates above INT32_MAX are
 // clamped: any gate above M < 2^28 is never met.  The last workgroup of a
-// chain scans u_f with one wave.
+// chain scans u_f with one wave and bounds the costs of each block-diagonal.
 __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ params, int L, int64_t rows, Work w)
 {
     const int c = blockIdx.y;
@@ -275,11 +281,9 @@ __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ pa
         // lane l sums a segment of stages, then the segment sums are scanned
         const int seg = (L + 63) / 64;
         const int lo = min(L, lane * seg), hi = min(L, lo + seg);
-        uint64_t su = 0, sb = 0, sp = 0;
-        for (int l = lo; l < hi; ++l) {
+        uint64_t su = 0;
+        for (int l = lo; l < hi; ++l)
             su += (uint64_t)r.uf[l];
-            sb += (uint64_t)r.ub[l];
-        }
         uint64_t incl = su;
         for (int off = 1; off < 64; off *= 2) {
             const uint64_t v = __shfl_up(incl, off);
@@ -291,43 +295,24 @@ __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ pa
         for (int l = lo; l < hi; ++l) {
             run += (uint64_t)r.uf[l];
             pre[l + 1] = (int64_t)run;
-            sp += run;
         }
-        for (int off = 32; off > 0; off /= 2) {
-            sb += __shfl_xor(sb, off);
-            sp += __shfl_xor(sp, off);
-        }
-        // V = sum_l P[l] + sum_j u_b^j = sum_j (L - j + 1) u_f^j + sum_j u_b^j
-        // (below 2^60 in the domain)
-        const uint64_t bound = sp + sb;
-        if (lane == 63) {
+        if (lane == 0)
             pre[0] = 0;
-            w.flags[c] = bound < kNarrowBound ? kModeNarrow : 0;
-        }
-        // Packed middle keys, per block-diagonal D: every candidate of a block
-        // (I, I + D) is the time of a schedule of one of its pairs (s, t), so
-        // at most V(s, t) = sum_{l=s}^{t} (P[l] - P[s-1]) + sum_{j=s}^{t} u_b^j,
-        // which grows with t - s: the block's bound is V over [16I + 1,
-        // min(16(I + D + 1), L)], and V_D the largest over I.  With PP and B
-        // the sums of P and of u_b up to a stage,
-        // V(x + 1, y) = PP[y] - PP[x] - (y - x) P[x] + B[y] - B[x];
+        // Value path and packed key width of every block-diagonal D from V_D,
+        // the largest over I of V over [16I + 1, min(16(I + D + 1), L)].  With
+        // PP and B the sums of P and of u_b up to a stage,
+        // V(x + 1, y) = sum_{l=x+1}^{y} (P[l] - P[x]) + B[y] - B[x]
+        //             = PP[y] - PP[x] - (y - x) P[x] + B[y] - B[x];
         // bsum keeps PP and B at the block ends min(16b, L), b = 0..nb.
         const int nb = (L + kT - 1) / kT;
-        if (nb < 2)
-            return;
         int32_t *pb = w.pbits + (int64_t)c * nb;
-        if (bound >= kNarrowBound) {
-            for (int D = lane; D < nb; D += 64)
-                pb[D] = 0;
-            return;
-        }
         int64_t *ppb = w.bsum + (int64_t)c * 2 * (nb + 1);
         int64_t *bb = ppb + (nb + 1);
         __syncthreads();  // pre[] of every lane written
         for (int b = 1 + lane; b <= nb; b += 64) {
-            const int hi = min(b * kT, L);
+            const int bhi = min(b * kT, L);
             int64_t sP = 0, sB = 0;
-            for (int l = (b - 1) * kT + 1; l <= hi; ++l) {
+            for (int l = (b - 1) * kT + 1; l <= bhi; ++l) {
                 sP += pre[l];
                 sB += r.ub[l - 1];
             }
@@ -362,13 +347,14 @@ __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ pa
         }
         __syncthreads();
         for (int D = lane; D < nb; D += 64) {
-            int64_t vmax = 0;
+            int64_t vmax = 0;  // below 2^45 in the domain
             for (int I = 0; I + D < nb; ++I) {
                 const int x = I * kT, yb = I + D + 1, y = min(yb * kT, L);
                 vmax = max(vmax, ppb[yb] - ppb[I] - (int64_t)(y - x) * pre[x] + bb[yb] - bb[I]);
             }
-            const uint64_t q = 0xFFFFFFFFull / ((uint64_t)vmax + 1);  // >= 4: vmax <= V < 2^30
-            pb[D] = 63 - __clzll((long long)q);
+            // (V_D + 1) << S <= 2^32 - 1 leaves S >= 2 bits on the narrow path
+            pb[D] = (uint64_t)vmax < kNarrowBound ? 63 - __clzll((long long)(0xFFFFFFFFull / ((uint64_t)vmax + 1)))
+                                                  : -1;
         }
         return;
     }
@@ -417,7 +403,7 @@ __global__ __launch_bounds__(256) void leaf_kernel(const int64_t *__restrict__ p
     const int64_t v = r.uf[s - 1] + r.ub[s - 1];
     cost[(int64_t)c * rows * pitch + idx] = ok ? v : kInf;
     dec[(int64_t)c * rows * pitch + idx] = ok ? 0 : -1;
-    if (cw.narrow)
+    if (cw.narrow(0))
         cw.shadow[idx] = ok ? (uint32_t)v : kInf32;
 }
 
@@ -542,7 +528,7 @@ __global__ __launch_bounds__(256) void diag_kernel(const int64_t *__restrict__ p
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
-    if (cw.narrow)
+    if (cw.narrow(block_diag(s, t)))
         diag_body<Narrow>(r, cw, L, m, pitch, s, t, tab, dtab);
     else
         diag_body<Wide>(r, cw, L, m, pitch, s, t, tab, dtab);
@@ -607,7 +593,7 @@ __global__ __launch_bounds__(256) void diag_split_kernel(const int64_t *__restri
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
-    if (cw.narrow)
+    if (cw.narrow(block_diag(s, t)))
         diag_split_body<Narrow>(r, cw, L, M, m, pitch, s, t, wave, part, tab, dtab);
     else
         diag_split_body<Wide>(r, cw, L, M, m, pitch, s, t, wave, part, tab, dtab);
@@ -618,7 +604,7 @@ __global__ __launch_bounds__(256) void diag_split_kernel(const int64_t *__restri
 __device__ inline bool middle_packed(const ChainWork &cw, int D, int span)
 {
     const int S = span > 0 ? 32 - __clz(span) : 0;
-    return cw.narrow && S <= cw.pbits[D];
+    return cw.narrow(D) && S <= cw.pbits[D];
 }
 
 // Middle splits of every block (I, I + D) of one block-diagonal.  A workgroup
@@ -753,8 +739,8 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
     const int k_lo = (I + 1) * kT;
     const int k_hi = J * kT;
     if (middle_packed(cw, delta, k_hi - k_lo))
-        return;  // middle_packed_kernel takes this chain
-    if (cw.narrow)
+        return;  // middle_packed_kernel takes this block-diagonal
+    if (cw.narrow(delta))
         middle_body<Narrow>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, tab);
     else
         middle_body<Wide>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, tab);
@@ -1022,7 +1008,7 @@ __global__ __launch_bounds__(kEdgeThreads) void edge_kernel(const int64_t *__res
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
-    if (cw.narrow)
+    if (cw.narrow(delta))
         edge_body<Narrow>(r, cw, L, m, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
     else
         edge_body<Wide>(r, cw, L, m, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
@@ -1049,9 +1035,8 @@ WorkLayout work_layout(int n_chains, int L, int64_t pitch)
     auto align = [](uint64_t x) { return (x + 255) / 256 * 256; };
     const uint64_t rows = (uint64_t)L * (L + 1) / 2;
     WorkLayout wl;
-    wl.flags = 0;
     const uint64_t nb = (uint64_t)((L + kT - 1) / kT);
-    wl.pre = align(wl.flags + 4ull * n_chains);
+    wl.pre = 0;
     wl.pbits = align(wl.pre + 8ull * n_chains * (L + 1));
     wl.bsum = align(wl.pbits + 4ull * n_chains * nb);
     wl.gnone = align(wl.bsum + 16ull * n_chains * (nb + 1));
@@ -1066,7 +1051,6 @@ Work work_view(void *base, int n_chains, int L, int64_t pitch)
     const WorkLayout wl = work_layout(n_chains, L, pitch);
     char *b = (char *)base;
     Work w;
-    w.flags = (int32_t *)(b + wl.flags);
     w.pre = (int64_t *)(b + wl.pre);
     w.pbits = (int32_t *)(b + wl.pbits);
     w.bsum = (int64_t *)(b + wl.bsum);

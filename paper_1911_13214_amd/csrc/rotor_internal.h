@@ -34,14 +34,13 @@ struct Tables {
     int64_t rows;           // L(L+1)/2
 };
 
-// Device workspace of a fill: per-chain value-path flag, prefix sums of u_f,
-// per block-diagonal key widths and the sums they are computed from, the
-// gates m_none and m_all of every pair, and a compact uint32 copy of the
-// cost table (used by chains whose costs stay below 2^30).
+// Device workspace of a fill: prefix sums of u_f, per block-diagonal value
+// path and packed key width and the sums they are computed from, the gates
+// m_none and m_all of every pair, and a compact uint32 copy of the cost table
+// (written and read by the pairs whose costs stay below 2^30).
 struct Work {
-    int32_t *flags;    // [n_chains]
     int64_t *pre;      // [n_chains][L + 1]
-    int32_t *pbits;    // [n_chains][nb], nb = ceil(L / 16): packed key bits of block-diagonal D
+    int32_t *pbits;    // [n_chains][nb], nb = ceil(L / 16): packed key bits of block-diagonal D, -1: 64-bit path
     int64_t *bsum;     // [n_chains][2][nb + 1]: sums of prefix sums of u_f, and of u_b, to block ends
     int32_t *gnone;    // [n_chains][rows]
     int32_t *gall;     // [n_chains][rows]
@@ -50,7 +49,7 @@ struct Work {
 
 // Byte offsets of the workspace sections (each 256-byte aligned).
 struct WorkLayout {
-    uint64_t flags, pre, pbits, bsum, gnone, gall, shadow, total;
+    uint64_t pre, pbits, bsum, gnone, gall, shadow, total;
 };
 WorkLayout work_layout(int n_chains, int L, int64_t pitch);
 Work work_view(void *base, int n_chains, int L, int64_t pitch);

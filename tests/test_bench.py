@@ -41,6 +41,10 @@ def test_arithmetic_type_follows_the_cost_bound():
     p = chaingen.random_chains(1, 500, seed=5, wa_hi=20)
     p[:, chaingen.UF] <<= 10
     p[:, chaingen.UB] <<= 10
+    # the whole chain's bound is past 2^30, the bounds of single blocks are not
+    assert bench.arithmetic_type(p) == "u32+int64"
+    p[:, chaingen.UF] <<= 12
+    p[:, chaingen.UB] <<= 12
     assert bench.arithmetic_type(p) == "int64"
     # the bound sum_l P[l] + sum u_b just below and at 2^30
     L = 4

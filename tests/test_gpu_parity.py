@@ -411,6 +411,25 @@ def test_packed_keys_per_block_diagonal(seed, shift):
 
 
 @pytest.mark.parametrize("schedule", SCHEDULES)
+@pytest.mark.parametrize("shift", [11, 12, 14, 16])
+def test_value_path_per_block_diagonal(shift, schedule):
+    # A chain whose cost bound is past 2^30 while the bounds of its shorter
+    # sub-chains are not: the pairs of the first block-diagonals take the
+    # 4-byte path (compact copy, saturating adds), the later ones the 64-bit
+    # keys, in both fill orders.
+    L, M = 160, 240
+    p = scaled_chain(8, L, shift)
+    nb = (L + 15) // 16
+    vd = {0: max(cost_bound(p[0][:, 16 * I:min(16 * (I + 1), L)]) for I in range(nb))}
+    vd.update(block_diagonal_bounds(p[0], L))
+    narrow = [D for D in range(nb) if vd[D] < 1 << 30]
+    assert cost_bound(p[0]) >= 1 << 30 and narrow == list(range(len(narrow))) and 0 < len(narrow) < nb
+    say(f"value path per block-diagonal shift={shift} narrow={narrow} {schedule}")
+    _, cost, dec = solve_on_gpu(p, M, schedule=schedule)
+    assert_same(p, M, cost, dec)
+
+
+@pytest.mark.parametrize("schedule", SCHEDULES)
 def test_batch_mixing_value_paths(schedule):
     # chains of one call may take different value paths
     params = chaingen.random_chains(6, 37, seed=21)
