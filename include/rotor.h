@@ -137,9 +137,10 @@ ROTOR_API int64_t rotor_row_index(int32_t L, int32_t s, int32_t t);
 ROTOR_API int32_t rotor_check_params(const int64_t *h_params, int32_t n_chains, int32_t L, int64_t M);
 
 /* Bytes of device workspace rotor_solve needs for these sizes: per-pair
- * gates, prefix sums, per-chain flags, a few words per block of 16 stages
- * and a compact 4-byte-per-cell copy of the cost table (about 40% of
- * cost_bytes + dec_bytes).  Host only.  Returns
+ * gates, prefix sums, a few words per block of 16 stages, a compact
+ * 4-byte-per-cell copy of the cost table (about 40% of cost_bytes +
+ * dec_bytes) and, for chains of more than 16 stages, a 2-byte copy of the
+ * cells of the 16 x 16 diagonal blocks.  Host only.  Returns
  * ROTOR_OK or ROTOR_EINVAL (as rotor_layout). */
 ROTOR_API int32_t rotor_workspace_bytes(int32_t n_chains, int32_t L, int64_t M, uint64_t *bytes);
 

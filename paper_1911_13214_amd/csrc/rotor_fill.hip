@@ -112,8 +112,20 @@ struct ChainWork {
     uint32_t *shadow;      // [rows][pitch] compact copy of the costs (narrow block-diagonals)
     const int32_t *pbits;  // [nb] per block-diagonal D: the largest S with (V_D + 1) << S <= 2^32 - 1,
                            // or -1 if V_D >= 2^30 (64-bit path)
+    int16_t *half;         // [16 L][hpitch] 2-byte copy of the diagonal blocks' cells
+    int64_t hpitch;
     // whether the pairs of block-diagonal D take the narrow path
     __device__ bool narrow(int D) const { return pbits[D] >= 0; }
+    // whether the diagonal blocks' costs fit the 2-byte copy: (V_0 + 1) << 17
+    // <= 2^32 - 1, i.e. V_0 <= 2^15 - 2, so finite values stay positive as
+    // int16 and infinity is stored as -1 (0xFFFF)
+    __device__ bool diag16() const { return pbits[0] >= 17; }
+    // row of the pair (s, t) of a diagonal block in the 2-byte copy:
+    // 16 (s - 1) + (t - 1) mod 16
+    __device__ int16_t *half_row(int s, int t) const
+    {
+        return half + ((int64_t)(s - 1) * kT + (t - 1) % kT) * hpitch;
+    }
 };
 
 // Block-diagonal of the pair (s, t): D = J - I for s in block I, t in block J.
@@ -127,6 +139,8 @@ __device__ inline ChainWork chain_work(const Work &w, int L, int64_t rows, int64
     cw.gall = w.gall + (int64_t)c * rows;
     cw.shadow = w.shadow + (int64_t)c * rows * pitch;
     cw.pbits = w.pbits + (int64_t)c * ((L + kT - 1) / kT);
+    cw.hpitch = half_pitch_of(pitch);
+    cw.half = w.half + (int64_t)c * L * kT * cw.hpitch;
     return cw;
 }
 
@@ -353,8 +367,15 @@ __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ pa
                 vmax = max(vmax, ppb[yb] - ppb[I] - (int64_t)(y - x) * pre[x] + bb[yb] - bb[I]);
             }
             // (V_D + 1) << S <= 2^32 - 1 leaves S >= 2 bits on the narrow path
-            pb[D] = (uint64_t)vmax < kNarrowBound ? 63 - __clzll((long long)(0xFFFFFFFFull / ((uint64_t)vmax + 1)))
-                                                  : -1;
+            int bits = (uint64_t)vmax < kNarrowBound
+                           ? 63 - __clzll((long long)(0xFFFFFFFFull / ((uint64_t)vmax + 1)))
+                           : -1;
+            // D = 0 has no middle products; its width only says whether the
+            // 2-byte copy of the diagonal blocks is used (>= 17), which only
+            // the edges of a chain of two blocks or more read
+            if (D == 0 && nb < 2)
+                bits = min(bits, 16);
+            pb[D] = bits;
         }
         return;
     }
@@ -405,6 +426,8 @@ __global__ __launch_bounds__(256) void leaf_kernel(const int64_t *__restrict__ p
     dec[(int64_t)c * rows * pitch + idx] = ok ? 0 : -1;
     if (cw.narrow(0))
         cw.shadow[idx] = ok ? (uint32_t)v : kInf32;
+    if (cw.diag16())
+        cw.half_row(s, s)[m] = ok ? (int16_t)v : (int16_t)-1;
 }
 
 // Row cursor of a run of splits of one pair (s, t): the X row (s, k) and the
@@ -484,6 +507,75 @@ __device__ __forceinline__ void relax_run(typename P::Acc &acc, const ChainRows 
     RelaxRun<P, kT - 1>::go(n, acc, r, m, k0, cur, prefix);
 }
 
+// Operand loads of the narrow path from the compact copy (4 bytes) or from
+// the 2-byte copy of the diagonal blocks (a sign-extending load: finite
+// values there are below 2^15, and the infinity 0xFFFF becomes 0xFFFFFFFF).
+typedef const __attribute__((address_space(1))) int16_t *global_c16;
+struct Load32 {
+    __device__ static uint32_t at(const char *row, int m) { return *(global_c32)(row + (uint32_t)m * 4u); }
+};
+struct Load16 {
+    __device__ static uint32_t at(const char *row, int m)
+    {
+        return (uint32_t)(int32_t) * (global_c16)(row + (uint32_t)m * 2u);
+    }
+};
+
+// Cursor of a narrow run whose X and Y rows come from different copies: X
+// moves xstep bytes per split, Y ystep bytes, and ystep shrinks by ydec.
+struct MixedCursor {
+    const char *x;
+    const char *y;
+    int64_t xstep;
+    int64_t ystep;
+    int64_t ydec;
+};
+
+// relax_fixed for a MixedCursor: N consecutive splits k0 .. k0 + N - 1, all
+// loads issued first.
+template <class XL, class YL, int N>
+__device__ __forceinline__ void relax_mixed(Narrow::Acc &acc, const ChainRows &r, int m, int k0, MixedCursor &cur,
+                                            uint64_t &prefix)
+{
+    uint32_t rx[N], ry[N];
+    int ri[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        ri[i] = m - (int)r.wa[k0 + i - 1];
+        rx[i] = XL::at(cur.x, m);
+        // a budget shifted below 0 reads the lane's own budget (in bounds)
+        ry[i] = YL::at(cur.y, ri[i] >= 0 ? ri[i] : m);
+        cur.x += cur.xstep;
+        cur.y += cur.ystep;
+        cur.ystep -= cur.ydec;
+    }
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const int k = k0 + i;
+        prefix += (uint64_t)r.uf[k - 1];
+        Narrow::relax(acc, Narrow::xop(rx[i], prefix, 0, ri[i] >= 0), ry[i], (uint32_t)(k + 1));
+    }
+}
+
+template <class XL, class YL, int N>
+struct MixedRun {
+    __device__ __forceinline__ static void go(int n, Narrow::Acc &acc, const ChainRows &r, int m, int k0,
+                                              MixedCursor &cur, uint64_t &prefix)
+    {
+        if (n == N)
+            relax_mixed<XL, YL, N>(acc, r, m, k0, cur, prefix);
+        else
+            MixedRun<XL, YL, N - 1>::go(n, acc, r, m, k0, cur, prefix);
+    }
+};
+template <class XL, class YL>
+struct MixedRun<XL, YL, 0> {
+    __device__ __forceinline__ static void go(int, Narrow::Acc &, const ChainRows &, int, int, MixedCursor &,
+                                              uint64_t &)
+    {
+    }
+};
+
 // Eq. (DP:mainrec) for one pair (s, t), all splits in straight-line runs of
 // up to kT - 1.  Rows (s, s'-1) are consecutive; the row of (s'+1, t) is
 // L - s' rows after the row of (s', t).
@@ -508,6 +600,10 @@ __device__ __forceinline__ void diag_body(const ChainRows &r, const ChainWork &c
     if (all_ok)
         P::relax_all(acc, c2, (uint64_t)(r.uf[s - 1] + r.ub[s - 1]));
     store_cell<P>(tab, dtab, cw.shadow, cell * pitch + m, acc);
+    if constexpr (P::kShadow) {
+        if (cw.diag16() && block_diag(s, t) == 0)
+            cw.half_row(s, t)[m] = P::finite(acc) ? (int16_t)P::value(acc) : (int16_t)-1;
+    }
 }
 
 // The pairs (s, s + d): inside the 16 x 16 diagonal blocks only (blocked
@@ -948,7 +1044,7 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
 // (I, I + D) of one block-diagonal; a workgroup is one cell at 128 budgets.
 // Splits are met in increasing order: low, then the stored middle partial,
 // then high.
-template <class P>
+template <class P, bool H>
 __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &cw, int L, int m, int64_t pitch,
                                           int s, int t, int k_lo, int k_hi, int64_t *tab, int16_t *dtab)
 {
@@ -968,8 +1064,16 @@ __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &c
     P::init(acc);
     // low splits k = s .. k_lo - 1: X from block (I, I), Y from this block
     uint64_t prefix = 0;
-    RowCursor low = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, s);
-    relax_run<P>(acc, r, m, s, k_lo - s, low, prefix);
+    const int64_t rb = pitch * 4, hb = cw.hpitch * 2;
+    if constexpr (H) {
+        // X rows (s, k) of the 2-byte copy are consecutive
+        MixedCursor low{(const char *)cw.half_row(s, s), (const char *)(cw.shadow + row_of(L, s + 1, t) * pitch), hb,
+                        (int64_t)(L - s - 1) * rb, rb};
+        MixedRun<Load16, Load32, kT - 1>::go(k_lo - s, acc, r, m, s, low, prefix);
+    } else {
+        RowCursor low = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, s);
+        relax_run<P>(acc, r, m, s, k_lo - s, low, prefix);
+    }
     // middle splits: the stored partial counts u_f from k_lo on
     int64_t stored = stored64;
     if (packed_partial) {
@@ -980,8 +1084,15 @@ __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &c
     P::merge_stored(acc, stored, prefix);
     // high splits k = 16J + 1 .. t - 1: X from this block, Y from block (J, J)
     prefix += (uint64_t)(cw.pre[k_hi] - cw.pre[k_lo - 1]);
-    RowCursor high = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, k_hi + 1);
-    relax_run<P>(acc, r, m, k_hi + 1, t - k_hi - 1, high, prefix);
+    if constexpr (H) {
+        // Y rows (k + 1, t) of the 2-byte copy are 16 rows apart
+        MixedCursor high{(const char *)(cw.shadow + row_of(L, s, k_hi + 1) * pitch),
+                         (const char *)cw.half_row(k_hi + 2, t), rb, kT * hb, 0};
+        MixedRun<Load32, Load16, kT - 1>::go(t - k_hi - 1, acc, r, m, k_hi + 1, high, prefix);
+    } else {
+        RowCursor high = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, k_hi + 1);
+        relax_run<P>(acc, r, m, k_hi + 1, t - k_hi - 1, high, prefix);
+    }
     if (m < cw.gnone[cell])
         P::init(acc);
     if (all_ok)
@@ -1008,10 +1119,12 @@ __global__ __launch_bounds__(kEdgeThreads) void edge_kernel(const int64_t *__res
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
-    if (cw.narrow(delta))
-        edge_body<Narrow>(r, cw, L, m, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
+    if (!cw.narrow(delta))
+        edge_body<Wide, false>(r, cw, L, m, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
+    else if (cw.diag16())
+        edge_body<Narrow, true>(r, cw, L, m, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
     else
-        edge_body<Wide>(r, cw, L, m, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
+        edge_body<Narrow, false>(r, cw, L, m, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
 }
 
 hipError_t check() { return hipGetLastError(); }
@@ -1042,7 +1155,9 @@ WorkLayout work_layout(int n_chains, int L, int64_t pitch)
     wl.gnone = align(wl.bsum + 16ull * n_chains * (nb + 1));
     wl.gall = align(wl.gnone + 4ull * n_chains * rows);
     wl.shadow = align(wl.gall + 4ull * n_chains * rows);
-    wl.total = align(wl.shadow + 4ull * n_chains * rows * (uint64_t)pitch);
+    wl.half = align(wl.shadow + 4ull * n_chains * rows * (uint64_t)pitch);
+    const uint64_t half_rows = nb >= 2 ? (uint64_t)L * kT : 0;  // no edges in a single block
+    wl.total = align(wl.half + 2ull * n_chains * half_rows * (uint64_t)half_pitch_of(pitch));
     return wl;
 }
 
@@ -1057,6 +1172,7 @@ Work work_view(void *base, int n_chains, int L, int64_t pitch)
     w.gnone = (int32_t *)(b + wl.gnone);
     w.gall = (int32_t *)(b + wl.gall);
     w.shadow = (uint32_t *)(b + wl.shadow);
+    w.half = (int16_t *)(b + wl.half);
     return w;
 }
 

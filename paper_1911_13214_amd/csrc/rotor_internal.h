@@ -22,6 +22,10 @@ __host__ __device__ inline int64_t row_of(int L, int s, int t)
 // (one cache line) after an aligned table base.
 __host__ __device__ inline int64_t pitch_of(int64_t M) { return (M + 1 + 31) / 32 * 32; }
 
+// Row pitch of the 2-byte copy of the diagonal blocks: a multiple of 64
+// elements (128 bytes).
+__host__ __device__ inline int64_t half_pitch_of(int64_t pitch) { return (pitch + 63) / 64 * 64; }
+
 // Everything one fill launch needs to address a batch of tables.
 struct Tables {
     const int64_t *params;  // [n_chains][6][L]
@@ -36,8 +40,10 @@ struct Tables {
 
 // Device workspace of a fill: prefix sums of u_f, per block-diagonal value
 // path and packed key width and the sums they are computed from, the gates
-// m_none and m_all of every pair, and a compact uint32 copy of the cost table
-// (written and read by the pairs whose costs stay below 2^30).
+// m_none and m_all of every pair, a compact uint32 copy of the cost table
+// (written and read by the pairs whose costs stay below 2^30), and a 2-byte
+// copy of the cells of the diagonal blocks (chains whose costs there stay
+// below 2^15).
 struct Work {
     int64_t *pre;      // [n_chains][L + 1]
     int32_t *pbits;    // [n_chains][nb], nb = ceil(L / 16): packed key bits of block-diagonal D, -1: 64-bit path
@@ -45,11 +51,12 @@ struct Work {
     int32_t *gnone;    // [n_chains][rows]
     int32_t *gall;     // [n_chains][rows]
     uint32_t *shadow;  // [n_chains][rows][pitch]
+    int16_t *half;     // [n_chains][nb][16][16][half_pitch]: 2-byte copy of the diagonal blocks' cells
 };
 
 // Byte offsets of the workspace sections (each 256-byte aligned).
 struct WorkLayout {
-    uint64_t pre, pbits, bsum, gnone, gall, shadow, total;
+    uint64_t pre, pbits, bsum, gnone, gall, shadow, half, total;
 };
 WorkLayout work_layout(int n_chains, int L, int64_t pitch);
 Work work_view(void *base, int n_chains, int L, int64_t pitch);

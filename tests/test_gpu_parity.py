@@ -429,6 +429,29 @@ def test_value_path_per_block_diagonal(shift, schedule):
     assert_same(p, M, cost, dec)
 
 
+@pytest.mark.parametrize("v0", [32752, 32766, 32767, 32768, 33600])
+def test_two_byte_copy_of_the_diagonal_blocks_at_its_limit(v0):
+    # The edges read the diagonal blocks' cells from a 2-byte copy when their
+    # bound V_0 (largest over the 16-stage blocks) is at most 2^15 - 2, else
+    # from the 4-byte copy.  Here u_f = 200, w_a = 1, w_abar = 2 on every
+    # stage and u_b = 347 but on stage 1, so V_0 is the first block's bound,
+    # and the oracle shows block cells reaching it: a value of 2^15 or more
+    # in the 2-byte copy would come back negative.
+    L, M = 40, 120
+    p = np.zeros((1, 6, L), dtype=np.int64)
+    p[0, chaingen.UF], p[0, chaingen.UB] = 200, 347
+    p[0, chaingen.WA], p[0, chaingen.WABAR] = 1, 2
+    p[0, chaingen.UB, 0] = 347 + v0 - (200 * 136 + 16 * 347)
+    assert max(cost_bound(p[0][:, b:b + 16]) for b in range(0, L, 16)) == v0
+    C, _ = oracle_tables(p, M)
+    block_cells = [orc.row(L, s, t) for s in range(1, L + 1) for t in range(s, min(L, (s - 1) // 16 * 16 + 16) + 1)]
+    finite = C[block_cells][C[block_cells] != np.iinfo(np.int64).max]
+    assert finite.max() == v0
+    say(f"two-byte diagonal blocks V_0={v0}")
+    _, cost, dec = solve_on_gpu(p, M, schedule="blocked")
+    assert_same(p, M, cost, dec)
+
+
 @pytest.mark.parametrize("schedule", SCHEDULES)
 def test_batch_mixing_value_paths(schedule):
     # chains of one call may take different value paths
