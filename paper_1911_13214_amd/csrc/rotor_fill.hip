@@ -1043,7 +1043,9 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
 // Edge splits, C_2 and the gates for the cells a + b = q of every block
 // (I, I + D) of one block-diagonal; a workgroup is one cell at 128 budgets.
 // Splits are met in increasing order: low, then the stored middle partial,
-// then high.
+// then high.  With H (narrow path, ChainWork::diag16), the operand that lies
+// in a diagonal block -- X of a low split, Y of a high one -- comes from the
+// 2-byte copy.
 template <class P, bool H>
 __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &cw, int L, int m, int64_t pitch,
                                           int s, int t, int k_lo, int k_hi, int64_t *tab, int16_t *dtab)
