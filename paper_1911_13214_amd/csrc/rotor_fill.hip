@@ -578,8 +578,10 @@ struct MixedRun<XL, YL, 0> {
 
 // Eq. (DP:mainrec) for one pair (s, t), all splits in straight-line runs of
 // up to kT - 1.  Rows (s, s'-1) are consecutive; the row of (s'+1, t) is
-// L - s' rows after the row of (s', t).
-template <class P>
+// L - s' rows after the row of (s', t).  With H (a pair inside a diagonal
+// block, narrow path, ChainWork::diag16) every operand comes from the 2-byte
+// copy, where the rows (s'+1, t) are 16 rows apart.
+template <class P, bool H>
 __device__ __forceinline__ void diag_body(const ChainRows &r, const ChainWork &cw, int L, int m, int64_t pitch,
                                           int s, int t, int64_t *tab, int16_t *dtab)
 {
@@ -588,13 +590,23 @@ __device__ __forceinline__ void diag_body(const ChainRows &r, const ChainWork &c
     const int ri = m - (int)r.wabar[s - 1];
     const bool all_ok = m >= cw.gall[cell] && ri >= 0;
     const int64_t below = row_of(L, s + 1, t) * pitch;
-    const typename P::Raw c2 = P::load(tab + below, cw.shadow + below, all_ok ? ri : m);
+    typename P::Raw c2;
+    if constexpr (H)
+        c2 = Load16::at((const char *)cw.half_row(s + 1, t), all_ok ? ri : m);
+    else
+        c2 = P::load(tab + below, cw.shadow + below, all_ok ? ri : m);
     typename P::Acc acc;
     P::init(acc);
     uint64_t prefix = 0;
-    RowCursor cur = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, s);
-    for (int k0 = s; k0 < t; k0 += kT - 1)
-        relax_run<P>(acc, r, m, k0, min(kT - 1, t - k0), cur, prefix);
+    if constexpr (H) {
+        const int64_t hb = cw.hpitch * 2;
+        MixedCursor cur{(const char *)cw.half_row(s, s), (const char *)cw.half_row(s + 1, t), hb, kT * hb, 0};
+        MixedRun<Load16, Load16, kT - 1>::go(t - s, acc, r, m, s, cur, prefix);  // t - s <= 15
+    } else {
+        RowCursor cur = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, s);
+        for (int k0 = s; k0 < t; k0 += kT - 1)
+            relax_run<P>(acc, r, m, k0, min(kT - 1, t - k0), cur, prefix);
+    }
     if (m < cw.gnone[cell])
         P::init(acc);
     if (all_ok)
@@ -624,10 +636,13 @@ __global__ __launch_bounds__(256) void diag_kernel(const int64_t *__restrict__ p
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
-    if (cw.narrow(block_diag(s, t)))
-        diag_body<Narrow>(r, cw, L, m, pitch, s, t, tab, dtab);
+    const int D = block_diag(s, t);
+    if (!cw.narrow(D))
+        diag_body<Wide, false>(r, cw, L, m, pitch, s, t, tab, dtab);
+    else if (D == 0 && cw.diag16())
+        diag_body<Narrow, true>(r, cw, L, m, pitch, s, t, tab, dtab);
     else
-        diag_body<Wide>(r, cw, L, m, pitch, s, t, tab, dtab);
+        diag_body<Narrow, false>(r, cw, L, m, pitch, s, t, tab, dtab);
 }
 
 // Streamed order for the longer diagonals: the d splits of each pair are
