@@ -1050,13 +1050,14 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     if (m > M || nt == 0)
         return;
     // the partial stays a packed key, in the cell's compact copy, which
-    // edge_kernel reads once and then overwrites with the final value
+    // edge_kernel reads once and then overwrites with the final value; used
+    // once, it is stored and loaded non-temporally
 #pragma unroll
     for (int i = 0; i < kSub; ++i)
 #pragma unroll
         for (int j = 0; j < kSub; ++j)
             if (j < nt)
-                cw.shadow[row_of(L, s0 + i, t0 + j) * pitch + m] = acc[i][j];
+                __builtin_nontemporal_store(acc[i][j], &cw.shadow[row_of(L, s0 + i, t0 + j) * pitch + m]);
 }
 
 // Edge splits, C_2 and the gates for the cells a + b = q of every block
@@ -1075,7 +1076,7 @@ __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &c
     // table) and the C_2 operand (the lane's own budget when C_2 is out of
     // reach)
     const bool packed_partial = P::kShadow && middle_packed(cw, (k_hi - k_lo) / kT + 1, k_hi - k_lo);
-    const uint32_t key = packed_partial ? load32(cw.shadow + cell * pitch, m) : 0u;
+    const uint32_t key = packed_partial ? __builtin_nontemporal_load(cw.shadow + cell * pitch + m) : 0u;
     const int64_t stored64 = packed_partial ? 0 : load64(tab + cell * pitch, m);
     const int ri = m - (int)r.wabar[s - 1];
     const bool all_ok = m >= cw.gall[cell] && ri >= 0;
