@@ -168,7 +168,7 @@ ROTOR_API int32_t rotor_solve(const int64_t *d_params, int32_t n_chains, int32_t
  * bit; they differ in speed.
  *   ROTOR_SCHEDULE_BLOCKED   16 x 16 blocks of pairs: register-tiled min-plus
  *                            products for the splits that reach across
- *                            blocks, 31 short launches per block-diagonal for
+ *                            blocks, 30 short launches per block-diagonal for
  *                            the others; the fast order for large tables.
  *   ROTOR_SCHEDULE_DIAGONAL  one launch per t - s over all pairs (the
  *                            wavefront the recurrence allows), the splits of

@@ -48,9 +48,10 @@
 //   low     k in [s, 16(I+1) - 1]: Y is a cell of the same block further down;
 //   high    k in [16J + 1, t - 1]: X is a cell of the same block to the left.
 // The low and high ranges hold at most 30 splits per cell and are taken by
-// edge_kernel in 31 steps over the block's anti-diagonals a + b = q
+// edge_kernel in 30 steps over the block's anti-diagonals a + b = q = 1..30
 // (a = 16(I+1) - s low splits, b = t - 16J - 1 high splits), each step
-// reading only finished cells.  A small table is instead filled in the
+// reading only finished cells; the corner a + b = 0 has neither and is
+// finished by the middle kernels.  A small table is instead filled in the
 // streamed order: one launch per diagonal d over all its pairs (diag_kernel,
 // or diag_split_kernel with the splits of a pair spread over four waves).
 #include "rotor_internal.h"
@@ -778,9 +779,29 @@ __device__ inline void middle_update(typename P::Acc (&acc)[kSub][kSub], const t
             P::relax(acc[i][j], x[i], y[j], sp);
 }
 
+// The corner cell (16I + 16, 16J + 1) of a block (I, J) has no low or high
+// splits: its middle result, whose u_f prefix starts at its own s, is its
+// whole C_1.  The middle kernels finish it (gates, C_2, final stores), so the
+// edge rounds start at a + b = 1.
+template <class P>
+__device__ inline void finish_corner(const ChainRows &r, const ChainWork &cw, int L, int m, int64_t pitch, int s,
+                                     int t, typename P::Acc acc, int64_t *tab, int16_t *dtab)
+{
+    const int64_t cell = row_of(L, s, t);
+    const int ri = m - (int)r.wabar[s - 1];
+    const bool all_ok = m >= cw.gall[cell] && ri >= 0;
+    const int64_t below = row_of(L, s + 1, t) * pitch;
+    const typename P::Raw c2 = P::load(tab + below, cw.shadow + below, all_ok ? ri : m);
+    if (m < cw.gnone[cell])
+        P::init(acc);
+    if (all_ok)
+        P::relax_all(acc, c2, (uint64_t)(r.uf[s - 1] + r.ub[s - 1]));
+    store_cell<P>(tab, dtab, cw.shadow, cell * pitch + m, acc);
+}
+
 template <class P>
 __device__ inline void middle_body(const ChainRows &r, const ChainWork &cw, int L, int M, int m, int64_t pitch,
-                                   int s0, int t0, int nt, int k_lo, int k_hi, int64_t *tab)
+                                   int s0, int t0, int nt, int k_lo, int k_hi, int64_t *tab, int16_t *dtab)
 {
     MiddleTile<P> tl;
 #pragma unroll
@@ -826,17 +847,22 @@ __device__ inline void middle_body(const ChainRows &r, const ChainWork &cw, int 
     }
     if (m > M)
         return;
+    // the wave whose last row is 16I + 16 and first column 16J + 1 holds the corner
+    const bool corner = s0 + kSub - 1 == k_lo && t0 == k_hi + 1;
 #pragma unroll
     for (int i = 0; i < kSub; ++i)
 #pragma unroll
-        for (int j = 0; j < kSub; ++j)
-            if (j < nt)
+        for (int j = 0; j < kSub; ++j) {
+            if (i == kSub - 1 && j == 0 && corner)
+                finish_corner<P>(r, cw, L, m, pitch, k_lo, k_hi + 1, acc[i][j], tab, dtab);
+            else if (j < nt)
                 tab[row_of(L, s0 + i, t0 + j) * pitch + m] = P::stored(acc[i][j]);
+        }
 }
 
 __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__ params, int L, int M,
                                                      int64_t pitch, int64_t rows, int delta,
-                                                     int64_t *__restrict__ cost, Work w)
+                                                     int64_t *__restrict__ cost, int16_t *__restrict__ dec, Work w)
 {
     const int c = blockIdx.z;
     const int I = blockIdx.y;
@@ -851,14 +877,15 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
     const ChainRows r = chain_rows(params, L, c);
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
+    int16_t *dtab = dec + (int64_t)c * rows * pitch;
     const int k_lo = (I + 1) * kT;
     const int k_hi = J * kT;
     if (middle_packed(cw, delta, k_hi - k_lo))
         return;  // middle_packed_kernel takes this block-diagonal
     if (cw.narrow(delta))
-        middle_body<Narrow>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, tab);
+        middle_body<Narrow>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, tab, dtab);
     else
-        middle_body<Wide>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, tab);
+        middle_body<Wide>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, tab, dtab);
 }
 
 // Packed middle products (same blocks, workgroups and register tiles as
@@ -937,7 +964,9 @@ __device__ __forceinline__ void ring_wait(int later)
 }
 
 __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__restrict__ params, int L, int M,
-                                                            int64_t pitch, int64_t rows, int delta, Work w)
+                                                            int64_t pitch, int64_t rows, int delta,
+                                                            int64_t *__restrict__ cost, int16_t *__restrict__ dec,
+                                                            Work w)
 {
     __shared__ uint32_t ring[kRing * kStage * kSplitWords];
     const Tile tile = xcd_tile();
@@ -1051,13 +1080,27 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
         return;
     // the partial stays a packed key, in the cell's compact copy, which
     // edge_kernel reads once and then overwrites with the final value; used
-    // once, it is stored and loaded non-temporally
+    // once, it is stored and loaded non-temporally.  The corner cell is
+    // finished here.
+    const bool corner = s0 + kSub - 1 == k_lo && t0 == k_hi + 1;
 #pragma unroll
     for (int i = 0; i < kSub; ++i)
 #pragma unroll
-        for (int j = 0; j < kSub; ++j)
-            if (j < nt)
+        for (int j = 0; j < kSub; ++j) {
+            if (i == kSub - 1 && j == 0 && corner) {
+                const uint32_t key = acc[i][j];
+                Narrow::Acc a;
+                Narrow::init(a);
+                if (key != kInf32) {
+                    a.val = key >> S;
+                    a.sp = (uint32_t)(k_lo + 1) + (key & ((1u << S) - 1u));
+                }
+                finish_corner<Narrow>(r, cw, L, m, pitch, k_lo, k_hi + 1, a, cost + (int64_t)c * rows * pitch,
+                                      dec + (int64_t)c * rows * pitch);
+            } else if (j < nt) {
                 __builtin_nontemporal_store(acc[i][j], &cw.shadow[row_of(L, s0 + i, t0 + j) * pitch + m]);
+            }
+        }
 }
 
 // Edge splits, C_2 and the gates for the cells a + b = q of every block
@@ -1258,16 +1301,18 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
             return e;
         // each chain is taken by one of the two kernels, the other returns at once
         middle_packed_kernel<<<dim3(mb64, nb - delta, tb.n_chains), 256, 0, stream>>>(
-            tb.params, L, tb.M, tb.pitch, tb.rows, delta, w);
-        if ((e = launched(kMiddle, pairs * (uint64_t)((delta - 1) * kT + 1), 0, 0)) != hipSuccess)
+            tb.params, L, tb.M, tb.pitch, tb.rows, delta, tb.cost, tb.dec, w);
+        // the middle splits of every pair, and C_2 of the corner cell of every block
+        const uint64_t corners = (uint64_t)(nb - delta);
+        if ((e = launched(kMiddle, pairs * (uint64_t)((delta - 1) * kT + 1), corners, corners)) != hipSuccess)
             return e;
         if ((e = before(kMiddle)) != hipSuccess)
             return e;
         middle_kernel<<<dim3(mb64, nb - delta, tb.n_chains), 256, 0, stream>>>(tb.params, L, tb.M, tb.pitch,
-                                                                               tb.rows, delta, tb.cost, w);
+                                                                               tb.rows, delta, tb.cost, tb.dec, w);
         if ((e = launched(kMiddle, 0, 0, 0)) != hipSuccess)
             return e;
-        for (int q = 0; q <= 2 * kT - 2; ++q) {
+        for (int q = 1; q <= 2 * kT - 2; ++q) {
             const int a_min = q - (kT - 1) > 0 ? q - (kT - 1) : 0;
             const int a_max = q < kT - 1 ? q : kT - 1;
             const int n_q = a_max - a_min + 1;
