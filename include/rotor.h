@@ -193,7 +193,7 @@ ROTOR_API int32_t rotor_solve_schedule(const int64_t *d_params, int32_t n_chains
 #define ROTOR_KERNEL_DIAG 1   /* pairs inside one 16-stage diagonal block, all splits */
 #define ROTOR_KERNEL_MIDDLE 2 /* split points whose operands lie in finished blocks */
 #define ROTOR_KERNEL_EDGE 3   /* remaining split points, C_2, gates, final cells */
-#define ROTOR_KERNEL_PREP 4   /* gates, prefix sums and value path of every chain */
+#define ROTOR_KERNEL_PREP 4   /* gates, prefix sums, value path of every block-diagonal */
 #define ROTOR_N_KERNEL_CLASSES 5
 
 typedef struct {
