@@ -2,6 +2,9 @@
 costs (ties between splits and between C_1 and C_2), zero sizes and
 overheads, sizes beyond the budget, heavy overheads, and costs scaled onto
 the 64-bit value path; batches of one to three chains; both fill orders.
+Longer chains (8 to 13 blocks of 16 stages) at costs scaled by up to 2^18
+put their block-diagonals on every side of the value-path thresholds (2-byte
+copy of the diagonal blocks, packed middle keys, 4-byte or 64-bit values).
 Every cell of both tables must equal the oracle's."""
 import numpy as np
 import pytest
@@ -50,3 +53,29 @@ def test_fuzz_parity(seed, schedule):
     _, cost, dec = solve_on_gpu(p, M, schedule=schedule)
     for c in range(n):
         assert_same(p, M, cost, dec, c)
+
+
+def long_case(seed):
+    rng = chaingen.SplitMix64(0xB10C + seed)
+    L = rng.uniform(120, 200)
+    M = rng.uniform(40, 260)
+    # from every block-diagonal narrow with the 2-byte copy (0), past the
+    # copy's limit (1, 2), to every block-diagonal on the 64-bit path (18)
+    shift = (0, 1, 2, 3, 5, 7, 9, 11, 13, 15, 16, 18)[seed]
+    p = np.zeros((1, 6, L), dtype=np.int64)
+    for l in range(L):
+        uf = rng.uniform(1, 100)
+        ub = max(1, 2 * uf + rng.uniform(-5, 5))
+        wa = rng.uniform(1, 12)
+        p[0, :, l] = (uf << shift, ub << shift, wa, wa * rng.uniform(1, 4), rng.uniform(0, 3), rng.uniform(0, 3))
+    return p, M, shift
+
+
+@pytest.mark.parametrize("schedule", SCHEDULES)
+@pytest.mark.parametrize("seed", range(12))
+def test_fuzz_long_chains(seed, schedule):
+    p, M, shift = long_case(seed)
+    L = p.shape[-1]
+    say(f"fuzz long seed={seed} L={L} M={M} shift={shift} {schedule}")
+    _, cost, dec = solve_on_gpu(p, M, schedule=schedule)
+    assert_same(p, M, cost, dec)
