@@ -801,7 +801,8 @@ __device__ inline void finish_corner(const ChainRows &r, const ChainWork &cw, in
 
 template <class P>
 __device__ inline void middle_body(const ChainRows &r, const ChainWork &cw, int L, int M, int m, int64_t pitch,
-                                   int s0, int t0, int nt, int k_lo, int k_hi, int64_t *tab, int16_t *dtab)
+                                   int s0, int t0, int nt, int k_lo, int k_hi, int finish, int64_t *tab,
+                                   int16_t *dtab)
 {
     MiddleTile<P> tl;
 #pragma unroll
@@ -847,8 +848,9 @@ __device__ inline void middle_body(const ChainRows &r, const ChainWork &cw, int 
     }
     if (m > M)
         return;
-    // the wave whose last row is 16I + 16 and first column 16J + 1 holds the corner
-    const bool corner = s0 + kSub - 1 == k_lo && t0 == k_hi + 1;
+    // the wave whose last row is 16I + 16 and first column 16J + 1 holds the
+    // corner (finished here unless the edge round a + b = 0 runs)
+    const bool corner = finish && s0 + kSub - 1 == k_lo && t0 == k_hi + 1;
 #pragma unroll
     for (int i = 0; i < kSub; ++i)
 #pragma unroll
@@ -861,7 +863,7 @@ __device__ inline void middle_body(const ChainRows &r, const ChainWork &cw, int 
 }
 
 __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__ params, int L, int M,
-                                                     int64_t pitch, int64_t rows, int delta,
+                                                     int64_t pitch, int64_t rows, int delta, int finish,
                                                      int64_t *__restrict__ cost, int16_t *__restrict__ dec, Work w)
 {
     const int c = blockIdx.z;
@@ -883,9 +885,9 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
     if (middle_packed(cw, delta, k_hi - k_lo))
         return;  // middle_packed_kernel takes this block-diagonal
     if (cw.narrow(delta))
-        middle_body<Narrow>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, tab, dtab);
+        middle_body<Narrow>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, finish, tab, dtab);
     else
-        middle_body<Wide>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, tab, dtab);
+        middle_body<Wide>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, finish, tab, dtab);
 }
 
 // Packed middle products (same blocks, workgroups and register tiles as
@@ -963,8 +965,34 @@ __device__ __forceinline__ void ring_wait(int later)
     }
 }
 
+// The partial slots of the cells of every block of block-diagonal delta, set
+// to infinity before a cut middle range merges into them (packed chains).
+__global__ __launch_bounds__(256) void fill_partials_kernel(int L, int M, int64_t pitch, int64_t rows, int delta,
+                                                            Work w)
+{
+    const int c = blockIdx.z;
+    const int I = blockIdx.y / (kT * kT);
+    const int cell = blockIdx.y - I * (kT * kT);
+    const int s = I * kT + 1 + cell / kT;
+    const int t = (I + delta) * kT + 1 + cell % kT;
+    const int m = blockIdx.x * 256 + threadIdx.x;
+    if (t > L || m > M)
+        return;
+    const ChainWork cw = chain_work(w, L, rows, pitch, c);
+    if (!middle_packed(cw, delta, (delta - 1) * kT))
+        return;
+    cw.shadow[row_of(L, s, t) * pitch + m] = kInf32;
+}
+
+// With n_part > 1 (block-diagonals of few blocks, whose launches would leave
+// most CUs idle), the middle split range of a block is cut into n_part runs
+// taken by different workgroups (x = part * chunks + chunk).  Their keys
+// share S and the offset base k_lo, so the unsigned minimum over the runs
+// is the minimum over the whole range, ties included: each run merges its
+// keys with an atomic minimum into the partial slots, which fill_partials
+// has set to infinity, and the corners are left to the edge round a + b = 0.
 __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__restrict__ params, int L, int M,
-                                                            int64_t pitch, int64_t rows, int delta,
+                                                            int64_t pitch, int64_t rows, int delta, int n_part,
                                                             int64_t *__restrict__ cost, int16_t *__restrict__ dec,
                                                             Work w)
 {
@@ -975,12 +1003,20 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     const int J = I + delta;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
-    const int m = tile.x * 64 + lane;
+    const int chunks = gridDim.x / n_part;
+    const int part = tile.x / chunks;
+    const int m = (tile.x - part * chunks) * 64 + lane;
     const int k_lo = (I + 1) * kT;
     const int k_hi = J * kT;
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     // uniform over the workgroup: every wave returns or none does
     if (!middle_packed(cw, delta, k_hi - k_lo))
+        return;
+    // this workgroup's run of middle splits [ka, kb]
+    const int run = (k_hi - k_lo + n_part) / n_part;
+    const int ka = k_lo + part * run;
+    const int kb = min(k_hi, ka + run - 1);
+    if (ka > kb)
         return;
     const int s0 = I * kT + (wave >> 1) * kSub + 1;
     const int t0 = J * kT + (wave & 1) * kSub + 1;
@@ -988,7 +1024,7 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     const int S = k_hi > k_lo ? 32 - __clz(k_hi - k_lo) : 0;
     const ChainRows r = chain_rows(params, L, c);
     const int mc = m <= M ? m : M;
-    const int n_stages = (k_hi - k_lo + kStage) / kStage;
+    const int n_stages = (kb - ka + kStage) / kStage;
 
     // rows this wave copies: waves 0, 1 the X rows (s, k) of s = 16I+1+8w ..,
     // waves 2, 3 the Y rows (k+1, t) of t = 16J+1+8(w-2) .. (past L: row L)
@@ -997,13 +1033,13 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     const char *src[kDmaPerSplit];  // each copied row at the next split to copy
 #pragma unroll
     for (int i = 0; i < kDmaPerSplit; ++i)
-        src[i] = (const char *)(cw.shadow + (copies_x ? row_of(L, first + i, k_lo) * pitch
-                                                      : row_of(L, k_lo + 1, min(first + i, L)) * pitch));
+        src[i] = (const char *)(cw.shadow + (copies_x ? row_of(L, first + i, ka) * pitch
+                                                      : row_of(L, ka + 1, min(first + i, L)) * pitch));
     const int64_t row_bytes = pitch * 4;
-    int k_copy = k_lo;  // next split to copy
+    int k_copy = ka;  // next split to copy
     uint32_t *const dst0 = ring + (copies_x ? wave * kSub : kT + (wave - 2) * kSub) * 64;
     int fill = 0;  // ring stage filled next
-    // copies of one stage; splits past k_hi copy split k_hi again, so every
+    // copies of one stage; splits past kb copy split kb again, so every
     // stage issues the same number of copies
     auto issue = [&]() {
         uint32_t *dst = dst0 + fill * (kStage * kSplitWords);
@@ -1016,7 +1052,7 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
             for (int i = 0; i < kDmaPerSplit; ++i)
                 __builtin_amdgcn_global_load_lds((global_void *)(src[i] + off),
                                                  (lds_void *)(dst + p * kSplitWords + i * 64), 4, 0, 0);
-            if (k < k_hi) {
+            if (k < kb) {
                 // to split k + 1: X rows advance one row, Y rows L - k - 1 rows
                 const int64_t step = copies_x ? row_bytes : (int64_t)(L - k - 1) * row_bytes;
 #pragma unroll
@@ -1039,11 +1075,12 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     for (int st = 0; st < kRing - 1; ++st)
         if (st < n_stages)
             issue();
-    uint32_t prefix = 0;  // sum of u_f from k_lo to k, at most V
+    // sum of u_f from k_lo to k, at most V
+    uint32_t prefix = (uint32_t)(cw.pre[ka - 1] - cw.pre[k_lo - 1]);
     const uint32_t *const x_lds0 = ring + (wave >> 1) * kSub * 64 + lane;
     const uint32_t *const y_lds0 = ring + (kT + (wave & 1) * kSub) * 64 + lane;
     int read = 0;  // ring stage read next
-    int k = k_lo;
+    int k = ka;
     for (int it = 0; it < n_stages; ++it) {
         // this wave's copies of stage it have landed, and so (after the
         // barrier) have every wave's; the stage refilled below was read by
@@ -1057,8 +1094,8 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
         uint32_t x[kStage][kSub], y[kStage][kSub];
 #pragma unroll
         for (int p = 0; p < kStage; ++p, ++k) {
-            const bool real = k <= k_hi;
-            const int ri = mc - (int)r.wa[(real ? k : k_hi) - 1];
+            const bool real = k <= kb;
+            const int ri = mc - (int)r.wa[(real ? k : kb) - 1];
             prefix += real ? (uint32_t)r.uf[k - 1] : 0u;
             const uint32_t add = real && ri >= 0 ? (prefix << S) | (uint32_t)(k - k_lo) : kInf32;
 #pragma unroll
@@ -1081,7 +1118,16 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     // the partial stays a packed key, in the cell's compact copy, which
     // edge_kernel reads once and then overwrites with the final value; used
     // once, it is stored and loaded non-temporally.  The corner cell is
-    // finished here.
+    // finished here when the range is not cut.
+    if (n_part > 1) {
+#pragma unroll
+        for (int i = 0; i < kSub; ++i)
+#pragma unroll
+            for (int j = 0; j < kSub; ++j)
+                if (j < nt)
+                    atomicMin(&cw.shadow[row_of(L, s0 + i, t0 + j) * pitch + m], acc[i][j]);
+        return;
+    }
     const bool corner = s0 + kSub - 1 == k_lo && t0 == k_hi + 1;
 #pragma unroll
     for (int i = 0; i < kSub; ++i)
@@ -1297,22 +1343,37 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
         uint64_t pairs = 0;
         for (int I = 0; I + delta < nb; ++I)
             pairs += (uint64_t)kT * (uint64_t)min(kT, L - (I + delta) * kT);
+        // A block-diagonal of few blocks cuts the packed middle ranges into
+        // runs for more workgroups (about 512), each of 32 splits or more;
+        // the corners then go to the edge round a + b = 0.
+        const unsigned wgs = mb64 * (unsigned)(nb - delta) * (unsigned)tb.n_chains;
+        const int span = (delta - 1) * kT + 1;
+        int n_part = 1;
+        if (wgs < 256)
+            n_part = max(1, min((int)((512 + wgs - 1) / wgs), span / 32));
+        const int finish = n_part == 1 ? 1 : 0;
         if ((e = before(kMiddle)) != hipSuccess)
             return e;
+        if (n_part > 1) {
+            fill_partials_kernel<<<dim3(mb256, (nb - delta) * kT * kT, tb.n_chains), 256, 0, stream>>>(
+                L, tb.M, tb.pitch, tb.rows, delta, w);
+            if ((e = launched(kMiddle, 0, 0, 0)) != hipSuccess)
+                return e;
+        }
         // each chain is taken by one of the two kernels, the other returns at once
-        middle_packed_kernel<<<dim3(mb64, nb - delta, tb.n_chains), 256, 0, stream>>>(
-            tb.params, L, tb.M, tb.pitch, tb.rows, delta, tb.cost, tb.dec, w);
+        middle_packed_kernel<<<dim3(mb64 * n_part, nb - delta, tb.n_chains), 256, 0, stream>>>(
+            tb.params, L, tb.M, tb.pitch, tb.rows, delta, n_part, tb.cost, tb.dec, w);
         // the middle splits of every pair, and C_2 of the corner cell of every block
-        const uint64_t corners = (uint64_t)(nb - delta);
-        if ((e = launched(kMiddle, pairs * (uint64_t)((delta - 1) * kT + 1), corners, corners)) != hipSuccess)
+        const uint64_t corners = finish ? (uint64_t)(nb - delta) : 0;
+        if ((e = launched(kMiddle, pairs * (uint64_t)span, corners, corners)) != hipSuccess)
             return e;
         if ((e = before(kMiddle)) != hipSuccess)
             return e;
-        middle_kernel<<<dim3(mb64, nb - delta, tb.n_chains), 256, 0, stream>>>(tb.params, L, tb.M, tb.pitch,
-                                                                               tb.rows, delta, tb.cost, tb.dec, w);
+        middle_kernel<<<dim3(mb64, nb - delta, tb.n_chains), 256, 0, stream>>>(
+            tb.params, L, tb.M, tb.pitch, tb.rows, delta, finish, tb.cost, tb.dec, w);
         if ((e = launched(kMiddle, 0, 0, 0)) != hipSuccess)
             return e;
-        for (int q = 1; q <= 2 * kT - 2; ++q) {
+        for (int q = finish; q <= 2 * kT - 2; ++q) {
             const int a_min = q - (kT - 1) > 0 ? q - (kT - 1) : 0;
             const int a_max = q < kT - 1 ? q : kT - 1;
             const int n_q = a_max - a_min + 1;
