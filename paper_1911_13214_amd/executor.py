@@ -230,6 +230,14 @@ def validate(L=24, seed=1, width=1024, batch=4096, slots=500, n_budgets=10, repe
     stages, dims = synthetic_chain(L, seed, width=width, device=dev)
     x = torch.randn(batch, dims[0], device=dev)
     dy = torch.randn(batch, dims[-1], device=dev)
+    # a few passes of the whole chain first, so that the estimate does not
+    # time a GPU still raising its clocks (the first work of a process)
+    for _ in range(3):
+        run_sequence(stages, x, dy, store_all_sequence(L))
+    _sync(dev)
+    for f in stages:
+        for q in f.parameters():
+            q.grad = None
     p = estimate(stages, x)
     ref = None
     plan = rotor.plan(p, slots=slots, n_budgets=n_budgets)
