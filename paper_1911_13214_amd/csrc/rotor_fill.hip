@@ -801,17 +801,17 @@ __device__ inline void finish_corner(const ChainRows &r, const ChainWork &cw, in
 
 template <class P>
 __device__ inline void middle_body(const ChainRows &r, const ChainWork &cw, int L, int M, int m, int64_t pitch,
-                                   int s0, int t0, int nt, int k_lo, int k_hi, int finish, int64_t *tab,
-                                   int16_t *dtab)
+                                   int s0, int t0, int nt, int k_lo, int k_hi, int ka, int kb, int n_part,
+                                   int64_t *tab, int16_t *dtab)
 {
     MiddleTile<P> tl;
 #pragma unroll
     for (int i = 0; i < kSub; ++i)
-        tl.xrow[i] = row_of(L, s0 + i, k_lo) * pitch;
+        tl.xrow[i] = row_of(L, s0 + i, ka) * pitch;
 #pragma unroll
     for (int j = 0; j < kSub; ++j)
         tl.ystep[j] = (int64_t)(j < nt ? j : nt - 1) * pitch;  // columns past L read the last one
-    tl.yrow = row_of(L, k_lo + 1, t0) * pitch;
+    tl.yrow = row_of(L, ka + 1, t0) * pitch;
     tl.tab = tab;
     tl.shadow = cw.shadow;
     tl.mc = m <= M ? m : M;
@@ -823,18 +823,18 @@ __device__ inline void middle_body(const ChainRows &r, const ChainWork &cw, int 
         for (int j = 0; j < kSub; ++j)
             P::init(acc[i][j]);
 
-    uint64_t prefix = 0;
+    uint64_t prefix = (uint64_t)(cw.pre[ka - 1] - cw.pre[k_lo - 1]);  // u_f from k_lo on
     typename P::Raw ax[kSub], ay[kSub], bx[kSub], by[kSub];
-    int k = k_lo;
+    int k = ka;
     int ra = tl.mc - (int)r.wa[k - 1];
     tl.load(ra, ax, ay);
-    for (; k + 1 <= k_hi; k += 2) {
+    for (; k + 1 <= kb; k += 2) {
         tl.advance(L, k, pitch);
         const int rb = tl.mc - (int)r.wa[k];
         tl.load(rb, bx, by);
         prefix += (uint64_t)r.uf[k - 1];
         middle_update<P>(acc, ax, ay, prefix, (uint32_t)(k + 1), ra >= 0);
-        if (k + 2 <= k_hi) {
+        if (k + 2 <= kb) {
             tl.advance(L, k + 1, pitch);
             ra = tl.mc - (int)r.wa[k + 1];
             tl.load(ra, ax, ay);
@@ -842,15 +842,27 @@ __device__ inline void middle_body(const ChainRows &r, const ChainWork &cw, int 
         prefix += (uint64_t)r.uf[k];
         middle_update<P>(acc, bx, by, prefix, (uint32_t)(k + 2), rb >= 0);
     }
-    if (k == k_hi) {
+    if (k == kb) {
         prefix += (uint64_t)r.uf[k - 1];
         middle_update<P>(acc, ax, ay, prefix, (uint32_t)(k + 1), ra >= 0);
     }
     if (m > M)
         return;
+    if (n_part > 1) {
+        // a run of a cut range: the stored forms (value << 32) | s' and
+        // (value << 16) | s' order by value, then split, as unsigned words
+#pragma unroll
+        for (int i = 0; i < kSub; ++i)
+#pragma unroll
+            for (int j = 0; j < kSub; ++j)
+                if (j < nt)
+                    atomicMin((unsigned long long *)&tab[row_of(L, s0 + i, t0 + j) * pitch + m],
+                              (unsigned long long)P::stored(acc[i][j]));
+        return;
+    }
     // the wave whose last row is 16I + 16 and first column 16J + 1 holds the
-    // corner (finished here unless the edge round a + b = 0 runs)
-    const bool corner = finish && s0 + kSub - 1 == k_lo && t0 == k_hi + 1;
+    // corner
+    const bool corner = s0 + kSub - 1 == k_lo && t0 == k_hi + 1;
 #pragma unroll
     for (int i = 0; i < kSub; ++i)
 #pragma unroll
@@ -863,14 +875,16 @@ __device__ inline void middle_body(const ChainRows &r, const ChainWork &cw, int 
 }
 
 __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__ params, int L, int M,
-                                                     int64_t pitch, int64_t rows, int delta, int finish,
+                                                     int64_t pitch, int64_t rows, int delta, int n_part,
                                                      int64_t *__restrict__ cost, int16_t *__restrict__ dec, Work w)
 {
     const int c = blockIdx.z;
     const int I = blockIdx.y;
     const int J = I + delta;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int m = blockIdx.x * 64 + (threadIdx.x & 63);
+    const int chunks = gridDim.x / n_part;
+    const int part = blockIdx.x / chunks;
+    const int m = (blockIdx.x - part * chunks) * 64 + (threadIdx.x & 63);
     const int s0 = I * kT + (wave >> 1) * kSub + 1;
     const int t0 = J * kT + (wave & 1) * kSub + 1;
     if (t0 > L)
@@ -884,10 +898,16 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
     const int k_hi = J * kT;
     if (middle_packed(cw, delta, k_hi - k_lo))
         return;  // middle_packed_kernel takes this block-diagonal
+    // this workgroup's run of middle splits, as in middle_packed_kernel
+    const int run = (k_hi - k_lo + n_part) / n_part;
+    const int ka = k_lo + part * run;
+    const int kb = min(k_hi, ka + run - 1);
+    if (ka > kb)
+        return;
     if (cw.narrow(delta))
-        middle_body<Narrow>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, finish, tab, dtab);
+        middle_body<Narrow>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, ka, kb, n_part, tab, dtab);
     else
-        middle_body<Wide>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, finish, tab, dtab);
+        middle_body<Wide>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, ka, kb, n_part, tab, dtab);
 }
 
 // Packed middle products (same blocks, workgroups and register tiles as
@@ -966,9 +986,10 @@ __device__ __forceinline__ void ring_wait(int later)
 }
 
 // The partial slots of the cells of every block of block-diagonal delta, set
-// to infinity before a cut middle range merges into them (packed chains).
+// to infinity before a cut middle range merges into them: the packed key in
+// the compact copy, or the stored form in the cost table.
 __global__ __launch_bounds__(256) void fill_partials_kernel(int L, int M, int64_t pitch, int64_t rows, int delta,
-                                                            Work w)
+                                                            int64_t *__restrict__ cost, Work w)
 {
     const int c = blockIdx.z;
     const int I = blockIdx.y / (kT * kT);
@@ -979,9 +1000,10 @@ __global__ __launch_bounds__(256) void fill_partials_kernel(int L, int M, int64_
     if (t > L || m > M)
         return;
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
-    if (!middle_packed(cw, delta, (delta - 1) * kT))
-        return;
-    cw.shadow[row_of(L, s, t) * pitch + m] = kInf32;
+    if (middle_packed(cw, delta, (delta - 1) * kT))
+        cw.shadow[row_of(L, s, t) * pitch + m] = kInf32;
+    else
+        cost[((int64_t)c * rows + row_of(L, s, t)) * pitch + m] = -1;  // all ones: above every stored form
 }
 
 // With n_part > 1 (block-diagonals of few blocks, whose launches would leave
@@ -1343,9 +1365,9 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
         uint64_t pairs = 0;
         for (int I = 0; I + delta < nb; ++I)
             pairs += (uint64_t)kT * (uint64_t)min(kT, L - (I + delta) * kT);
-        // A block-diagonal of few blocks cuts the packed middle ranges into
-        // runs for more workgroups (about 512), each of 32 splits or more;
-        // the corners then go to the edge round a + b = 0.
+        // A block-diagonal of few blocks cuts the middle ranges into runs for
+        // more workgroups (about 512), each of 32 splits or more; the corners
+        // then go to the edge round a + b = 0.
         const unsigned wgs = mb64 * (unsigned)(nb - delta) * (unsigned)tb.n_chains;
         const int span = (delta - 1) * kT + 1;
         int n_part = 1;
@@ -1356,7 +1378,7 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
             return e;
         if (n_part > 1) {
             fill_partials_kernel<<<dim3(mb256, (nb - delta) * kT * kT, tb.n_chains), 256, 0, stream>>>(
-                L, tb.M, tb.pitch, tb.rows, delta, w);
+                L, tb.M, tb.pitch, tb.rows, delta, tb.cost, w);
             if ((e = launched(kMiddle, 0, 0, 0)) != hipSuccess)
                 return e;
         }
@@ -1369,8 +1391,8 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
             return e;
         if ((e = before(kMiddle)) != hipSuccess)
             return e;
-        middle_kernel<<<dim3(mb64, nb - delta, tb.n_chains), 256, 0, stream>>>(
-            tb.params, L, tb.M, tb.pitch, tb.rows, delta, finish, tb.cost, tb.dec, w);
+        middle_kernel<<<dim3(mb64 * n_part, nb - delta, tb.n_chains), 256, 0, stream>>>(
+            tb.params, L, tb.M, tb.pitch, tb.rows, delta, n_part, tb.cost, tb.dec, w);
         if ((e = launched(kMiddle, 0, 0, 0)) != hipSuccess)
             return e;
         for (int q = finish; q <= 2 * kT - 2; ++q) {
