@@ -35,6 +35,10 @@
 //    place with its high word clamped to 2^30, so INT64_MAX lands just above
 //    2^62 and a sum of two keys never wraps.
 // C_2 is given the split field 0xFFFF (above every split), so C_1 wins ties.
+// When V_0 <= 2^15 - 2, the cells of the diagonal blocks are also kept in a
+// 2-byte copy (infinity -1), which a sign-extending load turns back into the
+// 4-byte form: the pairs inside a block and the edge splits read their
+// diagonal-block operands from it.
 //
 // Schedule.  The triangle of pairs is cut into 16 x 16 blocks (I, J) of stage
 // ranges S_I x S_J.  Diagonal blocks (I, I) are filled diagonal by diagonal
