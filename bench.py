@@ -147,6 +147,10 @@ def main():
                     help="before timing, run one plain device-to-device copy of this many MiB so that a "
                          "counter run can scale FETCH_SIZE / WRITE_SIZE by a kernel of known traffic")
     args = ap.parse_args()
+    if args.steps < 1 or args.warmup < 0:
+        ap.error("--steps must be at least 1 and --warmup at least 0")
+    if args.profile_steps < 1:
+        ap.error("--profile-steps must be at least 1: the roofline is priced on the kernel times it measures")
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the solver has no multi-GPU path (a batch of chains would "
               "shard by chain, a single chain over its budget range)", file=sys.stderr)

@@ -60,3 +60,10 @@ def test_more_than_one_gpu_is_refused_with_a_message():
     assert r.returncode == 2
     assert r.stdout == ""
     assert "one GPU" in r.stderr
+
+
+@pytest.mark.parametrize("args", [["--profile-steps", "0"], ["--steps", "0"], ["--warmup", "-1"]])
+def test_bad_counts_are_refused_before_any_device_work(args):
+    r = subprocess.run([sys.executable, bench.__file__, *args], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 2 and r.stdout == ""
+    assert "must be at least" in r.stderr
