@@ -27,7 +27,9 @@
 //    fits below 2^32 - 1 for the S bits of the block's middle split range):
 //    a candidate is one uint32 key (value << S) | (s' - first middle split),
 //    so one saturating add and one unsigned min relax it, ties going to the
-//    smaller split;
+//    smaller split.  When the range needs more bits than V_D leaves, but at
+//    least 7, it is relaxed in runs of 2^S splits, each with its own first
+//    split, and the runs' results are merged as (value << 32) | s';
 //  - wide, otherwise: operands are the int64 cells and a candidate is one
 //    64-bit key (value << 16) | s', so one unsigned min keeps the smallest
 //    value and, among equal values, the smallest split.  Finite values are
@@ -47,8 +49,8 @@
 //   middle  k in [16(I+1), 16J]: X in blocks (I, K) and Y in blocks (K, J)
 //           of smaller D -- all finished, the same range for every cell of
 //           the block: a register-tiled min-plus product (middle_packed_kernel,
-//           operands staged in LDS, or middle_kernel for chains outside the
-//           packed keys);
+//           operands staged in LDS, for packed keys and runs of them, or
+//           middle_kernel for the others);
 //   low     k in [s, 16(I+1) - 1]: Y is a cell of the same block further down;
 //   high    k in [16J + 1, t - 1]: X is a cell of the same block to the left.
 // The low and high ranges hold at most 30 splits per cell and are taken by
@@ -94,6 +96,7 @@ __device__ inline ChainRows chain_rows(const int64_t *__restrict__ params, int L
 
 typedef const __attribute__((address_space(1))) int64_t *global_c64;
 typedef const __attribute__((address_space(1))) uint32_t *global_c32;
+typedef __attribute__((address_space(1))) uint64_t *global_u64;
 
 // Load budget m of a table row: global address space, 32-bit byte offset
 // (M < 2^28).
@@ -727,6 +730,16 @@ __device__ inline bool middle_packed(const ChainWork &cw, int D, int span)
     return cw.narrow(D) && S <= cw.pbits[D];
 }
 
+// A narrow block-diagonal whose middle range is too wide for one packed key
+// takes packed runs of 2^pbits[D] splits instead (middle_packed_kernel), if
+// runs are 128 splits or more; each run's result goes to the cost table as
+// (value << 32) | s', the form middle_kernel stores.
+constexpr int kMinRunBits = 7;
+__device__ inline bool middle_runs(const ChainWork &cw, int D, int span)
+{
+    return cw.narrow(D) && !middle_packed(cw, D, span) && cw.pbits[D] >= kMinRunBits;
+}
+
 // Middle splits of every block (I, I + D) of one block-diagonal.  A workgroup
 // is one block at 64 budgets; its four waves hold the four 8 x 8 quarters of
 // the block, one accumulator per pair and lane.  For each middle split k the
@@ -900,7 +913,7 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
     const int k_lo = (I + 1) * kT;
     const int k_hi = J * kT;
-    if (middle_packed(cw, delta, k_hi - k_lo))
+    if (middle_packed(cw, delta, k_hi - k_lo) || middle_runs(cw, delta, k_hi - k_lo))
         return;  // middle_packed_kernel takes this block-diagonal
     // this workgroup's run of middle splits, as in middle_packed_kernel
     const int run = (k_hi - k_lo + n_part) / n_part;
@@ -1036,9 +1049,10 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     const int k_hi = J * kT;
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     // uniform over the workgroup: every wave returns or none does
-    if (!middle_packed(cw, delta, k_hi - k_lo))
+    const bool full = middle_packed(cw, delta, k_hi - k_lo);
+    if (!full && !middle_runs(cw, delta, k_hi - k_lo))
         return;
-    // this workgroup's run of middle splits [ka, kb]
+    // this workgroup's part of the middle splits [ka, kb]
     const int run = (k_hi - k_lo + n_part) / n_part;
     const int ka = k_lo + part * run;
     const int kb = min(k_hi, ka + run - 1);
@@ -1047,7 +1061,9 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     const int s0 = I * kT + (wave >> 1) * kSub + 1;
     const int t0 = J * kT + (wave & 1) * kSub + 1;
     const int nt = t0 <= L ? min(kSub, L - t0 + 1) : 0;
-    const int S = k_hi > k_lo ? 32 - __clz(k_hi - k_lo) : 0;
+    // key split bits: the whole range's, or those of a run of 2^S splits
+    const int S = full ? (k_hi > k_lo ? 32 - __clz(k_hi - k_lo) : 0) : cw.pbits[delta];
+    const int R = full ? INT_MAX : 1 << S;  // splits per run, a multiple of kStage
     const ChainRows r = chain_rows(params, L, c);
     const int mc = m <= M ? m : M;
     const int n_stages = (kb - ka + kStage) / kStage;
@@ -1107,6 +1123,47 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     const uint32_t *const y_lds0 = ring + (kT + (wave & 1) * kSub) * 64 + lane;
     int read = 0;  // ring stage read next
     int k = ka;
+    int run_base = full ? k_lo : ka;  // split of key offset 0
+    // Runs: at the end of each, the keys become (value << 32) | s' in the
+    // cost table: a plain store for the first run when the workgroup owns its
+    // cells (n_part == 1), an atomic minimum otherwise (the slots then start
+    // at all ones).  The corner keeps its best form in registers when this
+    // kernel finishes it.
+    int64_t *const tab = cost + (int64_t)c * rows * pitch;
+    const bool corner = s0 + kSub - 1 == k_lo && t0 == k_hi + 1;
+    uint64_t corner_best = ~0ull;
+    bool first_flush = true;
+    auto flush = [&]() {
+        const uint32_t mask = (1u << S) - 1u;
+        // the lane's byte offset and the first row, opaque here so that the
+        // compiler builds the 64 cell addresses in this rare step rather
+        // than holding them in registers across the loop
+        uint32_t lane_off = (uint32_t)m * 8u;
+        asm volatile("" : "+v"(lane_off));
+        int64_t row = row_of(L, s0, t0);
+        asm volatile("" : "+s"(row));
+#pragma unroll
+        for (int i = 0; i < kSub; ++i, row += L - (s0 + i - 1))
+#pragma unroll
+            for (int j = 0; j < kSub; ++j) {
+                const uint32_t key = acc[i][j];
+                acc[i][j] = kInf32;
+                const uint64_t st = key == kInf32 ? (uint64_t)kInf32 << 32
+                                                  : ((uint64_t)(key >> S) << 32) |
+                                                        (uint32_t)(run_base + 1 + (int)(key & mask));
+                if (n_part == 1 && i == kSub - 1 && j == 0 && corner) {
+                    corner_best = st < corner_best ? st : corner_best;
+                } else if (j < nt && m <= M) {
+                    // a wave-uniform row base and the lane's 32-bit offset
+                    global_u64 slot = (global_u64)((char *)(tab + (row + j) * pitch) + lane_off);
+                    if (n_part == 1 && first_flush)
+                        *slot = st;
+                    else if (key != kInf32)
+                        __hip_atomic_fetch_min(slot, st, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+        first_flush = false;
+    };
     for (int it = 0; it < n_stages; ++it) {
         // this wave's copies of stage it have landed, and so (after the
         // barrier) have every wave's; the stage refilled below was read by
@@ -1123,7 +1180,7 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
             const bool real = k <= kb;
             const int ri = mc - (int)r.wa[(real ? k : kb) - 1];
             prefix += real ? (uint32_t)r.uf[k - 1] : 0u;
-            const uint32_t add = real && ri >= 0 ? (prefix << S) | (uint32_t)(k - k_lo) : kInf32;
+            const uint32_t add = real && ri >= 0 ? (prefix << S) | (uint32_t)(k - run_base) : kInf32;
 #pragma unroll
             for (int i = 0; i < kSub; ++i)
                 x[p][i] = sat_add(rot_left(x_lds[p * kSplitWords + i * 64], S), add);
@@ -1138,6 +1195,24 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
 #pragma unroll
                 for (int p = 0; p < kStage; ++p)
                     acc[i][j] = min(acc[i][j], sat_add(x[p][i], y[p][j]));
+        if (k - run_base == R) {
+            flush();
+            run_base = k;
+        }
+    }
+    if (!full) {
+        if (k > run_base)
+            flush();
+        if (n_part == 1 && corner && m <= M) {
+            Narrow::Acc a;
+            Narrow::init(a);
+            if (corner_best < ((uint64_t)kInf32 << 32)) {
+                a.val = (uint32_t)(corner_best >> 32);
+                a.sp = (uint32_t)corner_best;
+            }
+            finish_corner<Narrow>(r, cw, L, m, pitch, k_lo, k_hi + 1, a, tab, dec + (int64_t)c * rows * pitch);
+        }
+        return;
     }
     if (m > M || nt == 0)
         return;
@@ -1154,7 +1229,6 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
                     atomicMin(&cw.shadow[row_of(L, s0 + i, t0 + j) * pitch + m], acc[i][j]);
         return;
     }
-    const bool corner = s0 + kSub - 1 == k_lo && t0 == k_hi + 1;
 #pragma unroll
     for (int i = 0; i < kSub; ++i)
 #pragma unroll
@@ -1167,8 +1241,7 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
                     a.val = key >> S;
                     a.sp = (uint32_t)(k_lo + 1) + (key & ((1u << S) - 1u));
                 }
-                finish_corner<Narrow>(r, cw, L, m, pitch, k_lo, k_hi + 1, a, cost + (int64_t)c * rows * pitch,
-                                      dec + (int64_t)c * rows * pitch);
+                finish_corner<Narrow>(r, cw, L, m, pitch, k_lo, k_hi + 1, a, tab, dec + (int64_t)c * rows * pitch);
             } else if (j < nt) {
                 __builtin_nontemporal_store(acc[i][j], &cw.shadow[row_of(L, s0 + i, t0 + j) * pitch + m]);
             }

@@ -71,12 +71,11 @@ def test_parity_batch_256_chains(schedule):
     assert hc == str(g["hash_cost"]) and hd == str(g["hash_dec"])
 
 
-@pytest.mark.parametrize("schedule", SCHEDULES)
-def test_parity_large_chain(schedule):
-    params, L, M, _, name = chaingen.config(5)
-    say(f"parity {name} {schedule}")
-    g = np.load(os.path.join(GOLDEN, "random_L500_M5000.npz"))
-    _, cost, dec = solve_on_gpu(params, M, schedule=schedule)
+def check_large_chain(params, M, cost, dec, g):
+    """The stored records of a large chain: top row, seeded cells, three
+    36-stage windows solved by the oracle now (C(s,t,.) depends on stages
+    s..t only), and the hashes of both whole tables."""
+    L = params.shape[2]
     order = gpu_rows_in_oracle_order(L)
     top = order[orc.row(L, 1, L)]
     np.testing.assert_array_equal(cost[0, top, :M + 1].cpu().numpy(), g["top_cost"])
@@ -87,9 +86,7 @@ def test_parity_large_chain(schedule):
     gd = dec[0].cpu().numpy()
     np.testing.assert_array_equal(gc[rows, cells[:, 2]], g["cell_cost"])
     np.testing.assert_array_equal(gd[rows, cells[:, 2]], g["cell_dec"])
-    # windows of the chain, solved by the oracle now: C(s,t,.) depends on
-    # stages s..t only
-    for a, b in [(1, 36), (233, 268), (465, 500)]:
+    for a, b in [(1, 36), (233, 268), (L - 35, L)]:
         sub = np.ascontiguousarray(params[:, :, a - 1:b])
         C, D = orc.solve(sub, M)
         Ls = b - a + 1
@@ -103,6 +100,33 @@ def test_parity_large_chain(schedule):
     hc, hd = canonical_hashes(cost, dec, L, M)
     assert hc == str(g["hash_cost"]), "whole cost table hash"
     assert hd == str(g["hash_dec"]), "whole decision table hash"
+
+
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_parity_large_chain(schedule):
+    params, L, M, _, name = chaingen.config(5)
+    say(f"parity {name} {schedule}")
+    g = np.load(os.path.join(GOLDEN, "random_L500_M5000.npz"))
+    _, cost, dec = solve_on_gpu(params, M, schedule=schedule)
+    check_large_chain(params, M, cost, dec, g)
+
+
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_parity_large_chain_costs_x8(schedule):
+    # The large chain with u_f and u_b times 8: its block-diagonals take
+    # whole packed keys, runs of 128 splits (several per range, one
+    # workgroup holding the whole range and finishing the corner cell) and
+    # (value, split) pairs.
+    params, L, M, _, name = chaingen.config(5)
+    g = np.load(os.path.join(GOLDEN, "random_L500_M5000_x8.npz"))
+    params[:, :2] <<= int(g["cost_shift"])
+    modes = middle_modes(params[0], L, M, 1)
+    kinds = {m if isinstance(m, str) else m[0] for m in modes.values()}
+    assert kinds == {"packed", "runs", "pairs"}
+    assert any(m[0] == "runs" and m[2] == 1 and m[3] > 2 << m[1] for m in modes.values() if m != "pairs")
+    say(f"parity {name} costs x 8 {schedule}")
+    _, cost, dec = solve_on_gpu(params, M, schedule=schedule)
+    check_large_chain(params, M, cost, dec, g)
 
 
 @pytest.mark.parametrize("L,M,seed", [(1, 0, 1), (1, 37, 2), (2, 15, 3), (3, 16, 4), (5, 1, 9), (17, 255, 5),
@@ -406,6 +430,49 @@ def test_packed_keys_per_block_diagonal(seed, shift):
     assert any(span_bits[D] == key_bits(vd[D]) for D in packed)
     assert any(span_bits[D] == key_bits(vd[D]) + 1 for D in vd)
     say(f"packed per block-diagonal seed={seed} shift={shift} bound={v} packed={sorted(packed)}")
+    _, cost, dec = solve_on_gpu(p, M, schedule="blocked")
+    assert_same(p, M, cost, dec)
+
+
+def middle_modes(p, L, M, n_chains):
+    """How the blocked fill relaxes the middle splits of each block-diagonal
+    D >= 1 of one chain: ("packed", parts) when its whole range fits a packed
+    key, ("runs", S, parts, splits per part) when runs of 2^S splits do (S >=
+    7), "pairs" or "wide" otherwise.  A range is cut into parts when its
+    launch has fewer than 256 workgroups of 64 budgets."""
+    nb = (L + 15) // 16
+    vd = block_diagonal_bounds(p, L)
+    out = {}
+    for D in range(1, nb):
+        n = 16 * (D - 1)  # last split minus first
+        if vd[D] >= 1 << 30:
+            out[D] = "wide"
+            continue
+        wgs = (M + 64) // 64 * (nb - D) * n_chains
+        parts = max(1, min(-(-512 // wgs), (n + 1) // 32)) if wgs < 256 else 1
+        S = key_bits(vd[D])
+        if n.bit_length() <= S:
+            out[D] = ("packed", parts)
+        elif S >= 7:
+            out[D] = ("runs", S, parts, (n + parts) // parts)
+        else:
+            out[D] = "pairs"
+    return out
+
+
+@pytest.mark.parametrize("L,M,seed,shift", [(200, 240, 8, 5), (240, 200, 7, 4), (256, 300, 9, 4)])
+def test_packed_runs_per_block_diagonal(L, M, seed, shift):
+    # Block-diagonals whose bound leaves a packed key 7 bits or more, but
+    # fewer than their split range needs, relax the range in runs of 2^S
+    # splits and merge the runs' (value, split) results in the cost table by
+    # atomic minima.  At these sizes their ranges are cut into parts of one
+    # run each; the large chain with costs x 8 (stored hashes) has whole
+    # ranges of several runs.
+    p = scaled_chain(seed, L, shift)
+    modes = middle_modes(p[0], L, M, 1)
+    runs = {D: m for D, m in modes.items() if m[0] == "runs"}
+    assert runs and all(m[2] > 1 for m in runs.values())
+    say(f"packed runs L={L} M={M} seed={seed} shift={shift} {sorted(runs.items())}")
     _, cost, dec = solve_on_gpu(p, M, schedule="blocked")
     assert_same(p, M, cost, dec)
 
