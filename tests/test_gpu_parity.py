@@ -535,6 +535,22 @@ def test_batch_mixing_value_paths(schedule):
         assert_same(params, M, cost, dec, c)
 
 
+def test_batch_mixing_middle_paths():
+    # One blocked fill whose chains take different middle paths in the same
+    # launches: packed keys and packed runs, packed keys only, packed keys
+    # with (value, split) pairs and 64-bit keys, 64-bit keys only.
+    L, M = 200, 240
+    shifts = (5, 0, 12, 22)
+    p = np.concatenate([scaled_chain(30 + i, L, sh) for i, sh in enumerate(shifts)])
+    kinds = [{m if isinstance(m, str) else m[0] for m in middle_modes(p[c], L, M, len(shifts)).values()}
+             for c in range(len(shifts))]
+    assert kinds == [{"packed", "runs"}, {"packed"}, {"packed", "pairs", "wide"}, {"wide"}]
+    say(f"batch mixing middle paths L={L} M={M} {kinds}")
+    _, cost, dec = solve_on_gpu(p, M, schedule="blocked")
+    for c in range(len(shifts)):
+        assert_same(p, M, cost, dec, c)
+
+
 @pytest.mark.parametrize("L,M", [(5, (1 << 28) - 1), (20, (1 << 24) + 3)])
 def test_largest_budgets(L, M):
     # M at the domain's limit: C(s, t, m) depends only on budgets up to m, and
