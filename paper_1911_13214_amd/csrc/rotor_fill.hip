@@ -915,10 +915,10 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
     const int k_hi = J * kT;
     if (middle_packed(cw, delta, k_hi - k_lo) || middle_runs(cw, delta, k_hi - k_lo))
         return;  // middle_packed_kernel takes this block-diagonal
-    // this workgroup's run of middle splits, as in middle_packed_kernel
-    const int run = (k_hi - k_lo + n_part) / n_part;
-    const int ka = k_lo + part * run;
-    const int kb = min(k_hi, ka + run - 1);
+    // this workgroup's part of the middle splits, as in middle_packed_kernel
+    const int part_len = (k_hi - k_lo + n_part) / n_part;
+    const int ka = k_lo + part * part_len;
+    const int kb = min(k_hi, ka + part_len - 1);
     if (ka > kb)
         return;
     if (cw.narrow(delta))
@@ -1053,9 +1053,9 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     if (!full && !middle_runs(cw, delta, k_hi - k_lo))
         return;
     // this workgroup's part of the middle splits [ka, kb]
-    const int run = (k_hi - k_lo + n_part) / n_part;
-    const int ka = k_lo + part * run;
-    const int kb = min(k_hi, ka + run - 1);
+    const int part_len = (k_hi - k_lo + n_part) / n_part;
+    const int ka = k_lo + part * part_len;
+    const int kb = min(k_hi, ka + part_len - 1);
     if (ka > kb)
         return;
     const int s0 = I * kT + (wave >> 1) * kSub + 1;
