@@ -68,7 +68,13 @@ namespace {
 constexpr int64_t kInf = INT64_MAX;
 constexpr int kT = 16;   // block side, in stages
 constexpr int kSub = 8;  // per-wave register tile side
-constexpr int kEdgeThreads = 128;  // budgets per edge workgroup (measured best of 64..512)
+// An edge workgroup is one wave holding kEdgeBudgets budgets per lane, 64
+// apart: 128 consecutive budgets, whose loads it issues together (measured on
+// MI355X at L = 500, M = 5000, against one budget per lane in 128-thread
+// workgroups: edges 13.70 -> 13.24 ms; 128-thread workgroups of two budgets
+// per lane 13.53 ms, three or four budgets per lane 14.0-14.4 ms).
+constexpr int kEdgeThreads = 64;
+constexpr int kEdgeBudgets = 2;
 // The automatic schedule fills small tables diagonal by diagonal: measured on
 // MI355X, that is faster up to about 2e9 split candidates for one chain
 // (L = 250 at M = 500) and 4e8 for a batch, whose blocked launches are wider,
@@ -519,6 +525,69 @@ __device__ __forceinline__ void relax_run(typename P::Acc &acc, const ChainRows 
     RelaxRun<P, kT - 1>::go(n, acc, r, m, k0, cur, prefix);
 }
 
+// relax_fixed for NB budgets m[0..NB) of one lane: the loads of every split
+// and budget are issued first.
+template <class P, int N, int NB>
+__device__ __forceinline__ void relax_fixed_nb(typename P::Acc (&acc)[NB], const ChainRows &r, const int (&m)[NB],
+                                               int k0, RowCursor &cur, uint64_t &prefix)
+{
+    typename P::Raw rx[N][NB], ry[N][NB];
+    int wa[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        wa[i] = (int)r.wa[k0 + i - 1];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const int ri = m[b] - wa[i];
+            rx[i][b] = P::load_at(cur.x, m[b]);
+            ry[i][b] = P::load_at(cur.y, ri >= 0 ? ri : m[b]);
+        }
+        cur.x += cur.row_bytes;
+        cur.y += cur.ystep;
+        cur.ystep -= cur.row_bytes;
+    }
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const int k = k0 + i;
+        prefix += (uint64_t)r.uf[k - 1];
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+            P::relax(acc[b], P::xop(rx[i][b], prefix, (uint32_t)(k + 1), m[b] >= wa[i]), P::yop(ry[i][b]),
+                     (uint32_t)(k + 1));
+    }
+}
+
+template <class P, int N, int NB>
+struct RelaxRunNB {
+    __device__ __forceinline__ static void go(int n, typename P::Acc (&acc)[NB], const ChainRows &r,
+                                              const int (&m)[NB], int k0, RowCursor &cur, uint64_t &prefix)
+    {
+        if (n == N)
+            relax_fixed_nb<P, N, NB>(acc, r, m, k0, cur, prefix);
+        else
+            RelaxRunNB<P, N - 1, NB>::go(n, acc, r, m, k0, cur, prefix);
+    }
+};
+template <class P, int NB>
+struct RelaxRunNB<P, 0, NB> {
+    __device__ __forceinline__ static void go(int, typename P::Acc (&)[NB], const ChainRows &, const int (&)[NB], int,
+                                              RowCursor &, uint64_t &)
+    {
+    }
+};
+
+// n <= kT - 1 splits from k0 for NB budgets, in straight-line runs of up to
+// 8 splits: longer runs of 4-byte operands would hold more registers than the
+// runs from the 2-byte copy (101 against 78 VGPRs for the edge kernel).
+template <class P, int NB>
+__device__ __forceinline__ void relax_run_nb(typename P::Acc (&acc)[NB], const ChainRows &r, const int (&m)[NB],
+                                             int k0, int n, RowCursor &cur, uint64_t &prefix)
+{
+    constexpr int kRun = 8;
+    for (; n > 0; n -= kRun, k0 += kRun)
+        RelaxRunNB<P, kRun, NB>::go(n < kRun ? n : kRun, acc, r, m, k0, cur, prefix);
+}
+
 // Operand loads of the narrow path from the compact copy (4 bytes) or from
 // the 2-byte copy of the diagonal blocks (a sign-extending load: finite
 // values there are below 2^15, and the infinity 0xFFFF becomes 0xFFFFFFFF).
@@ -584,6 +653,57 @@ template <class XL, class YL>
 struct MixedRun<XL, YL, 0> {
     __device__ __forceinline__ static void go(int, Narrow::Acc &, const ChainRows &, int, int, MixedCursor &,
                                               uint64_t &)
+    {
+    }
+};
+
+// relax_mixed for NB budgets m[0..NB) of one lane: the loads of every split
+// and budget are issued first.
+template <class XL, class YL, int N, int NB>
+__device__ __forceinline__ void relax_mixed_nb(Narrow::Acc (&acc)[NB], const ChainRows &r, const int (&m)[NB],
+                                               int k0, MixedCursor &cur, uint64_t &prefix)
+{
+    uint32_t rx[N][NB], ry[N][NB];
+    int wa[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        wa[i] = (int)r.wa[k0 + i - 1];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const int ri = m[b] - wa[i];
+            rx[i][b] = XL::at(cur.x, m[b]);
+            // a budget shifted below 0 reads the lane's own budget (in bounds)
+            ry[i][b] = YL::at(cur.y, ri >= 0 ? ri : m[b]);
+        }
+        cur.x += cur.xstep;
+        cur.y += cur.ystep;
+        cur.ystep -= cur.ydec;
+    }
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const int k = k0 + i;
+        prefix += (uint64_t)r.uf[k - 1];
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+            Narrow::relax(acc[b], Narrow::xop(rx[i][b], prefix, 0, m[b] >= wa[i]), ry[i][b], (uint32_t)(k + 1));
+    }
+}
+
+template <class XL, class YL, int N, int NB>
+struct MixedRunNB {
+    __device__ __forceinline__ static void go(int n, Narrow::Acc (&acc)[NB], const ChainRows &r, const int (&m)[NB],
+                                              int k0, MixedCursor &cur, uint64_t &prefix)
+    {
+        if (n == N)
+            relax_mixed_nb<XL, YL, N, NB>(acc, r, m, k0, cur, prefix);
+        else
+            MixedRunNB<XL, YL, N - 1, NB>::go(n, acc, r, m, k0, cur, prefix);
+    }
+};
+template <class XL, class YL, int NB>
+struct MixedRunNB<XL, YL, 0, NB> {
+    __device__ __forceinline__ static void go(int, Narrow::Acc (&)[NB], const ChainRows &, const int (&)[NB], int,
+                                              MixedCursor &, uint64_t &)
     {
     }
 };
@@ -1255,23 +1375,41 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
 // in a diagonal block -- X of a low split, Y of a high one -- comes from the
 // 2-byte copy.
 template <class P, bool H>
-__device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &cw, int L, int m, int64_t pitch,
+__device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &cw, int L, int M, int m0, int64_t pitch,
                                           int s, int t, int k_lo, int k_hi, int64_t *tab, int16_t *dtab)
 {
+    constexpr int NB = kEdgeBudgets;
     const int64_t cell = row_of(L, s, t);
+    // the lane's budgets m0 + b * kEdgeThreads; those past M load budget M
+    // and store nothing
+    int m[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+        m[b] = min(m0 + b * kEdgeThreads, M);
     // loads that depend on nothing go first: the stored middle partial (a
     // packed key in the compact copy, or (value << 32) | s' in the cost
     // table) and the C_2 operand (the lane's own budget when C_2 is out of
     // reach)
     const bool packed_partial = P::kShadow && middle_packed(cw, (k_hi - k_lo) / kT + 1, k_hi - k_lo);
-    const uint32_t key = packed_partial ? __builtin_nontemporal_load(cw.shadow + cell * pitch + m) : 0u;
-    const int64_t stored64 = packed_partial ? 0 : load64(tab + cell * pitch, m);
-    const int ri = m - (int)r.wabar[s - 1];
-    const bool all_ok = m >= cw.gall[cell] && ri >= 0;
+    const int wab = (int)r.wabar[s - 1];
+    const int32_t gall = cw.gall[cell];
     const int64_t below = row_of(L, s + 1, t) * pitch;
-    const typename P::Raw c2 = P::load(tab + below, cw.shadow + below, all_ok ? ri : m);
-    typename P::Acc acc;
-    P::init(acc);
+    uint32_t key[NB];
+    int64_t stored64[NB];
+    typename P::Raw c2[NB];
+    bool all_ok[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        key[b] = packed_partial ? __builtin_nontemporal_load(cw.shadow + cell * pitch + m[b]) : 0u;
+        stored64[b] = packed_partial ? 0 : load64(tab + cell * pitch, m[b]);
+        const int ri = m[b] - wab;
+        all_ok[b] = m[b] >= gall && ri >= 0;
+        c2[b] = P::load(tab + below, cw.shadow + below, all_ok[b] ? ri : m[b]);
+    }
+    typename P::Acc acc[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+        P::init(acc[b]);
     // low splits k = s .. k_lo - 1: X from block (I, I), Y from this block
     uint64_t prefix = 0;
     const int64_t rb = pitch * 4, hb = cw.hpitch * 2;
@@ -1279,35 +1417,46 @@ __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &c
         // X rows (s, k) of the 2-byte copy are consecutive
         MixedCursor low{(const char *)cw.half_row(s, s), (const char *)(cw.shadow + row_of(L, s + 1, t) * pitch), hb,
                         (int64_t)(L - s - 1) * rb, rb};
-        MixedRun<Load16, Load32, kT - 1>::go(k_lo - s, acc, r, m, s, low, prefix);
+        MixedRunNB<Load16, Load32, kT - 1, NB>::go(k_lo - s, acc, r, m, s, low, prefix);
     } else {
         RowCursor low = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, s);
-        relax_run<P>(acc, r, m, s, k_lo - s, low, prefix);
+        relax_run_nb<P, NB>(acc, r, m, s, k_lo - s, low, prefix);
     }
     // middle splits: the stored partial counts u_f from k_lo on
-    int64_t stored = stored64;
-    if (packed_partial) {
-        const int S = k_hi > k_lo ? 32 - __clz(k_hi - k_lo) : 0;
-        const uint32_t split = (uint32_t)(k_lo + 1) + (key & ((1u << S) - 1u));
-        stored = key == kInf32 ? (int64_t)((uint64_t)kInf32 << 32) : (int64_t)(((uint64_t)(key >> S) << 32) | split);
+    const int S = k_hi > k_lo ? 32 - __clz(k_hi - k_lo) : 0;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        int64_t stored = stored64[b];
+        if (packed_partial) {
+            const uint32_t split = (uint32_t)(k_lo + 1) + (key[b] & ((1u << S) - 1u));
+            stored = key[b] == kInf32 ? (int64_t)((uint64_t)kInf32 << 32)
+                                      : (int64_t)(((uint64_t)(key[b] >> S) << 32) | split);
+        }
+        P::merge_stored(acc[b], stored, prefix);
     }
-    P::merge_stored(acc, stored, prefix);
     // high splits k = 16J + 1 .. t - 1: X from this block, Y from block (J, J)
     prefix += (uint64_t)(cw.pre[k_hi] - cw.pre[k_lo - 1]);
     if constexpr (H) {
         // Y rows (k + 1, t) of the 2-byte copy are 16 rows apart
         MixedCursor high{(const char *)(cw.shadow + row_of(L, s, k_hi + 1) * pitch),
                          (const char *)cw.half_row(k_hi + 2, t), rb, kT * hb, 0};
-        MixedRun<Load32, Load16, kT - 1>::go(t - k_hi - 1, acc, r, m, k_hi + 1, high, prefix);
+        MixedRunNB<Load32, Load16, kT - 1, NB>::go(t - k_hi - 1, acc, r, m, k_hi + 1, high, prefix);
     } else {
         RowCursor high = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, k_hi + 1);
-        relax_run<P>(acc, r, m, k_hi + 1, t - k_hi - 1, high, prefix);
+        relax_run_nb<P, NB>(acc, r, m, k_hi + 1, t - k_hi - 1, high, prefix);
     }
-    if (m < cw.gnone[cell])
-        P::init(acc);
-    if (all_ok)
-        P::relax_all(acc, c2, (uint64_t)(r.uf[s - 1] + r.ub[s - 1]));
-    store_cell<P>(tab, dtab, cw.shadow, cell * pitch + m, acc);
+    const int32_t gnone = cw.gnone[cell];
+    const uint64_t ufub = (uint64_t)(r.uf[s - 1] + r.ub[s - 1]);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        if (m[b] < gnone)
+            P::init(acc[b]);
+        if (all_ok[b])
+            P::relax_all(acc[b], c2[b], ufub);
+        const int mb = m0 + b * kEdgeThreads;
+        if (mb <= M)
+            store_cell<P>(tab, dtab, cw.shadow, cell * pitch + mb, acc[b]);
+    }
 }
 
 __global__ __launch_bounds__(kEdgeThreads) void edge_kernel(const int64_t *__restrict__ params, int L, int M,
@@ -1322,19 +1471,19 @@ __global__ __launch_bounds__(kEdgeThreads) void edge_kernel(const int64_t *__res
     const int J = I + delta;
     const int s = (I + 1) * kT - a;
     const int t = J * kT + 1 + (q - a);
-    const int m = blockIdx.x * kEdgeThreads + threadIdx.x;
-    if (t > L || m > M)
+    const int m0 = blockIdx.x * (kEdgeThreads * kEdgeBudgets) + threadIdx.x;
+    if (t > L || m0 > M)
         return;
     const ChainRows r = chain_rows(params, L, c);
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
     if (!cw.narrow(delta))
-        edge_body<Wide, false>(r, cw, L, m, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
+        edge_body<Wide, false>(r, cw, L, M, m0, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
     else if (cw.diag16())
-        edge_body<Narrow, true>(r, cw, L, m, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
+        edge_body<Narrow, true>(r, cw, L, M, m0, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
     else
-        edge_body<Narrow, false>(r, cw, L, m, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
+        edge_body<Narrow, false>(r, cw, L, M, m0, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
 }
 
 hipError_t check() { return hipGetLastError(); }
@@ -1393,7 +1542,7 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
     const uint64_t nc = (uint64_t)tb.n_chains;
     const unsigned mb256 = (unsigned)((tb.M + 1 + 255) / 256);
     const unsigned mb64 = (unsigned)((tb.M + 1 + 63) / 64);
-    const unsigned mb_edge = (unsigned)((tb.M + kEdgeThreads) / kEdgeThreads);
+    const unsigned mb_edge = (unsigned)((tb.M + kEdgeThreads * kEdgeBudgets) / (kEdgeThreads * kEdgeBudgets));
     auto launched = [&](KernelClass k, uint64_t c1, uint64_t c2, uint64_t cells) -> hipError_t {
         hipError_t e = check();
         if (e == hipSuccess && obs)
