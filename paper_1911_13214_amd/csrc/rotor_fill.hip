@@ -714,45 +714,67 @@ struct MixedRunNB<XL, YL, 0, NB> {
 // block, narrow path, ChainWork::diag16) every operand comes from the 2-byte
 // copy, where the rows (s'+1, t) are 16 rows apart.
 template <class P, bool H>
-__device__ __forceinline__ void diag_body(const ChainRows &r, const ChainWork &cw, int L, int m, int64_t pitch,
+__device__ __forceinline__ void diag_body(const ChainRows &r, const ChainWork &cw, int L, int M, int m0, int64_t pitch,
                                           int s, int t, int64_t *tab, int16_t *dtab)
 {
+    constexpr int NB = kEdgeBudgets;
     const int64_t cell = row_of(L, s, t);
+    // the lane's budgets m0 + b * kEdgeThreads; those past M load budget M
+    // and store nothing
+    int m[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+        m[b] = min(m0 + b * kEdgeThreads, M);
     // the C_2 operand first (the lane's own budget when it is out of reach)
-    const int ri = m - (int)r.wabar[s - 1];
-    const bool all_ok = m >= cw.gall[cell] && ri >= 0;
+    const int wab = (int)r.wabar[s - 1];
+    const int32_t gall = cw.gall[cell];
     const int64_t below = row_of(L, s + 1, t) * pitch;
-    typename P::Raw c2;
-    if constexpr (H)
-        c2 = Load16::at((const char *)cw.half_row(s + 1, t), all_ok ? ri : m);
-    else
-        c2 = P::load(tab + below, cw.shadow + below, all_ok ? ri : m);
-    typename P::Acc acc;
-    P::init(acc);
+    typename P::Raw c2[NB];
+    bool all_ok[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        const int ri = m[b] - wab;
+        all_ok[b] = m[b] >= gall && ri >= 0;
+        if constexpr (H)
+            c2[b] = Load16::at((const char *)cw.half_row(s + 1, t), all_ok[b] ? ri : m[b]);
+        else
+            c2[b] = P::load(tab + below, cw.shadow + below, all_ok[b] ? ri : m[b]);
+    }
+    typename P::Acc acc[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+        P::init(acc[b]);
     uint64_t prefix = 0;
     if constexpr (H) {
         const int64_t hb = cw.hpitch * 2;
         MixedCursor cur{(const char *)cw.half_row(s, s), (const char *)cw.half_row(s + 1, t), hb, kT * hb, 0};
-        MixedRun<Load16, Load16, kT - 1>::go(t - s, acc, r, m, s, cur, prefix);  // t - s <= 15
+        MixedRunNB<Load16, Load16, kT - 1, NB>::go(t - s, acc, r, m, s, cur, prefix);  // t - s <= 15
     } else {
         RowCursor cur = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, s);
-        for (int k0 = s; k0 < t; k0 += kT - 1)
-            relax_run<P>(acc, r, m, k0, min(kT - 1, t - k0), cur, prefix);
+        relax_run_nb<P, NB>(acc, r, m, s, t - s, cur, prefix);
     }
-    if (m < cw.gnone[cell])
-        P::init(acc);
-    if (all_ok)
-        P::relax_all(acc, c2, (uint64_t)(r.uf[s - 1] + r.ub[s - 1]));
-    store_cell<P>(tab, dtab, cw.shadow, cell * pitch + m, acc);
-    if constexpr (P::kShadow) {
-        if (cw.diag16() && block_diag(s, t) == 0)
-            cw.half_row(s, t)[m] = P::finite(acc) ? (int16_t)P::value(acc) : (int16_t)-1;
+    const int32_t gnone = cw.gnone[cell];
+    const uint64_t ufub = (uint64_t)(r.uf[s - 1] + r.ub[s - 1]);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        if (m[b] < gnone)
+            P::init(acc[b]);
+        if (all_ok[b])
+            P::relax_all(acc[b], c2[b], ufub);
+        const int mb = m0 + b * kEdgeThreads;
+        if (mb <= M) {
+            store_cell<P>(tab, dtab, cw.shadow, cell * pitch + mb, acc[b]);
+            if constexpr (P::kShadow) {
+                if (cw.diag16() && block_diag(s, t) == 0)
+                    cw.half_row(s, t)[mb] = P::finite(acc[b]) ? (int16_t)P::value(acc[b]) : (int16_t)-1;
+            }
+        }
     }
 }
 
 // The pairs (s, s + d): inside the 16 x 16 diagonal blocks only (blocked
 // fill), or all of them (streamed fill of a small table, one launch per d).
-__global__ __launch_bounds__(256) void diag_kernel(const int64_t *__restrict__ params, int L, int M,
+__global__ __launch_bounds__(kEdgeThreads) void diag_kernel(const int64_t *__restrict__ params, int L, int M,
                                                    int64_t pitch, int64_t rows, int d, int whole,
                                                    int64_t *__restrict__ cost, int16_t *__restrict__ dec, Work w)
 {
@@ -761,8 +783,8 @@ __global__ __launch_bounds__(256) void diag_kernel(const int64_t *__restrict__ p
     const int t = s + d;
     if (!whole && (s - 1) / kT != (t - 1) / kT)
         return;
-    const int m = blockIdx.x * 256 + threadIdx.x;
-    if (m > M)
+    const int m0 = blockIdx.x * (kEdgeThreads * kEdgeBudgets) + threadIdx.x;
+    if (m0 > M)
         return;
     const ChainRows r = chain_rows(params, L, c);
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
@@ -770,11 +792,11 @@ __global__ __launch_bounds__(256) void diag_kernel(const int64_t *__restrict__ p
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
     const int D = block_diag(s, t);
     if (!cw.narrow(D))
-        diag_body<Wide, false>(r, cw, L, m, pitch, s, t, tab, dtab);
+        diag_body<Wide, false>(r, cw, L, M, m0, pitch, s, t, tab, dtab);
     else if (D == 0 && cw.diag16())
-        diag_body<Narrow, true>(r, cw, L, m, pitch, s, t, tab, dtab);
+        diag_body<Narrow, true>(r, cw, L, M, m0, pitch, s, t, tab, dtab);
     else
-        diag_body<Narrow, false>(r, cw, L, m, pitch, s, t, tab, dtab);
+        diag_body<Narrow, false>(r, cw, L, M, m0, pitch, s, t, tab, dtab);
 }
 
 // Streamed order for the longer diagonals: the d splits of each pair are
@@ -1577,7 +1599,7 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
             diag_split_kernel<<<dim3(mb64, L - d, tb.n_chains), 256, 0, stream>>>(tb.params, L, tb.M, tb.pitch,
                                                                                   tb.rows, d, tb.cost, tb.dec, w);
         else
-            diag_kernel<<<dim3(mb256, L - d, tb.n_chains), 256, 0, stream>>>(tb.params, L, tb.M, tb.pitch, tb.rows,
+            diag_kernel<<<dim3(mb_edge, L - d, tb.n_chains), kEdgeThreads, 0, stream>>>(tb.params, L, tb.M, tb.pitch, tb.rows,
                                                                              d, streamed ? 1 : 0, tb.cost, tb.dec, w);
         const uint64_t pairs = streamed ? (uint64_t)(L - d) : in_block_pairs(L, d);
         if ((e = launched(kDiag, pairs * d, pairs, pairs)) != hipSuccess)
