@@ -129,6 +129,20 @@ def test_parity_large_chain_costs_x8(schedule):
     check_large_chain(params, M, cost, dec, g)
 
 
+@pytest.mark.parametrize("M", [62, 63, 64, 126, 127, 128, 191])
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_budget_counts_around_the_lane_layout(M, schedule):
+    # The edge and diagonal kernels give each lane two budgets 64 apart in
+    # workgroups of 128 budgets: budget counts M + 1 just below, at and above
+    # 64 and 128 leave the second budget of some lanes, or a whole second
+    # workgroup, with nothing or part to do.
+    L = 48
+    params = chaingen.random_chains(1, L, seed=100 + M)
+    say(f"lane layout L={L} M={M} {schedule}")
+    _, cost, dec = solve_on_gpu(params, M, schedule=schedule)
+    assert_same(params, M, cost, dec)
+
+
 @pytest.mark.parametrize("L,M,seed", [(1, 0, 1), (1, 37, 2), (2, 15, 3), (3, 16, 4), (5, 1, 9), (17, 255, 5),
                                       (33, 257, 6), (40, 1023, 7), (64, 300, 8)])
 @pytest.mark.parametrize("schedule", SCHEDULES)
