@@ -90,30 +90,39 @@ int64_t oracle_m_none(int L, const int64_t *p, int s, int t)
     return g;
 }
 
-/* Input domain shared with the GPU library: non-negative values, sizes and
- * overheads below 2^30, M below 2^28, and L * sum(u_f) + sum(u_b) below 2^44
- * (a bound on every finite cost: no stage is run forward more than L times in
- * a persistent schedule). */
+/* The oracle's own input domain: what its int64 arithmetic handles without
+ * overflow, whatever any other implementation supports.
+ *  - 1 <= L <= 32767 (decisions are int16) and 0 <= M < 2^31;
+ *  - every value >= 0;
+ *  - sizes and overheads below 2^60: a gate adds at most four of them;
+ *  - L * sum(u_f) + sum(u_b) below 2^62.  A C_1 or C_2 candidate of the pair
+ *    (s, t) is the time of a persistent schedule of [s, t] (Theorem 1), in
+ *    which no stage runs forward more than t - s + 1 <= L times, so every
+ *    candidate and every partial sum of one stays below 2^62 < INT64_MAX.
+ * Theorem 1 defines C for any non-negative integers; these limits only keep
+ * the arithmetic exact. */
 int oracle_check(int L, int64_t M, const int64_t *p)
 {
-    if (L < 1 || L > 32767 || M < 0 || M >= ((int64_t)1 << 28))
+    const uint64_t cost_bound = (uint64_t)1 << 62;
+    if (L < 1 || L > 32767 || M < 0 || M >= ((int64_t)1 << 31))
         return -1;
     orc_chain c = {L, M, p};
     uint64_t suf = 0, sub = 0;
     for (int l = 1; l <= L; ++l) {
-        if (uf(&c, l) < 0 || ub(&c, l) < 0 || uf(&c, l) >= ((int64_t)1 << 44) || ub(&c, l) >= ((int64_t)1 << 44))
+        if (uf(&c, l) < 0 || ub(&c, l) < 0 || (uint64_t)uf(&c, l) >= cost_bound ||
+            (uint64_t)ub(&c, l) >= cost_bound)
             return -1;
         int64_t s[4] = {wa(&c, l), wab(&c, l), of(&c, l), ob(&c, l)};
         for (int k = 0; k < 4; ++k)
-            if (s[k] < 0 || s[k] >= ((int64_t)1 << 30))
+            if (s[k] < 0 || s[k] >= ((int64_t)1 << 60))
                 return -1;
         suf += (uint64_t)uf(&c, l);
         sub += (uint64_t)ub(&c, l);
-        if (suf >= ((uint64_t)1 << 44) || sub >= ((uint64_t)1 << 44))
+        if (suf >= cost_bound || sub >= cost_bound)
             return -1;
     }
-    /* L * suf + sub < 2^44, written without overflow */
-    if (suf > (((uint64_t)1 << 44) - sub) / (uint64_t)L)
+    /* L * suf + sub < 2^62, written without overflow */
+    if (suf > (cost_bound - sub) / (uint64_t)L)
         return -1;
     return 0;
 }

@@ -276,15 +276,45 @@ def test_edge_cases():
 
 
 def test_domain_checks():
+    # the oracle's own domain: what its int64 arithmetic carries exactly
+    # (Theorem 1 defines C for any non-negative integers)
     p = chaingen.random_chains(1, 4, seed=1)
     assert orc.check(p, 100)
-    for row, val in [(0, -1), (2, -1), (3, 1 << 30), (5, -3)]:
+    for row, val in [(0, -1), (1, -1), (2, -1), (3, 1 << 60), (4, 1 << 60), (5, -3)]:
         q = p.copy()
         q[0, row, 1] = val
         assert not orc.check(q, 100)
+    for row in (2, 3, 4, 5):
+        q = p.copy()
+        q[0, row, 1] = (1 << 60) - 1
+        assert orc.check(q, 100)
     assert not orc.check(p, -1)
-    assert not orc.check(p, 1 << 28)
-    assert orc.check(p, (1 << 28) - 1)
+    assert not orc.check(p, 1 << 31)
+    assert orc.check(p, (1 << 31) - 1)
     q = p.copy()
-    q[0, 0, :] = 1 << 41  # L * sum(u_f) = 16 * 2^41, beyond 2^44
+    q[0, 0, :] = 1 << 59  # L * sum(u_f) = 16 * 2^59 = 2^63, beyond 2^62
     assert not orc.check(q, 100)
+    q[0, 0, :] = (1 << 57) - 1  # 16 * 4 * (2^57 - 1) + sum(u_b) < 2^62
+    assert orc.check(q, 100)
+    with pytest.raises(ValueError):
+        orc.solve(-np.ones((1, 6, 2), dtype=np.int64), 10)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_brute_force_beyond_the_library_domain(seed):
+    # times near 2^45 put L * sum(u_f) + sum(u_b) above the GPU library's
+    # limit of 2^44 (its packed keys), but well inside the oracle's 2^62: the
+    # oracle still equals brute force over every persistent schedule there,
+    # and the library refuses the same chain
+    L = 3 + seed
+    p = wide_chain(5000 + seed, L=L)
+    rng = np.random.default_rng(seed)
+    p[0, 0] += (1 << 45) + rng.integers(0, 1 << 20, L)
+    p[0, 1] += (1 << 45) + rng.integers(0, 1 << 20, L)
+    M = 120
+    assert orc.check(p, M)
+    from paper_1911_13214_amd import rotor
+    assert rotor.rotor_check_params(p, M) == rotor.ROTOR_EDOMAIN
+    _check_against_brute_force(p, M)
+    C, _ = orc.solve(p, M)
+    assert C[orc.row(L, 1, L), M] != INF and C[orc.row(L, 1, L), M] >= L << 46
