@@ -28,10 +28,15 @@
  *
  * Domain.  Every value is >= 0; sizes and overheads are < 2^30; M < 2^28;
  * for every chain L * sum(u_f) + sum(u_b) < 2^44 (this bounds every finite
- * cost: a persistent schedule runs each forward at most L times).
- * rotor_check_params verifies this on a host copy.  Kernels never access
- * memory out of bounds whatever the parameter values; outside the domain the
- * table contents are unspecified.
+ * cost: a persistent schedule runs each forward at most L times).  These are
+ * limits of this library's number formats, narrower than the problem itself.
+ * rotor_check_params verifies them on a host copy; rotor_solve also checks
+ * every chain on the device and records the result in its workspace, which
+ * rotor_solve_status reports, and rotor_reconstruct refuses a chain outside
+ * the domain.  The kernels read and write only within the caller's buffers
+ * whatever the parameter values (every shifted budget is checked to lie in
+ * [0, m] before it is read); outside the domain the table contents are
+ * unspecified.
  *
  * Budgets.  Column m = 0..M of the tables is the budget of the definition of
  * C_BP: the input a^{s-1} of the sub-chain is not counted, the gradient
@@ -137,11 +142,11 @@ ROTOR_API int64_t rotor_row_index(int32_t L, int32_t s, int32_t t);
 ROTOR_API int32_t rotor_check_params(const int64_t *h_params, int32_t n_chains, int32_t L, int64_t M);
 
 /* Bytes of device workspace rotor_solve needs for these sizes: per-pair
- * gates, prefix sums, a few words per block of 16 stages, a compact
- * 4-byte-per-cell copy of the cost table (about 40% of cost_bytes +
- * dec_bytes) and, for chains of more than 16 stages, a 2-byte copy of the
- * cells of the 16 x 16 diagonal blocks.  Host only.  Returns
- * ROTOR_OK or ROTOR_EINVAL (as rotor_layout). */
+ * gates, prefix sums, a few words per block of 16 stages, a domain status
+ * word per chain, a compact 4-byte-per-cell copy of the cost table (about
+ * 40% of cost_bytes + dec_bytes) and, for chains of more than 16 stages, a
+ * 2-byte copy of the cells of the 16 x 16 diagonal blocks.  Host only.
+ * Returns ROTOR_OK or ROTOR_EINVAL (as rotor_layout). */
 ROTOR_API int32_t rotor_workspace_bytes(int32_t n_chains, int32_t L, int64_t M, uint64_t *bytes);
 
 /* Fill the cost table C_BP(s, t, m) and the decision table for every chain,
@@ -163,6 +168,22 @@ ROTOR_API int32_t rotor_workspace_bytes(int32_t n_chains, int32_t L, int64_t M, 
  * share a workspace must not overlap. */
 ROTOR_API int32_t rotor_solve(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
                               int16_t *d_dec, void *d_work, uint64_t work_bytes, void *stream);
+
+/* Domain report of the solve that last used this workspace: waits for
+ * `stream` (the stream of that solve), then reads the status word the fill
+ * recorded for each chain.
+ *   d_work, work_bytes  DEVICE: the workspace given to rotor_solve (same
+ *                       n_chains, L, M).
+ *   h_chain_status      HOST, n_chains int32 written (may be NULL):
+ *                       ROTOR_OK, or ROTOR_EDOMAIN for a chain whose
+ *                       parameters are outside the domain (its tables are
+ *                       unspecified).
+ * Returns ROTOR_OK if every chain was in the domain, ROTOR_EDOMAIN if one
+ * was not, ROTOR_EINVAL for bad arguments or a workspace no solve has
+ * written, ROTOR_EDEVICE if the copy fails.  Synchronous; allocates no device
+ * memory. */
+ROTOR_API int32_t rotor_solve_status(const void *d_work, uint64_t work_bytes, int32_t n_chains, int32_t L, int64_t M,
+                                     int32_t *h_chain_status, void *stream);
 
 /* Fill orders of rotor_solve_schedule.  Both fill the same tables, bit for
  * bit; they differ in speed.
@@ -231,7 +252,9 @@ ROTOR_API int32_t rotor_solve_timed(const int64_t *d_params, int32_t n_chains, i
  *              ROTOR_ECAPACITY: the length needed; only cap ops are written).
  *   d_status   DEVICE, written: n_budgets int32, ROTOR_OK, ROTOR_INFEASIBLE
  *              (C(1, L, m) is infinite; count 0), ROTOR_ECAPACITY,
- *              ROTOR_EINVAL (budget out of range) or ROTOR_ECORRUPT.
+ *              ROTOR_EINVAL (budget out of range), ROTOR_EDOMAIN (the
+ *              chain's parameters are outside the domain; count 0) or
+ *              ROTOR_ECORRUPT.
  * Asynchronous.  Returns ROTOR_OK once enqueued, ROTOR_EINVAL for bad
  * arguments (including L > ROTOR_MAX_L_RECONSTRUCT), ROTOR_EDEVICE if the
  * launch fails.  Allocates nothing. */

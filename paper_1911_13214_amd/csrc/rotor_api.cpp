@@ -1,5 +1,6 @@
-// C ABI entry points of include/rotor.h: argument checks, table geometry and
-// the launches.  The arithmetic of the method lives in the kernels.
+// C ABI entry points of include/rotor.h that enqueue device work: argument
+// checks and the launches.  The arithmetic of the method lives in the
+// kernels; the host-only entry points are in rotor_host.cpp.
 #include <stdint.h>
 
 #include <vector>
@@ -9,25 +10,6 @@
 using namespace rotor;
 
 namespace {
-
-constexpr int64_t kMaxSize = (int64_t)1 << 30;
-constexpr int64_t kMaxBudget = (int64_t)1 << 28;
-constexpr uint64_t kCostBound = (uint64_t)1 << 44;
-
-bool sizes_ok(int32_t n_chains, int32_t L, int64_t M)
-{
-    return n_chains >= 1 && n_chains <= ROTOR_MAX_CHAINS && L >= 1 && L <= ROTOR_MAX_L && M >= 0 && M < kMaxBudget;
-}
-
-// Number of elements of one table, or 0 on overflow.
-uint64_t table_elems(int32_t n_chains, int32_t L, int64_t M)
-{
-    const unsigned __int128 e = (unsigned __int128)n_chains * (uint64_t)((int64_t)L * (L + 1) / 2) *
-                                (uint64_t)pitch_of(M);
-    if (e * 8 >= ((unsigned __int128)1 << 63))
-        return 0;
-    return (uint64_t)e;
-}
 
 bool solve_args_ok(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, const int64_t *d_cost,
                    const int16_t *d_dec, const void *d_work, uint64_t work_bytes)
@@ -131,86 +113,6 @@ struct TimingObserver : LaunchObserver {
 
 extern "C" {
 
-int32_t rotor_version(void) { return ROTOR_VERSION; }
-
-const char *rotor_status_string(int32_t status)
-{
-    switch (status) {
-    case ROTOR_OK: return "ok";
-    case ROTOR_EINVAL: return "invalid argument";
-    case ROTOR_EDOMAIN: return "chain parameter outside the supported domain";
-    case ROTOR_EDEVICE: return "HIP runtime error";
-    case ROTOR_INFEASIBLE: return "no sequence fits the memory budget";
-    case ROTOR_ECAPACITY: return "output array too small";
-    case ROTOR_ECORRUPT: return "decision table inconsistent";
-    case ROTOR_ESEQUENCE: return "operation sequence not valid";
-    default: return "unknown status";
-    }
-}
-
-int32_t rotor_layout(int32_t n_chains, int32_t L, int64_t M, int64_t *pitch, int64_t *rows_per_chain,
-                     uint64_t *cost_bytes, uint64_t *dec_bytes)
-{
-    if (!sizes_ok(n_chains, L, M))
-        return ROTOR_EINVAL;
-    const uint64_t e = table_elems(n_chains, L, M);
-    if (e == 0)
-        return ROTOR_EINVAL;
-    if (pitch)
-        *pitch = pitch_of(M);
-    if (rows_per_chain)
-        *rows_per_chain = (int64_t)L * (L + 1) / 2;
-    if (cost_bytes)
-        *cost_bytes = e * sizeof(int64_t);
-    if (dec_bytes)
-        *dec_bytes = e * sizeof(int16_t);
-    return ROTOR_OK;
-}
-
-int64_t rotor_row_index(int32_t L, int32_t s, int32_t t)
-{
-    if (L < 1 || L > ROTOR_MAX_L || s < 1 || t < s || t > L)
-        return -1;
-    return row_of(L, s, t);
-}
-
-int32_t rotor_check_params(const int64_t *h_params, int32_t n_chains, int32_t L, int64_t M)
-{
-    if (!h_params || !sizes_ok(n_chains, L, M))
-        return ROTOR_EINVAL;
-    for (int32_t c = 0; c < n_chains; ++c) {
-        const int64_t *p = h_params + (int64_t)c * ROTOR_N_ROWS * L;
-        uint64_t suf = 0, sub = 0;
-        for (int32_t l = 0; l < L; ++l) {
-            const int64_t uf = p[ROTOR_ROW_UF * L + l], ub = p[ROTOR_ROW_UB * L + l];
-            if (uf < 0 || ub < 0 || (uint64_t)uf >= kCostBound || (uint64_t)ub >= kCostBound)
-                return ROTOR_EDOMAIN;
-            for (int row = ROTOR_ROW_WA; row <= ROTOR_ROW_OB; ++row) {
-                const int64_t v = p[row * L + l];
-                if (v < 0 || v >= kMaxSize)
-                    return ROTOR_EDOMAIN;
-            }
-            suf += (uint64_t)uf;
-            sub += (uint64_t)ub;
-            if (suf >= kCostBound || sub >= kCostBound)
-                return ROTOR_EDOMAIN;
-        }
-        // L * suf + sub < 2^44
-        if (suf > (kCostBound - sub) / (uint64_t)L)
-            return ROTOR_EDOMAIN;
-    }
-    return ROTOR_OK;
-}
-
-int32_t rotor_workspace_bytes(int32_t n_chains, int32_t L, int64_t M, uint64_t *bytes)
-{
-    if (!sizes_ok(n_chains, L, M) || table_elems(n_chains, L, M) == 0)
-        return ROTOR_EINVAL;
-    if (bytes)
-        *bytes = work_layout(n_chains, L, pitch_of(M)).total;
-    return ROTOR_OK;
-}
-
 int32_t rotor_solve(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
                     int16_t *d_dec, void *d_work, uint64_t work_bytes, void *stream)
 {
@@ -244,6 +146,31 @@ int32_t rotor_solve_timed(const int64_t *d_params, int32_t n_chains, int32_t L, 
     hipError_t e = launch_fill(tb, w, ROTOR_SCHEDULE_AUTO, (hipStream_t)stream, &obs);
     const hipError_t f = obs.finish((hipStream_t)stream);
     return (e == hipSuccess && f == hipSuccess) ? ROTOR_OK : ROTOR_EDEVICE;
+}
+
+int32_t rotor_solve_status(const void *d_work, uint64_t work_bytes, int32_t n_chains, int32_t L, int64_t M,
+                           int32_t *h_chain_status, void *stream)
+{
+    if (!d_work || (uintptr_t)d_work % 8 || !sizes_ok(n_chains, L, M) || table_elems(n_chains, L, M) == 0)
+        return ROTOR_EINVAL;
+    const WorkLayout wl = work_layout(n_chains, L, pitch_of(M));
+    if (work_bytes < wl.total)
+        return ROTOR_EINVAL;
+    std::vector<int32_t> st(h_chain_status ? 0 : (size_t)n_chains);
+    int32_t *dst = h_chain_status ? h_chain_status : st.data();
+    const hipStream_t s = (hipStream_t)stream;
+    if (hipMemcpyAsync(dst, (const char *)d_work + wl.status, sizeof(int32_t) * (size_t)n_chains,
+                       hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+        return ROTOR_EDEVICE;
+    int32_t worst = ROTOR_OK;
+    for (int32_t c = 0; c < n_chains; ++c) {
+        if (dst[c] != ROTOR_OK && dst[c] != ROTOR_EDOMAIN)
+            return ROTOR_EINVAL;  // not a workspace a solve has written
+        if (dst[c] == ROTOR_EDOMAIN)
+            worst = ROTOR_EDOMAIN;
+    }
+    return worst;
 }
 
 int32_t rotor_reconstruct(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, const int16_t *d_dec,

@@ -66,7 +66,7 @@ namespace rotor {
 namespace {
 
 constexpr int64_t kInf = INT64_MAX;
-constexpr int kT = 16;   // block side, in stages
+constexpr int kT = kBlock;  // block side, in stages
 constexpr int kSub = 8;  // per-wave register tile side
 // An edge workgroup is one wave holding kEdgeBudgets budgets per lane, 64
 // apart: 128 consecutive budgets, whose loads it issues together (measured on
@@ -89,15 +89,40 @@ constexpr uint32_t kAllSplit = 0xFFFF;  // split field of a C_2 candidate
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
 constexpr uint64_t kNarrowBound = 1ull << 30;
 
-struct ChainRows {
-    const int64_t *uf, *ub, *wa, *wabar, *of, *ob;  // stage l at index l-1
+// The parameters of one chain as given (stage l at index l-1).
+struct ChainParams {
+    const int64_t *uf, *ub, *wa, *wabar, *of, *ob;
 };
 
-__device__ inline ChainRows chain_rows(const int64_t *__restrict__ params, int L, int c)
+__device__ inline ChainParams chain_params(const int64_t *__restrict__ params, int L, int c)
 {
     const int64_t *p = params + (int64_t)c * ROTOR_N_ROWS * L;
     return {p + ROTOR_ROW_UF * L, p + ROTOR_ROW_UB * L, p + ROTOR_ROW_WA * L,
             p + ROTOR_ROW_WABAR * L, p + ROTOR_ROW_OF * L, p + ROTOR_ROW_OB * L};
+}
+
+// What the fill kernels read of a chain: the times as given and the two
+// sizes that shift operand budgets, w_a and w_abar, as prep_kernel clamped
+// them into [0, M + 1] (stage l at index l-1).  In the domain the clamp
+// changes nothing the recurrence sees (a shift beyond M puts every operand
+// out of reach either way); outside it, every shifted budget m - w stays
+// within [m - M - 1, m], so an operand is only ever loaded at a budget in
+// [0, M], whatever the parameter values.
+// The sizes are read through the constant address space: written by an
+// earlier kernel and read-only during the fill, they then take scalar loads
+// like the parameters, which the compiler could not assume for a workspace
+// pointer the kernel also writes through.
+typedef const __attribute__((address_space(4))) int32_t *const_i32;
+struct ChainRows {
+    const int64_t *uf, *ub;
+    const_i32 wa, wabar;
+};
+
+__device__ inline ChainRows chain_rows(const int64_t *__restrict__ params, const Work &w, int L, int c)
+{
+    const int64_t *p = params + (int64_t)c * ROTOR_N_ROWS * L;
+    const_i32 sh = (const_i32)(w.shift + (int64_t)c * 2 * L);
+    return {p + ROTOR_ROW_UF * L, p + ROTOR_ROW_UB * L, sh, sh + L};
 }
 
 typedef const __attribute__((address_space(1))) int64_t *global_c64;
@@ -301,15 +326,25 @@ __device__ inline void store_cell(int64_t *cost, int16_t *dec, uint32_t *shadow,
 // delta^t stored), Section 4.2; delta has the size of a.  The maximum over
 // s < j < t in m_none is a running maximum along t: a wave prefix maximum
 // per step plus the carry of the steps before.  Gates above INT32_MAX are
-// clamped: any gate above M < 2^28 is never met.  The last workgroup of a
-// chain scans u_f with one wave and bounds the costs of each block-diagonal.
-__global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ params, int L, int64_t rows, Work w)
+// clamped: any gate above M < 2^28 is never met.  Workgroup s - 1 also
+// writes the shift sizes w_a^s and w_abar^s clamped into [0, M + 1] (see
+// ChainRows).  The last workgroup of a chain checks its parameters against
+// the domain, scans u_f with one wave and bounds the costs of each
+// block-diagonal.
+__global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ params, int L, int M, int64_t rows,
+                                                  Work w)
 {
     const int c = blockIdx.y;
     const int lane = threadIdx.x;
-    const ChainRows r = chain_rows(params, L, c);
+    const ChainParams r = chain_params(params, L, c);
     auto clamp32 = [](int64_t v) { return (int32_t)(v < INT32_MAX ? v : INT32_MAX); };
     if (blockIdx.x == gridDim.x - 1) {
+        // the chain's domain status, which rotor_solve_status reports: the
+        // fill stays in bounds outside the domain, but its tables are then
+        // unspecified
+        const bool in_domain = chain_in_domain(params + (int64_t)c * ROTOR_N_ROWS * L, L, lane);
+        if (lane == 0)
+            w.status[c] = in_domain ? ROTOR_OK : ROTOR_EDOMAIN;
         // lane l sums a segment of stages, then the segment sums are scanned
         const int seg = (L + 63) / 64;
         const int lo = min(L, lane * seg), hi = min(L, lo + seg);
@@ -398,6 +433,12 @@ __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ pa
         return;
     }
     const int s = blockIdx.x + 1;
+    if (lane == 0) {
+        auto clamp_shift = [&](int64_t v) { return (int32_t)(v < 0 ? 0 : v > (int64_t)M + 1 ? (int64_t)M + 1 : v); };
+        int32_t *sh = w.shift + (int64_t)c * 2 * L;
+        sh[s - 1] = clamp_shift(r.wa[s - 1]);
+        sh[L + s - 1] = clamp_shift(r.wabar[s - 1]);
+    }
     int32_t *gn = w.gnone + (int64_t)c * rows;
     int32_t *ga = w.gall + (int64_t)c * rows;
     const int64_t first = r.wa[s - 1] + r.of[s - 1];
@@ -434,7 +475,7 @@ __global__ __launch_bounds__(256) void leaf_kernel(const int64_t *__restrict__ p
     const int m = blockIdx.x * 256 + threadIdx.x;
     if (m > M)
         return;
-    const ChainRows r = chain_rows(params, L, c);
+    const ChainRows r = chain_rows(params, w, L, c);
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     const int64_t row = row_of(L, s, s);
     const bool ok = m >= cw.gall[row];
@@ -480,7 +521,7 @@ __device__ __forceinline__ void relax_fixed(typename P::Acc &acc, const ChainRow
     int ri[N];
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-        ri[i] = m - (int)r.wa[k0 + i - 1];
+        ri[i] = m - r.wa[k0 + i - 1];
         rx[i] = P::load_at(cur.x, m);
         // a budget shifted below 0 reads the lane's own budget (in bounds);
         // xop discards the candidate
@@ -535,7 +576,7 @@ __device__ __forceinline__ void relax_fixed_nb(typename P::Acc (&acc)[NB], const
     int wa[N];
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-        wa[i] = (int)r.wa[k0 + i - 1];
+        wa[i] = r.wa[k0 + i - 1];
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
             const int ri = m[b] - wa[i];
@@ -622,7 +663,7 @@ __device__ __forceinline__ void relax_mixed(Narrow::Acc &acc, const ChainRows &r
     int ri[N];
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-        ri[i] = m - (int)r.wa[k0 + i - 1];
+        ri[i] = m - r.wa[k0 + i - 1];
         rx[i] = XL::at(cur.x, m);
         // a budget shifted below 0 reads the lane's own budget (in bounds)
         ry[i] = YL::at(cur.y, ri[i] >= 0 ? ri[i] : m);
@@ -667,7 +708,7 @@ __device__ __forceinline__ void relax_mixed_nb(Narrow::Acc (&acc)[NB], const Cha
     int wa[N];
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-        wa[i] = (int)r.wa[k0 + i - 1];
+        wa[i] = r.wa[k0 + i - 1];
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
             const int ri = m[b] - wa[i];
@@ -726,7 +767,7 @@ __device__ __forceinline__ void diag_body(const ChainRows &r, const ChainWork &c
     for (int b = 0; b < NB; ++b)
         m[b] = min(m0 + b * kEdgeThreads, M);
     // the C_2 operand first (the lane's own budget when it is out of reach)
-    const int wab = (int)r.wabar[s - 1];
+    const int wab = r.wabar[s - 1];
     const int32_t gall = cw.gall[cell];
     const int64_t below = row_of(L, s + 1, t) * pitch;
     typename P::Raw c2[NB];
@@ -786,7 +827,7 @@ __global__ __launch_bounds__(kEdgeThreads) void diag_kernel(const int64_t *__res
     const int m0 = blockIdx.x * (kEdgeThreads * kEdgeBudgets) + threadIdx.x;
     if (m0 > M)
         return;
-    const ChainRows r = chain_rows(params, L, c);
+    const ChainRows r = chain_rows(params, w, L, c);
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
@@ -832,7 +873,7 @@ __device__ __forceinline__ void diag_split_body(const ChainRows &r, const ChainW
     for (int v = 1; v < 4; ++v)
         P::merge_later(acc, part[v][lane]);
     const int64_t cell = row_of(L, s, t);
-    const int ri = m - (int)r.wabar[s - 1];
+    const int ri = m - r.wabar[s - 1];
     const bool all_ok = m >= cw.gall[cell] && ri >= 0;
     const int64_t below = row_of(L, s + 1, t) * pitch;
     const typename P::Raw c2 = P::load(tab + below, cw.shadow + below, all_ok ? ri : m);
@@ -854,7 +895,7 @@ __global__ __launch_bounds__(256) void diag_split_kernel(const int64_t *__restri
     const int t = s + d;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int m = blockIdx.x * 64 + (threadIdx.x & 63);
-    const ChainRows r = chain_rows(params, L, c);
+    const ChainRows r = chain_rows(params, w, L, c);
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
@@ -947,7 +988,7 @@ __device__ inline void finish_corner(const ChainRows &r, const ChainWork &cw, in
                                      int t, typename P::Acc acc, int64_t *tab, int16_t *dtab)
 {
     const int64_t cell = row_of(L, s, t);
-    const int ri = m - (int)r.wabar[s - 1];
+    const int ri = m - r.wabar[s - 1];
     const bool all_ok = m >= cw.gall[cell] && ri >= 0;
     const int64_t below = row_of(L, s + 1, t) * pitch;
     const typename P::Raw c2 = P::load(tab + below, cw.shadow + below, all_ok ? ri : m);
@@ -985,17 +1026,17 @@ __device__ inline void middle_body(const ChainRows &r, const ChainWork &cw, int 
     uint64_t prefix = (uint64_t)(cw.pre[ka - 1] - cw.pre[k_lo - 1]);  // u_f from k_lo on
     typename P::Raw ax[kSub], ay[kSub], bx[kSub], by[kSub];
     int k = ka;
-    int ra = tl.mc - (int)r.wa[k - 1];
+    int ra = tl.mc - r.wa[k - 1];
     tl.load(ra, ax, ay);
     for (; k + 1 <= kb; k += 2) {
         tl.advance(L, k, pitch);
-        const int rb = tl.mc - (int)r.wa[k];
+        const int rb = tl.mc - r.wa[k];
         tl.load(rb, bx, by);
         prefix += (uint64_t)r.uf[k - 1];
         middle_update<P>(acc, ax, ay, prefix, (uint32_t)(k + 1), ra >= 0);
         if (k + 2 <= kb) {
             tl.advance(L, k + 1, pitch);
-            ra = tl.mc - (int)r.wa[k + 1];
+            ra = tl.mc - r.wa[k + 1];
             tl.load(ra, ax, ay);
         }
         prefix += (uint64_t)r.uf[k];
@@ -1049,7 +1090,7 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
     if (t0 > L)
         return;
     const int nt = min(kSub, L - t0 + 1);
-    const ChainRows r = chain_rows(params, L, c);
+    const ChainRows r = chain_rows(params, w, L, c);
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
@@ -1206,7 +1247,7 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     // key split bits: the whole range's, or those of a run of 2^S splits
     const int S = full ? (k_hi > k_lo ? 32 - __clz(k_hi - k_lo) : 0) : cw.pbits[delta];
     const int R = full ? INT_MAX : 1 << S;  // splits per run, a multiple of kStage
-    const ChainRows r = chain_rows(params, L, c);
+    const ChainRows r = chain_rows(params, w, L, c);
     const int mc = m <= M ? m : M;
     const int n_stages = (kb - ka + kStage) / kStage;
 
@@ -1230,7 +1271,7 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
 #pragma unroll
         for (int p = 0; p < kStage; ++p) {
             const int k = k_copy;
-            const int ri = mc - (int)r.wa[k - 1];
+            const int ri = mc - r.wa[k - 1];
             const uint32_t off = 4u * (uint32_t)(copies_x ? mc : (ri >= 0 ? ri : mc));
 #pragma unroll
             for (int i = 0; i < kDmaPerSplit; ++i)
@@ -1320,7 +1361,7 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
 #pragma unroll
         for (int p = 0; p < kStage; ++p, ++k) {
             const bool real = k <= kb;
-            const int ri = mc - (int)r.wa[(real ? k : kb) - 1];
+            const int ri = mc - r.wa[(real ? k : kb) - 1];
             prefix += real ? (uint32_t)r.uf[k - 1] : 0u;
             const uint32_t add = real && ri >= 0 ? (prefix << S) | (uint32_t)(k - run_base) : kInf32;
 #pragma unroll
@@ -1413,7 +1454,7 @@ __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &c
     // table) and the C_2 operand (the lane's own budget when C_2 is out of
     // reach)
     const bool packed_partial = P::kShadow && middle_packed(cw, (k_hi - k_lo) / kT + 1, k_hi - k_lo);
-    const int wab = (int)r.wabar[s - 1];
+    const int wab = r.wabar[s - 1];
     const int32_t gall = cw.gall[cell];
     const int64_t below = row_of(L, s + 1, t) * pitch;
     uint32_t key[NB];
@@ -1496,7 +1537,7 @@ __global__ __launch_bounds__(kEdgeThreads) void edge_kernel(const int64_t *__res
     const int m0 = blockIdx.x * (kEdgeThreads * kEdgeBudgets) + threadIdx.x;
     if (t > L || m0 > M)
         return;
-    const ChainRows r = chain_rows(params, L, c);
+    const ChainRows r = chain_rows(params, w, L, c);
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
@@ -1524,24 +1565,6 @@ uint64_t in_block_pairs(int L, int d)
 
 }  // namespace
 
-WorkLayout work_layout(int n_chains, int L, int64_t pitch)
-{
-    auto align = [](uint64_t x) { return (x + 255) / 256 * 256; };
-    const uint64_t rows = (uint64_t)L * (L + 1) / 2;
-    WorkLayout wl;
-    const uint64_t nb = (uint64_t)((L + kT - 1) / kT);
-    wl.pre = 0;
-    wl.pbits = align(wl.pre + 8ull * n_chains * (L + 1));
-    wl.bsum = align(wl.pbits + 4ull * n_chains * nb);
-    wl.gnone = align(wl.bsum + 16ull * n_chains * (nb + 1));
-    wl.gall = align(wl.gnone + 4ull * n_chains * rows);
-    wl.shadow = align(wl.gall + 4ull * n_chains * rows);
-    wl.half = align(wl.shadow + 4ull * n_chains * rows * (uint64_t)pitch);
-    const uint64_t half_rows = nb >= 2 ? (uint64_t)L * kT : 0;  // no edges in a single block
-    wl.total = align(wl.half + 2ull * n_chains * half_rows * (uint64_t)half_pitch_of(pitch));
-    return wl;
-}
-
 Work work_view(void *base, int n_chains, int L, int64_t pitch)
 {
     const WorkLayout wl = work_layout(n_chains, L, pitch);
@@ -1552,6 +1575,8 @@ Work work_view(void *base, int n_chains, int L, int64_t pitch)
     w.bsum = (int64_t *)(b + wl.bsum);
     w.gnone = (int32_t *)(b + wl.gnone);
     w.gall = (int32_t *)(b + wl.gall);
+    w.status = (int32_t *)(b + wl.status);
+    w.shift = (int32_t *)(b + wl.shift);
     w.shadow = (uint32_t *)(b + wl.shadow);
     w.half = (int16_t *)(b + wl.half);
     return w;
@@ -1576,7 +1601,7 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
 
     if ((e = before(kPrep)) != hipSuccess)
         return e;
-    prep_kernel<<<dim3(L + 1, tb.n_chains), 64, 0, stream>>>(tb.params, L, tb.rows, w);
+    prep_kernel<<<dim3(L + 1, tb.n_chains), 64, 0, stream>>>(tb.params, L, tb.M, tb.rows, w);
     if ((e = launched(kPrep, 0, 0, 0)) != hipSuccess)
         return e;
     if ((e = before(kLeaf)) != hipSuccess)

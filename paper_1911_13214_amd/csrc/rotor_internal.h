@@ -5,26 +5,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "rotor.h"
+#include "rotor_geometry.h"
 
 namespace rotor {
-
-// Row of the pair (s, t), 1 <= s <= t <= L, in a chain's table: the upper
-// triangle stored s-major, so the rows (s, s), (s, s+1), ..., (s, L) are
-// consecutive and the row of (s, t+1) follows the row of (s, t).
-__host__ __device__ inline int64_t row_of(int L, int s, int t)
-{
-    return (int64_t)(s - 1) * L - (int64_t)(s - 1) * (s - 2) / 2 + (t - s);
-}
-
-// Row pitch: M + 1 rounded up to 32 elements, so that every row of the int64
-// table starts 256 bytes and every row of the 4-byte compact copy 128 bytes
-// (one cache line) after an aligned table base.
-__host__ __device__ inline int64_t pitch_of(int64_t M) { return (M + 1 + 31) / 32 * 32; }
-
-// Row pitch of the 2-byte copy of the diagonal blocks: a multiple of 64
-// elements (128 bytes).
-__host__ __device__ inline int64_t half_pitch_of(int64_t pitch) { return (pitch + 63) / 64 * 64; }
 
 // Everything one fill launch needs to address a batch of tables.
 struct Tables {
@@ -40,26 +23,53 @@ struct Tables {
 
 // Device workspace of a fill: prefix sums of u_f, per block-diagonal value
 // path and packed key width and the sums they are computed from, the gates
-// m_none and m_all of every pair, a compact uint32 copy of the cost table
-// (written and read by the pairs whose costs stay below 2^30), and a 2-byte
-// copy of the cells of the diagonal blocks (chains whose costs there stay
-// below 2^15).
+// m_none and m_all of every pair, a domain status word per chain, the sizes
+// by which operand budgets are shifted (clamped, see prep_kernel), a compact
+// uint32 copy of the cost table (written and read by the pairs whose costs
+// stay below 2^30), and a 2-byte copy of the cells of the diagonal blocks
+// (chains whose costs there stay below 2^15).
 struct Work {
     int64_t *pre;      // [n_chains][L + 1]
     int32_t *pbits;    // [n_chains][nb], nb = ceil(L / 16): packed key bits of block-diagonal D, -1: 64-bit path
     int64_t *bsum;     // [n_chains][2][nb + 1]: sums of prefix sums of u_f, and of u_b, to block ends
     int32_t *gnone;    // [n_chains][rows]
     int32_t *gall;     // [n_chains][rows]
+    int32_t *status;   // [n_chains]: ROTOR_OK, or ROTOR_EDOMAIN if the chain's parameters are outside the domain
+    int32_t *shift;    // [n_chains][2][L]: w_a and w_abar of every stage, clamped into [0, M + 1]
     uint32_t *shadow;  // [n_chains][rows][pitch]
     int16_t *half;     // [n_chains][nb][16][16][half_pitch]: 2-byte copy of the diagonal blocks' cells
 };
 
-// Byte offsets of the workspace sections (each 256-byte aligned).
-struct WorkLayout {
-    uint64_t pre, pbits, bsum, gnone, gall, shadow, half, total;
-};
-WorkLayout work_layout(int n_chains, int L, int64_t pitch);
 Work work_view(void *base, int n_chains, int L, int64_t pitch);
+
+// Whether one chain's parameters [6][L] lie in the domain of the library
+// (rotor_geometry.h), decided by the 64 lanes of one wave together; every
+// lane returns the same answer.  The sums are checked term by term, so no
+// value can wrap them.
+__device__ inline bool chain_in_domain(const int64_t *p, int L, int lane)
+{
+    bool bad = false;
+    uint64_t suf = 0, sub = 0;
+    for (int l = lane; l < L; l += 64) {
+        const int64_t uf = p[ROTOR_ROW_UF * L + l], ub = p[ROTOR_ROW_UB * L + l];
+        bad |= uf < 0 || ub < 0 || (uint64_t)uf >= kCostBound || (uint64_t)ub >= kCostBound;
+        for (int row = ROTOR_ROW_WA; row <= ROTOR_ROW_OB; ++row) {
+            const int64_t v = p[row * L + l];
+            bad |= v < 0 || v >= kMaxSize;
+        }
+        if (!bad) {  // each term below 2^44, at most 512 terms per lane: no wrap
+            suf += (uint64_t)uf;
+            sub += (uint64_t)ub;
+        }
+    }
+    for (int off = 32; off >= 1; off /= 2) {
+        suf += __shfl_xor(suf, off);
+        sub += __shfl_xor(sub, off);
+    }
+    bad = __any(bad);
+    // L * suf + sub < 2^44, without overflow
+    return !bad && suf < kCostBound && sub < kCostBound && suf <= (kCostBound - sub) / (uint64_t)L;
+}
 
 // Kernel classes of the fill, in the order of rotor_kernel_stats.
 enum KernelClass { kLeaf = 0, kDiag = 1, kMiddle = 2, kEdge = 3, kPrep = 4 };

@@ -6,7 +6,7 @@
 
 #include <vector>
 
-#include "rotor_internal.h"
+#include "rotor.h"
 
 namespace {
 

@@ -24,9 +24,17 @@ __global__ void walk_kernel(const int64_t *__restrict__ params, int L, int M, in
                             rotor_op *__restrict__ ops, int64_t *__restrict__ count, int32_t *__restrict__ status)
 {
     extern __shared__ uint64_t stack[];
+    // the whole wave checks the chain's parameters; a table filled from
+    // parameters outside the domain is unspecified and is not walked
+    const bool in_domain = chain_in_domain(params, L, threadIdx.x);
     if (threadIdx.x != 0)
         return;
     const int b = blockIdx.x;
+    if (!in_domain) {
+        count[b] = 0;
+        status[b] = ROTOR_EDOMAIN;
+        return;
+    }
     const int64_t *wa = params + (int64_t)ROTOR_ROW_WA * L;
     const int64_t *wabar = params + (int64_t)ROTOR_ROW_WABAR * L;
     rotor_op *out = ops + (int64_t)b * cap;
@@ -72,8 +80,10 @@ __global__ void walk_kernel(const int64_t *__restrict__ params, int L, int M, in
                 st = ROTOR_ECORRUPT;
                 break;
             }
+            // a budget outside [0, M] (a negative size: parameters outside
+            // the domain) is never read
             const int64_t mr = m - wa[sp - 2];
-            if (mr < 0 || top + 2 > L + 1) {
+            if (mr < 0 || mr > M || top + 2 > L + 1) {
                 st = ROTOR_ECORRUPT;
                 break;
             }
@@ -85,7 +95,7 @@ __global__ void walk_kernel(const int64_t *__restrict__ params, int L, int M, in
         } else {
             // F_all^s, then [s+1, t] with abar^s stored, then B^s.
             const int64_t mr = m - wabar[s - 1];
-            if (mr < 0 || top + 2 > L + 1) {
+            if (mr < 0 || mr > M || top + 2 > L + 1) {
                 st = ROTOR_ECORRUPT;
                 break;
             }

@@ -41,6 +41,7 @@ SIGNATURES = {
     "rotor_solve": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp, _u64, _vp]),
     "rotor_solve_schedule": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp, _u64, _vp, _i32]),
     "rotor_reconstruct": (_i32, [_vp, _i32, _i32, _i64, _vp, _i32, _i32, _vp, _i64, _vp, _vp, _vp, _vp]),
+    "rotor_solve_status": (_i32, [_vp, _u64, _i32, _i32, _i64, _vp, _vp]),
     "rotor_solve_timed": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp, _u64, _vp, _vp]),
     "rotor_discretize": (_i32, [_vp, _i32, _i32, _vp, _i64, _vp]),
     "rotor_store_all_peak": (_i32, [_vp, _i32, _P(_i64)]),
@@ -175,6 +176,20 @@ def rotor_solve_timed(d_params, n_chains: int, L: int, M: int, d_cost, d_dec, d_
     _check(lib().rotor_solve_timed(p, n_chains, L, M, c, d, w, wb, _stream_ptr(stream),
                                    ctypes.cast(stats, ctypes.c_void_p)), "rotor_solve_timed")
     return {name: {f: getattr(st, f) for f, _ in KernelStats._fields_} for name, st in zip(KERNEL_CLASSES, stats)}
+
+
+def rotor_solve_status(d_work, n_chains: int, L: int, M: int, stream=None):
+    """Domain report of the solve that last used ``d_work`` (synchronises the
+    stream): (status, per-chain statuses), status ROTOR_OK or
+    ROTOR_EDOMAIN."""
+    if not hasattr(d_work, "is_cuda") or not d_work.is_cuda or not d_work.is_contiguous():
+        raise ValueError("workspace must be a contiguous CUDA tensor")
+    per = np.zeros(n_chains, dtype=np.int32)
+    st = lib().rotor_solve_status(d_work.data_ptr(), d_work.numel() * d_work.element_size(), n_chains, L, M,
+                                  per.ctypes.data, _stream_ptr(stream))
+    if st not in (ROTOR_OK, ROTOR_EDOMAIN):
+        raise RotorError(st, "rotor_solve_status")
+    return st, per
 
 
 def rotor_reconstruct(d_params, n_chains: int, L: int, M: int, d_dec, chain: int, d_budgets, cap: int, d_ops,

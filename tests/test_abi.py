@@ -73,14 +73,16 @@ def test_workspace_size(n_chains, L, M):
     pitch, rows, cb, db = rotor.rotor_layout(n_chains, L, M)
     ws = rotor.rotor_workspace_bytes(n_chains, L, M)
     # a 4-byte copy of every cell plus per-pair gates and per-stage prefixes,
-    # per block of 16 stages a key width and two sums, and (two blocks or
-    # more) a 2-byte copy of the diagonal blocks: 16 rows per stage of
-    # pitch rounded to 64
+    # per block of 16 stages a key width and two sums, per chain a status
+    # word and two 4-byte shift sizes per stage, and (two blocks or more) a
+    # 2-byte copy of the diagonal blocks: 16 rows per stage of pitch rounded
+    # to 64
     nb = (L + 15) // 16
     half = 2 * n_chains * L * 16 * ((pitch + 63) // 64 * 64) if nb >= 2 else 0
     need = n_chains * rows * (4 * pitch + 8) + n_chains * 8 * (L + 1) + n_chains * (4 * nb + 16 * (nb + 1)) + half
+    need += n_chains * (4 + 8 * L)
     assert ws >= need
-    assert ws <= need + 8 * 256
+    assert ws <= need + 10 * 256
     assert ws % 256 == 0
 
 
@@ -139,3 +141,9 @@ def test_solve_and_reconstruct_reject_bad_arguments_before_any_device_work():
     assert r(fake, 1, 10, 100, fake, 0, 1, fake, 10, None, fake, fake, None) == rotor.ROTOR_EINVAL  # ops
     assert r(fake, 1, 8192, 10, fake, 0, 1, fake, 10, fake, fake, fake, None) == rotor.ROTOR_EINVAL  # L
     assert r(fake, 1, 10, 100, fake, 0, 1, fake, -1, fake, fake, fake, None) == rotor.ROTOR_EINVAL  # cap
+    st = lib.rotor_solve_status
+    assert st(None, big, 1, 10, 100, None, None) == rotor.ROTOR_EINVAL  # workspace
+    assert st(fake, need - 1, 1, 10, 100, None, None) == rotor.ROTOR_EINVAL  # too small
+    assert st(ctypes.c_void_p(0x1004), big, 1, 10, 100, None, None) == rotor.ROTOR_EINVAL  # misaligned
+    assert st(fake, big, 0, 10, 100, None, None) == rotor.ROTOR_EINVAL  # n_chains
+    assert st(fake, big, 1, 10, 1 << 28, None, None) == rotor.ROTOR_EINVAL  # M

@@ -1,0 +1,87 @@
+"""Parameters outside the library's domain, passed straight to the device
+entry points (no host check): the fill stays within the caller's buffers,
+rotor_solve_status reports the chain, rotor_reconstruct refuses it, and a
+chain in the domain solved in the same batch still equals the oracle."""
+import numpy as np
+import pytest
+
+from gpu_util import chain_tables
+from oracle import oracle as orc
+from paper_1911_13214_amd import chaingen
+
+pytestmark = pytest.mark.gpu
+
+L, M = 40, 300  # three 16-stage blocks: diagonal blocks, middle products and edge rounds
+# (row, stage index, value): each makes the chain leave the domain
+BAD = [
+    ("negative w_a", 2, 7, -9),
+    ("w_a with bit 31 set", 2, 20, (1 << 31) + 5),
+    ("w_a beyond 2^32", 2, 33, (1 << 32) + 3),
+    ("negative w_abar", 3, 12, -7),
+    ("w_abar with bit 31 set", 3, 30, (1 << 31) + 1),
+    ("huge w_abar", 3, 5, (1 << 62)),
+    ("negative u_f", 0, 9, -100),
+    ("u_f at 2^44", 0, 17, 1 << 44),
+    ("negative u_b", 1, 3, -1),
+    ("o_f at 2^40", 4, 25, 1 << 40),
+    ("negative o_b", 5, 39, -4),
+]
+
+
+def _solve_raw(params, schedule):
+    """Upload without the host check and fill through the C ABI."""
+    import torch
+
+    from paper_1911_13214_amd import rotor
+    n = params.shape[0]
+    d_params = torch.from_numpy(np.ascontiguousarray(params)).to("cuda")
+    cost, dec = rotor.alloc_tables(n, L, M, "cuda")
+    work = rotor.alloc_workspace(n, L, M, "cuda")
+    rotor.rotor_solve_schedule(d_params, n, L, M, cost, dec, work, schedule)
+    torch.cuda.synchronize()
+    return d_params, cost, dec, work
+
+
+@pytest.mark.parametrize("schedule", ["blocked", "diagonal"])
+@pytest.mark.parametrize("what,row,col,val", BAD, ids=[b[0] for b in BAD])
+def test_out_of_domain_chain_is_reported(what, row, col, val, schedule):
+    import torch
+
+    from paper_1911_13214_amd import rotor
+    print(f"domain {what} {schedule}", flush=True)
+    good = chaingen.random_chains(1, L, seed=77)
+    bad = good.copy()
+    bad[0, row, col] = val
+    assert rotor.rotor_check_params(bad, M) == rotor.ROTOR_EDOMAIN
+    params = np.concatenate([bad, good, bad])  # chains 0 and 2 outside, chain 1 inside
+    d_params, cost, dec, work = _solve_raw(params, schedule)
+    st, per = rotor.rotor_solve_status(work, 3, L, M)
+    assert st == rotor.ROTOR_EDOMAIN
+    assert per.tolist() == [rotor.ROTOR_EDOMAIN, rotor.ROTOR_OK, rotor.ROTOR_EDOMAIN]
+    # the chain inside the domain is untouched by its neighbours
+    C, D = orc.solve(good, M)
+    gc, gd = chain_tables(cost, dec, 1, L, M)
+    assert np.array_equal(gc, C) and np.array_equal(gd, D)
+    # the walk refuses the chains outside the domain, walks the other
+    budgets = torch.tensor([M, M // 2], dtype=torch.int64, device="cuda")
+    cap = L * (L + 1) // 2 + L
+    for c, want in [(0, rotor.ROTOR_EDOMAIN), (1, rotor.ROTOR_OK), (2, rotor.ROTOR_EDOMAIN)]:
+        ops = torch.zeros((2, cap, 2), dtype=torch.int32, device="cuda")
+        count = torch.full((2,), -1, dtype=torch.int64, device="cuda")
+        status = torch.full((2,), 99, dtype=torch.int32, device="cuda")
+        rotor.rotor_reconstruct(d_params, 3, L, M, dec, c, budgets, cap, ops, count, status)
+        torch.cuda.synchronize()
+        got = status.cpu().numpy()
+        if want == rotor.ROTOR_OK:
+            assert set(got.tolist()) <= {rotor.ROTOR_OK, rotor.ROTOR_INFEASIBLE}
+        else:
+            assert got.tolist() == [want, want] and count.cpu().numpy().tolist() == [0, 0]
+
+
+def test_status_of_a_batch_in_the_domain():
+    from paper_1911_13214_amd import rotor
+    print("domain: batch inside", flush=True)
+    params = chaingen.random_chains(4, L, seed=78)
+    _, _, _, work = _solve_raw(params, "auto")
+    st, per = rotor.rotor_solve_status(work, 4, L, M)
+    assert st == rotor.ROTOR_OK and per.tolist() == [0, 0, 0, 0]
