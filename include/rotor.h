@@ -60,7 +60,10 @@
  * Streams.  `stream` is a hipStream_t passed as void* (NULL: the default
  * stream).  Entry points that take device buffers only enqueue work and
  * return; argument errors are reported synchronously by the return value,
- * device-side failures surface at the caller's next synchronisation.  The
+ * device-side failures surface at the caller's next synchronisation.  Before
+ * enqueuing, they clear the calling thread's pending HIP error (the one
+ * hipGetLastError would return), so that ROTOR_EDEVICE reports a failure of
+ * their own launches only.  The
  * library keeps no state between calls and allocates no device memory (the
  * caller passes the solve's workspace); concurrent calls on distinct output
  * buffers and workspaces are independent.

@@ -1584,6 +1584,10 @@ Work work_view(void *base, int n_chains, int L, int64_t pitch)
 
 hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_t stream, LaunchObserver *obs)
 {
+    // hipGetLastError also returns an error an earlier runtime call of the
+    // caller left behind: clear it, so that the checks below see only these
+    // launches
+    (void)hipGetLastError();
     const int L = tb.L;
     const uint64_t W = (uint64_t)tb.M + 1;
     const uint64_t nc = (uint64_t)tb.n_chains;

@@ -117,6 +117,7 @@ hipError_t launch_reconstruct(const int64_t *params, int L, int M, int64_t pitch
                               rotor_op *ops, int64_t *count, int32_t *status, hipStream_t stream)
 {
     (void)rows;
+    (void)hipGetLastError();  // an error the caller's earlier calls left behind is not this launch's
     const size_t lds = sizeof(uint64_t) * (size_t)(L + 1);
     walk_kernel<<<dim3(n_budgets), 64, lds, stream>>>(params, L, M, pitch, dec_chain, budgets, cap, ops, count,
                                                       status);

@@ -70,6 +70,16 @@ def lib():
     """The loaded library.  Raises if it has not been built."""
     global _lib
     if _lib is None:
+        # torch ships its own HIP runtime under the same soname as the
+        # system's (libamdhip64.so.7).  Loaded after torch, the library binds
+        # to torch's runtime; loaded first, it would pull in the system copy
+        # and torch would then load a second runtime, whose memory and
+        # streams the library's launches would not know.  So torch comes
+        # first.
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -c 'import __graft_entry__ as g; "
                                "g.build()'` (hipcc, gfx950)")
