@@ -66,7 +66,8 @@
  * their own launches only.  The
  * library keeps no state between calls and allocates no device memory (the
  * caller passes the solve's workspace); concurrent calls on distinct output
- * buffers and workspaces are independent.
+ * buffers and workspaces are independent.  The one exception is
+ * rotor_solve_noalloc, whose workspace is a static device array per device.
  */
 #ifndef ROTOR_H
 #define ROTOR_H
@@ -171,6 +172,30 @@ ROTOR_API int32_t rotor_workspace_bytes(int32_t n_chains, int32_t L, int64_t M, 
  * share a workspace must not overlap. */
 ROTOR_API int32_t rotor_solve(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
                               int16_t *d_dec, void *d_work, uint64_t work_bytes, void *stream);
+
+/* Workspace bytes of rotor_solve_noalloc: a static device array of this size
+ * (128 MiB), held by every device the library runs on until the process
+ * ends. */
+#define ROTOR_NOALLOC_WORK_BYTES (128ull << 20)
+
+/* rotor_solve for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same fill, same tables, same fill order, with the workspace taken from
+ * a static device array of ROTOR_NOALLOC_WORK_BYTES bytes per device instead
+ * of a caller buffer.  The caller still passes parameters and tables (as for
+ * rotor_solve).  It calls no hipMalloc, hipFree or allocating library
+ * routine.  Every call on one device shares that device's array, so calls
+ * that overlap on one device (different streams, or host threads) race and
+ * must be serialised by the caller; nothing left in the array by an earlier
+ * call affects a later one.  The per-device domain status is not kept for
+ * rotor_solve_status (use rotor_check_params on the host).
+ * Returns ROTOR_OK once every kernel is enqueued, ROTOR_EINVAL for a null or
+ * misaligned pointer or a size out of range, ROTOR_ECAPACITY if the
+ * workspace these sizes need (rotor_workspace_bytes) exceeds
+ * ROTOR_NOALLOC_WORK_BYTES, ROTOR_EDEVICE if the array's address cannot be
+ * found or a launch fails. */
+ROTOR_API int32_t rotor_solve_noalloc(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M,
+                                      int64_t *d_cost, int16_t *d_dec, void *stream);
 
 /* Domain report of the solve that last used this workspace: waits for
  * `stream` (the stream of that solve), then reads the status word the fill

@@ -11,7 +11,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "librotor.so")
-SOURCES = ["rotor_host.cpp", "rotor_api.cpp", "rotor_plan.cpp", "rotor_fill.hip", "rotor_reconstruct.hip"]
+SOURCES = ["rotor_host.cpp", "rotor_api.cpp", "rotor_plan.cpp", "rotor_fill.hip", "rotor_reconstruct.hip", "rotor_noalloc.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

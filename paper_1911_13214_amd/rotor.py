@@ -41,6 +41,7 @@ SIGNATURES = {
     "rotor_solve": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp, _u64, _vp]),
     "rotor_solve_schedule": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp, _u64, _vp, _i32]),
     "rotor_reconstruct": (_i32, [_vp, _i32, _i32, _i64, _vp, _i32, _i32, _vp, _i64, _vp, _vp, _vp, _vp]),
+    "rotor_solve_noalloc": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp]),
     "rotor_solve_status": (_i32, [_vp, _u64, _i32, _i32, _i64, _vp, _vp]),
     "rotor_solve_timed": (_i32, [_vp, _i32, _i32, _i64, _vp, _vp, _vp, _u64, _vp, _vp]),
     "rotor_discretize": (_i32, [_vp, _i32, _i32, _vp, _i64, _vp]),
@@ -186,6 +187,21 @@ def rotor_solve_timed(d_params, n_chains: int, L: int, M: int, d_cost, d_dec, d_
     _check(lib().rotor_solve_timed(p, n_chains, L, M, c, d, w, wb, _stream_ptr(stream),
                                    ctypes.cast(stats, ctypes.c_void_p)), "rotor_solve_timed")
     return {name: {f: getattr(st, f) for f, _ in KernelStats._fields_} for name, st in zip(KERNEL_CLASSES, stats)}
+
+
+NOALLOC_WORK_BYTES = 128 << 20
+
+
+def rotor_solve_noalloc(d_params, n_chains: int, L: int, M: int, d_cost, d_dec, stream=None):
+    """rotor_solve with the library's static device workspace instead of a
+    caller buffer (asynchronous; calls on one device must not overlap)."""
+    import torch
+    _, _, cb, db = rotor_layout(n_chains, L, M)
+    if d_params.numel() < n_chains * N_ROWS * L or d_cost.numel() * 8 < cb or d_dec.numel() * 2 < db:
+        raise ValueError("buffer smaller than the layout requires")
+    _check(lib().rotor_solve_noalloc(_dev_ptr(d_params, torch.int64, "params"), n_chains, L, M,
+                                     _dev_ptr(d_cost, torch.int64, "cost"), _dev_ptr(d_dec, torch.int16, "dec"),
+                                     _stream_ptr(stream)), "rotor_solve_noalloc")
 
 
 def rotor_solve_status(d_work, n_chains: int, L: int, M: int, stream=None):
