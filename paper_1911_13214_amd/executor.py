@@ -27,7 +27,6 @@ discretise, reconstruct, sequence cost) runs in the library through
 """
 from __future__ import annotations
 
-import time
 
 import numpy as np
 
@@ -166,8 +165,9 @@ def estimate(stages, x, repeats=3, batch_runs=4):
 
 def measure(stages, x, dy, ops, repeats=3):
     """Run ``ops`` ``repeats`` times after one warm-up; returns (median time
-    in microseconds, peak memory in bytes above what was allocated before the
-    sequence started: parameters, their gradients, x and dy)."""
+    in microseconds, from HIP events on the stream the sequence runs on,
+    peak memory in bytes above what was allocated before the sequence
+    started: parameters, their gradients, x and dy)."""
     import torch
 
     dev = x.device
@@ -177,10 +177,12 @@ def measure(stages, x, dy, ops, repeats=3):
         _sync(dev)
         base = torch.cuda.memory_allocated(dev)
         torch.cuda.reset_peak_memory_stats(dev)
-        t0 = time.perf_counter()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
         g = run_sequence(stages, x, dy, ops)
+        e1.record()
         _sync(dev)
-        times.append(time.perf_counter() - t0)
+        times.append(e0.elapsed_time(e1) * 1e-3)
         peaks.append(torch.cuda.max_memory_allocated(dev) - base)
         del g
     return float(np.median(times) * 1e6), int(max(peaks))

@@ -10,8 +10,10 @@ pytestmark = pytest.mark.gpu
 
 def test_sequences_run_within_budget_and_as_predicted():
     from paper_1911_13214_amd import executor as ex
-    print("executor validate L=12 width=512 batch=2048", flush=True)
-    res = ex.validate(L=12, seed=3, width=512, batch=2048, slots=500, n_budgets=10, repeats=5)
+    # a chain whose sequences keep the device busy (about 15 ms each), timed
+    # with HIP events, so that the times compared are the device's
+    print("executor validate L=24 width=1024 batch=4096", flush=True)
+    res = ex.validate(L=24, seed=1, width=1024, batch=4096, slots=500, n_budgets=10, repeats=5)
     ok = [r for r in res["rows"] if r["feasible"]]
     assert len(ok) >= 4
     assert res["all_gradients_equal"]
@@ -20,12 +22,9 @@ def test_sequences_run_within_budget_and_as_predicted():
         # allocator slack: blocks are rounded to 512 bytes, plus the input gradient at the end
         assert r["measured_bytes"] <= r["budget_bytes"] * 1.02 + (8 << 20), r
     assert res["mape_memory"] < 0.03, res["mape_memory"]
-    # wall-clock times of a 2 ms chain issued from the host against the
-    # model's device times: 6% apart in a warm process, up to a third on the
-    # first run of a fresh GPU (at a size where the device dominates, 4.5%)
-    assert res["mape_time"] < 0.5, res["mape_time"]
-    # less memory, more recomputation: the tightest budget is not measurably
-    # faster than the loosest.  A sequence of this chain takes about 2 ms of
-    # host-issued launches, whose wall-clock times vary by a few percent.
+    # the model's time (Section 5.4 reports 7.8% mean error on real networks)
+    assert res["mape_time"] < 0.15, res["mape_time"]
+    # less memory, more recomputation: the tightest feasible budget is slower
+    # than the loosest (16.5 against 13.9 ms predicted)
     times = [r["measured_us"] for r in ok]
-    assert times[0] >= times[-1] * 0.9, times
+    assert times[0] >= times[-1] * 0.98, times
