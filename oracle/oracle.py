@@ -35,11 +35,16 @@ def build(force: bool = True) -> str:
 
 
 def lib():
+    """The oracle library: ``oracle/liboracle.so``, or the build named by the
+    environment variable ROTOR_ORACLE_LIB (the sanitizer build of the tests)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB):
-            build(force=False)
-        l = ctypes.CDLL(LIB)
+        path = os.environ.get("ROTOR_ORACLE_LIB")
+        if not path:
+            path = LIB
+            if not os.path.exists(LIB):
+                build(force=False)
+        l = ctypes.CDLL(path)
         i64p = ctypes.POINTER(ctypes.c_int64)
         i16p = ctypes.POINTER(ctypes.c_int16)
         i32p = ctypes.POINTER(ctypes.c_int32)

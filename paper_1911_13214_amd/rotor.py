@@ -68,9 +68,13 @@ class RotorError(RuntimeError):
 
 
 def lib():
-    """The loaded library.  Raises if it has not been built."""
+    """The loaded library (``librotor.so`` beside this file, or the build
+    named by the environment variable ROTOR_LIB).  Raises if it has not been
+    built.  A host-only build (the sanitizer build of the CPU tests) lacks
+    the device entry points: they stay unbound, and calling one raises."""
     global _lib
     if _lib is None:
+        override = os.environ.get("ROTOR_LIB")
         # torch ships its own HIP runtime under the same soname as the
         # system's (libamdhip64.so.7).  Loaded after torch, the library binds
         # to torch's runtime; loaded first, it would pull in the system copy
@@ -81,11 +85,14 @@ def lib():
             import torch  # noqa: F401
         except ImportError:
             pass
-        if not os.path.exists(LIB_PATH):
-            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -c 'import __graft_entry__ as g; "
+        path = override or LIB_PATH
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing: build it with `python -c 'import __graft_entry__ as g; "
                                "g.build()'` (hipcc, gfx950)")
-        l = ctypes.CDLL(LIB_PATH)
+        l = ctypes.CDLL(path)
         for name, (res, args) in SIGNATURES.items():
+            if override and not hasattr(l, name):
+                continue
             f = getattr(l, name)
             f.restype = res
             f.argtypes = args
