@@ -213,12 +213,16 @@ ROTOR_API int32_t rotor_solve_noalloc(const int64_t *d_params, int32_t n_chains,
 ROTOR_API int32_t rotor_solve_status(const void *d_work, uint64_t work_bytes, int32_t n_chains, int32_t L, int64_t M,
                                      int32_t *h_chain_status, void *stream);
 
-/* Fill orders of rotor_solve_schedule.  Both fill the same tables, bit for
+/* Fill orders of rotor_solve_schedule.  All fill the same tables, bit for
  * bit; they differ in speed.
  *   ROTOR_SCHEDULE_BLOCKED   16 x 16 blocks of pairs: register-tiled min-plus
  *                            products for the splits that reach across
- *                            blocks, 30 short launches per block-diagonal for
- *                            the others; the fast order for large tables.
+ *                            blocks; the splits inside the block's own rows
+ *                            and columns ("edges") by rows (16 launches per
+ *                            block-diagonal) when a block-diagonal holds at
+ *                            least 256 blocks over all chains, else by
+ *                            anti-diagonals (30 short launches); the fast
+ *                            order for large tables.
  *   ROTOR_SCHEDULE_DIAGONAL  one launch per t - s over all pairs (the
  *                            wavefront the recurrence allows), the splits of
  *                            a pair spread over four waves from t - s = 16 on;
@@ -227,10 +231,15 @@ ROTOR_API int32_t rotor_solve_status(const void *d_work, uint64_t work_bytes, in
  *                            candidates (L^3/6 (M+1)) for one chain, or 4e8
  *                            summed over a batch, or when one chain has
  *                            M < 63; BLOCKED otherwise (the order rotor_solve
- *                            uses). */
+ *                            uses).
+ *   ROTOR_SCHEDULE_BLOCKED_ROWS, ROTOR_SCHEDULE_BLOCKED_ROUNDS
+ *                            BLOCKED with the edges of every block-diagonal
+ *                            by rows, or by anti-diagonals. */
 #define ROTOR_SCHEDULE_AUTO 0
 #define ROTOR_SCHEDULE_BLOCKED 1
 #define ROTOR_SCHEDULE_DIAGONAL 2
+#define ROTOR_SCHEDULE_BLOCKED_ROWS 3
+#define ROTOR_SCHEDULE_BLOCKED_ROUNDS 4
 
 /* rotor_solve with an explicit fill order; ROTOR_EINVAL for an unknown one. */
 ROTOR_API int32_t rotor_solve_schedule(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M,

@@ -51,7 +51,7 @@ SIGNATURES = {
 }
 
 KERNEL_CLASSES = ("leaf", "diag", "middle", "edge", "prep")
-SCHEDULES = {"auto": 0, "blocked": 1, "diagonal": 2}
+SCHEDULES = {"auto": 0, "blocked": 1, "diagonal": 2, "rows": 3, "rounds": 4}
 
 
 class KernelStats(ctypes.Structure):

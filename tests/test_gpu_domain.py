@@ -42,7 +42,7 @@ def _solve_raw(params, schedule):
     return d_params, cost, dec, work
 
 
-@pytest.mark.parametrize("schedule", ["blocked", "diagonal"])
+@pytest.mark.parametrize("schedule", ["rounds", "rows", "diagonal"])
 @pytest.mark.parametrize("what,row,col,val", BAD, ids=[b[0] for b in BAD])
 def test_out_of_domain_chain_is_reported(what, row, col, val, schedule):
     import torch

@@ -20,7 +20,10 @@ def say(msg):
     print(msg, flush=True)
 
 
-SCHEDULES = ["blocked", "diagonal"]
+# the blocked fill with its edges by anti-diagonal rounds and by rows, and
+# the streamed diagonals
+SCHEDULES = ["rounds", "rows", "diagonal"]
+EDGE_ORDERS = ["rounds", "rows"]
 _oracle_cache = {}
 
 
@@ -399,7 +402,8 @@ def test_wide_value_path(L, M, seed, schedule):
 
 
 @pytest.mark.parametrize("L,M,seed", [(70, 300, 5), (90, 200, 6)])
-def test_narrow_chain_beyond_packed_keys(L, M, seed):
+@pytest.mark.parametrize("edges", EDGE_ORDERS)
+def test_narrow_chain_beyond_packed_keys(L, M, seed, edges):
     # costs below 2^30 (compact copy) but too large to leave the split field
     # room once the middle range has 16 splits or more: the first
     # block-diagonal takes packed keys, the later ones the (value, split) pairs
@@ -408,7 +412,7 @@ def test_narrow_chain_beyond_packed_keys(L, M, seed):
     v = cost_bound(p[0])
     assert (1 << 26) < v < (1 << 30)
     say(f"narrow beyond packed L={L} M={M} bound={v}")
-    _, cost, dec = solve_on_gpu(p, M, schedule="blocked")
+    _, cost, dec = solve_on_gpu(p, M, schedule=edges)
     assert_same(p, M, cost, dec)
 
 
@@ -427,7 +431,8 @@ def block_diagonal_bounds(p, L):
 
 
 @pytest.mark.parametrize("seed,shift", [(8, 7), (8, 8), (8, 9), (7, 6)])
-def test_packed_keys_per_block_diagonal(seed, shift):
+@pytest.mark.parametrize("edges", EDGE_ORDERS)
+def test_packed_keys_per_block_diagonal(seed, shift, edges):
     # The packed middle keys of block-diagonal D need (V_D + 1) << S to fit
     # in 32 bits, with S the bits of its split range and V_D the bound of its
     # longest pairs.  At these cost scales some block-diagonals fit with no
@@ -444,7 +449,7 @@ def test_packed_keys_per_block_diagonal(seed, shift):
     assert any(span_bits[D] == key_bits(vd[D]) for D in packed)
     assert any(span_bits[D] == key_bits(vd[D]) + 1 for D in vd)
     say(f"packed per block-diagonal seed={seed} shift={shift} bound={v} packed={sorted(packed)}")
-    _, cost, dec = solve_on_gpu(p, M, schedule="blocked")
+    _, cost, dec = solve_on_gpu(p, M, schedule=edges)
     assert_same(p, M, cost, dec)
 
 
@@ -475,7 +480,8 @@ def middle_modes(p, L, M, n_chains):
 
 
 @pytest.mark.parametrize("L,M,seed,shift", [(200, 240, 8, 5), (240, 200, 7, 4), (256, 300, 9, 4)])
-def test_packed_runs_per_block_diagonal(L, M, seed, shift):
+@pytest.mark.parametrize("edges", EDGE_ORDERS)
+def test_packed_runs_per_block_diagonal(L, M, seed, shift, edges):
     # Block-diagonals whose bound leaves a packed key 7 bits or more, but
     # fewer than their split range needs, relax the range in runs of 2^S
     # splits and merge the runs' (value, split) results in the cost table by
@@ -487,7 +493,7 @@ def test_packed_runs_per_block_diagonal(L, M, seed, shift):
     runs = {D: m for D, m in modes.items() if m[0] == "runs"}
     assert runs and all(m[2] > 1 for m in runs.values())
     say(f"packed runs L={L} M={M} seed={seed} shift={shift} {sorted(runs.items())}")
-    _, cost, dec = solve_on_gpu(p, M, schedule="blocked")
+    _, cost, dec = solve_on_gpu(p, M, schedule=edges)
     assert_same(p, M, cost, dec)
 
 
@@ -511,7 +517,8 @@ def test_value_path_per_block_diagonal(shift, schedule):
 
 
 @pytest.mark.parametrize("v0", [32752, 32766, 32767, 32768, 33600])
-def test_two_byte_copy_of_the_diagonal_blocks_at_its_limit(v0):
+@pytest.mark.parametrize("edges", EDGE_ORDERS)
+def test_two_byte_copy_of_the_diagonal_blocks_at_its_limit(v0, edges):
     # The edges read the diagonal blocks' cells from a 2-byte copy when their
     # bound V_0 (largest over the 16-stage blocks) is at most 2^15 - 2, else
     # from the 4-byte copy.  Here u_f = 200, w_a = 1, w_abar = 2 on every
@@ -529,7 +536,7 @@ def test_two_byte_copy_of_the_diagonal_blocks_at_its_limit(v0):
     finite = C[block_cells][C[block_cells] != np.iinfo(np.int64).max]
     assert finite.max() == v0
     say(f"two-byte diagonal blocks V_0={v0}")
-    _, cost, dec = solve_on_gpu(p, M, schedule="blocked")
+    _, cost, dec = solve_on_gpu(p, M, schedule=edges)
     assert_same(p, M, cost, dec)
 
 
@@ -549,7 +556,8 @@ def test_batch_mixing_value_paths(schedule):
         assert_same(params, M, cost, dec, c)
 
 
-def test_batch_mixing_middle_paths():
+@pytest.mark.parametrize("edges", EDGE_ORDERS)
+def test_batch_mixing_middle_paths(edges):
     # One blocked fill whose chains take different middle paths in the same
     # launches: packed keys and packed runs, packed keys only, packed keys
     # with (value, split) pairs and 64-bit keys, 64-bit keys only.
@@ -560,7 +568,7 @@ def test_batch_mixing_middle_paths():
              for c in range(len(shifts))]
     assert kinds == [{"packed", "runs"}, {"packed"}, {"packed", "pairs", "wide"}, {"wide"}]
     say(f"batch mixing middle paths L={L} M={M} {kinds}")
-    _, cost, dec = solve_on_gpu(p, M, schedule="blocked")
+    _, cost, dec = solve_on_gpu(p, M, schedule=edges)
     for c in range(len(shifts)):
         assert_same(p, M, cost, dec, c)
 
