@@ -113,7 +113,7 @@ def cpu_baseline(params, M, stages=None):
 def arithmetic_type(params):
     """The integer types the fill computes in.  The library takes uint32 with
     saturation for the pairs whose block-diagonal of 16-stage blocks has a cost
-    bound below 2^30 (the bound of a sub-chain [s, t] is
+    bound below 2^32 - 1 (the bound of a sub-chain [s, t] is
     sum_{j=s}^{t} (t - j + 1) u_f^j + sum_{j=s}^{t} u_b^j, and it grows with the
     sub-chain), int64 for the others: "u32" when that holds for the whole
     chain, "int64" when not even for one block, else "u32+int64"."""
@@ -126,9 +126,10 @@ def arithmetic_type(params):
     L = p.shape[-1]
     whole = max(bound(c, 0, L) for c in p)
     block = max(bound(c, b, min(b + 16, L)) for c in p for b in range(0, L, 16))
-    if whole < (1 << 30):
+    narrow = (1 << 32) - 1
+    if whole < narrow:
         return "u32"
-    return "int64" if block >= (1 << 30) else "u32+int64"
+    return "int64" if block >= narrow else "u32+int64"
 
 
 def kernel_code_digest(path=None):

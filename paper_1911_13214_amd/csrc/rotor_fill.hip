@@ -18,11 +18,12 @@
 // 16 x 16 blocks of block-diagonal D (D = 0: within one block), bounds every
 // pair of the block-diagonal and grows with D; a pair's operands are
 // sub-chains of it, of block-diagonals up to its own.
-//  - narrow, when V_D < 2^30: operands are read from a compact uint32 copy of
-//    the table (INT64_MAX stored as 0xFFFFFFFF), which the pairs of narrow
-//    block-diagonals write, and added with unsigned saturation; the best
-//    value and its split are kept side by side and splits are visited in
-//    increasing s' with a strict <;
+//  - narrow, when V_D < 2^32 - 1: operands are read from a compact uint32
+//    copy of the table (INT64_MAX stored as 0xFFFFFFFF), which the pairs of
+//    narrow block-diagonals write, and added with unsigned saturation (a
+//    finite candidate is at most V_D, below the infinity, so no finite sum
+//    saturates); the best value and its split are kept side by side and
+//    splits are visited in increasing s' with a strict <;
 //  - packed (middle products of narrow block-diagonals, when (V_D + 1) << S
 //    fits below 2^32 - 1 for the S bits of the block's middle split range):
 //    a candidate is one uint32 key (value << S) | (s' - first middle split),
@@ -89,7 +90,7 @@ constexpr int kStreamBelowBudgets = 64;
 constexpr int kSplitMinD = 16;  // streamed diagonals from this length spread their splits over four waves
 constexpr uint32_t kAllSplit = 0xFFFF;  // split field of a C_2 candidate
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
-constexpr uint64_t kNarrowBound = 1ull << 30;
+constexpr uint64_t kNarrowBound = 0xFFFFFFFFull;  // V_D below: the narrow path
 
 // The parameters of one chain as given (stage l at index l-1).
 struct ChainParams {
@@ -153,7 +154,7 @@ struct ChainWork {
     const int32_t *gall;   // [rows] m_all(s, t)
     uint32_t *shadow;      // [rows][pitch] compact copy of the costs (narrow block-diagonals)
     const int32_t *pbits;  // [nb] per block-diagonal D: the largest S with (V_D + 1) << S <= 2^32 - 1,
-                           // or -1 if V_D >= 2^30 (64-bit path)
+                           // or -1 if V_D >= 2^32 - 1 (64-bit path)
     int16_t *half;         // [16 L][hpitch] 2-byte copy of the diagonal blocks' cells
     int64_t hpitch;
     // whether the pairs of block-diagonal D take the narrow path
@@ -422,7 +423,7 @@ __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ pa
                 const int x = I * kT, yb = I + D + 1, y = min(yb * kT, L);
                 vmax = max(vmax, ppb[yb] - ppb[I] - (int64_t)(y - x) * pre[x] + bb[yb] - bb[I]);
             }
-            // (V_D + 1) << S <= 2^32 - 1 leaves S >= 2 bits on the narrow path
+            // (V_D + 1) << S <= 2^32 - 1 leaves S >= 0 bits on the narrow path
             int bits = (uint64_t)vmax < kNarrowBound
                            ? 63 - __clzll((long long)(0xFFFFFFFFull / ((uint64_t)vmax + 1)))
                            : -1;

@@ -26,7 +26,7 @@ struct Tables {
 // m_none and m_all of every pair, a domain status word per chain, the sizes
 // by which operand budgets are shifted (clamped, see prep_kernel), a compact
 // uint32 copy of the cost table (written and read by the pairs whose costs
-// stay below 2^30), and a 2-byte copy of the cells of the diagonal blocks
+// stay below 2^32 - 1), and a 2-byte copy of the cells of the diagonal blocks
 // (chains whose costs there stay below 2^15).
 struct Work {
     int64_t *pre;      // [n_chains][L + 1]

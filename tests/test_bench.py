@@ -41,17 +41,17 @@ def test_arithmetic_type_follows_the_cost_bound():
     p = chaingen.random_chains(1, 500, seed=5, wa_hi=20)
     p[:, chaingen.UF] <<= 10
     p[:, chaingen.UB] <<= 10
-    # the whole chain's bound is past 2^30, the bounds of single blocks are not
+    # the whole chain's bound is past 2^32 - 1, the bounds of single blocks are not
     assert bench.arithmetic_type(p) == "u32+int64"
-    p[:, chaingen.UF] <<= 12
-    p[:, chaingen.UB] <<= 12
+    p[:, chaingen.UF] <<= 14
+    p[:, chaingen.UB] <<= 14
     assert bench.arithmetic_type(p) == "int64"
-    # the bound sum_l P[l] + sum u_b just below and at 2^30
+    # the bound sum_l P[l] + sum u_b just below and at 2^32 - 1
     L = 4
     p = np.zeros((1, 6, L), dtype=np.int64)
-    p[0, chaingen.UF, 0] = ((1 << 30) - 1) // L
+    p[0, chaingen.UF, 0] = ((1 << 32) - 2) // L
     assert bench.arithmetic_type(p) == "u32"
-    p[0, chaingen.UB, 0] = (1 << 30) - L * p[0, chaingen.UF, 0]
+    p[0, chaingen.UB, 0] = (1 << 32) - 1 - L * p[0, chaingen.UF, 0]
     assert bench.arithmetic_type(p) == "int64"
 
 

@@ -27,7 +27,7 @@ def fuzz_stage(rng, kind):
         return u(0, 50), u(0, 100), u(0, 1) * u(0, 8), u(0, 12), u(0, 1) * u(0, 5), u(0, 1) * u(0, 5)
     if kind == "large":
         return u(1, 1000), u(1, 2000), u(1, 90), u(1, 200), u(0, 40), u(0, 40)
-    # wide: costs near 2^22 times the usual range push the cost bound past 2^30
+    # wide: costs near 2^22 times the usual range push the cost bound past 2^32
     return u(1, 100) << 22, u(1, 200) << 22, u(1, 10), u(1, 30), u(0, 3), u(0, 3)
 
 

@@ -370,6 +370,10 @@ def test_timed_solve_matches_and_counts_the_work(cfg):
     assert stats["prep"]["launches"] == 1
 
 
+# the narrow (4-byte) value path takes block-diagonals whose cost bound is below this
+NARROW_BOUND = (1 << 32) - 1
+
+
 def cost_bound(p):
     """sum_l P[l] + sum u_b = sum_j (L - j + 1) u_f^j + sum u_b: no stage runs
     forward more often than the stages after it plus one, so every finite cost
@@ -385,10 +389,10 @@ def scaled_chain(seed, L, shift):
 
 
 def wide_costs_chain(seed, L):
-    """A chain whose cost bound exceeds 2^30, so the solver takes its 64-bit
-    value path."""
+    """A chain whose cost bound exceeds 2^32 - 2, so the solver takes its
+    64-bit value path."""
     p = scaled_chain(seed, L, 22)
-    assert cost_bound(p[0]) >= 1 << 30
+    assert cost_bound(p[0]) >= NARROW_BOUND
     return p
 
 
@@ -464,7 +468,7 @@ def middle_modes(p, L, M, n_chains):
     out = {}
     for D in range(1, nb):
         n = 16 * (D - 1)  # last split minus first
-        if vd[D] >= 1 << 30:
+        if vd[D] >= NARROW_BOUND:
             out[D] = "wide"
             continue
         wgs = (M + 64) // 64 * (nb - D) * n_chains
@@ -498,9 +502,9 @@ def test_packed_runs_per_block_diagonal(L, M, seed, shift, edges):
 
 
 @pytest.mark.parametrize("schedule", SCHEDULES)
-@pytest.mark.parametrize("shift", [11, 12, 14, 16])
+@pytest.mark.parametrize("shift", [13, 14, 16, 18])
 def test_value_path_per_block_diagonal(shift, schedule):
-    # A chain whose cost bound is past 2^30 while the bounds of its shorter
+    # A chain whose cost bound is past 2^32 - 2 while the bounds of its shorter
     # sub-chains are not: the pairs of the first block-diagonals take the
     # 4-byte path (compact copy, saturating adds), the later ones the 64-bit
     # keys, in both fill orders.
@@ -509,8 +513,8 @@ def test_value_path_per_block_diagonal(shift, schedule):
     nb = (L + 15) // 16
     vd = {0: max(cost_bound(p[0][:, 16 * I:min(16 * (I + 1), L)]) for I in range(nb))}
     vd.update(block_diagonal_bounds(p[0], L))
-    narrow = [D for D in range(nb) if vd[D] < 1 << 30]
-    assert cost_bound(p[0]) >= 1 << 30 and narrow == list(range(len(narrow))) and 0 < len(narrow) < nb
+    narrow = [D for D in range(nb) if vd[D] < NARROW_BOUND]
+    assert cost_bound(p[0]) >= NARROW_BOUND and narrow == list(range(len(narrow))) and 0 < len(narrow) < nb
     say(f"value path per block-diagonal shift={shift} narrow={narrow} {schedule}")
     _, cost, dec = solve_on_gpu(p, M, schedule=schedule)
     assert_same(p, M, cost, dec)
@@ -549,7 +553,7 @@ def test_batch_mixing_value_paths(schedule):
         params[c, 1] *= 1 << 22
     params[2, 0] *= 1 << 13
     params[2, 1] *= 1 << 13
-    assert cost_bound(params[1]) >= 1 << 30 and (1 << 27) < cost_bound(params[2]) < (1 << 30)
+    assert cost_bound(params[1]) >= NARROW_BOUND and (1 << 27) < cost_bound(params[2]) < NARROW_BOUND
     M = 200
     _, cost, dec = solve_on_gpu(params, M, schedule=schedule)
     for c in range(6):
@@ -562,7 +566,7 @@ def test_batch_mixing_middle_paths(edges):
     # launches: packed keys and packed runs, packed keys only, packed keys
     # with (value, split) pairs and 64-bit keys, 64-bit keys only.
     L, M = 200, 240
-    shifts = (5, 0, 12, 22)
+    shifts = (5, 0, 14, 22)
     p = np.concatenate([scaled_chain(30 + i, L, sh) for i, sh in enumerate(shifts)])
     kinds = [{m if isinstance(m, str) else m[0] for m in middle_modes(p[c], L, M, len(shifts)).values()}
              for c in range(len(shifts))]
