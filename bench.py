@@ -36,7 +36,10 @@ HBM_PEAK_GBS = 8000.0
 # cycles on each), at 2.4 GHz: 614.4 G wave-instructions/s (39.3 T
 # lane-instructions/s).
 VALU_PEAK_GWIS = 256 * 2.4
-FILL_SOURCE = os.path.join(ROOT, "paper_1911_13214_amd", "csrc", "rotor_fill.hip")
+CSRC = os.path.join(ROOT, "paper_1911_13214_amd", "csrc")
+# the sources of the fill kernels, whose digest the counter records carry
+FILL_SOURCES = [os.path.join(CSRC, f) for f in ("rotor_paths.h", "rotor_fill.hip", "rotor_rows.h", "rotor_rows_0.hip",
+                                                "rotor_rows_1.hip", "rotor_rows_2.hip", "rotor_rows_3.hip")]
 
 
 def log(*a):
@@ -133,9 +136,10 @@ def arithmetic_type(params):
 
 
 def kernel_code_digest(path=None):
-    """sha256 of the fill kernels' source with comments and whitespace
-    removed: it changes when the code changes, not when a comment does."""
-    text = open(path or FILL_SOURCE).read()
+    """sha256 of the fill kernels' sources (or of the file `path`) with
+    comments and whitespace removed: it changes when the code changes, not
+    when a comment does."""
+    text = "\n".join(open(p).read() for p in ([path] if path else FILL_SOURCES))
     text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
     text = re.sub(r"//[^\n]*", " ", text)
     return hashlib.sha256("".join(text.split()).encode()).hexdigest()

@@ -11,7 +11,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "librotor.so")
-SOURCES = ["rotor_host.cpp", "rotor_api.cpp", "rotor_plan.cpp", "rotor_fill.hip", "rotor_reconstruct.hip", "rotor_noalloc.hip"]
+SOURCES = ["rotor_host.cpp", "rotor_api.cpp", "rotor_plan.cpp", "rotor_fill.hip", "rotor_rows_0.hip",
+           "rotor_rows_1.hip", "rotor_rows_2.hip", "rotor_rows_3.hip", "rotor_reconstruct.hip", "rotor_noalloc.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -28,9 +29,28 @@ FLAGS = [
 
 
 def build(verbose: bool = False) -> str:
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
+    """Compile every source to an object (in parallel: the fill kernels take
+    minutes), then link the shared library."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    objdir = os.path.join(PKG, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    compile_flags = [f for f in FLAGS if f != "-shared"]
+
+    def compile_one(src):
+        obj = os.path.join(objdir, os.path.splitext(src)[0] + ".o")
+        cmd = [HIPCC, *compile_flags, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, src), "-o", obj]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        subprocess.check_call(cmd)
+        return obj
+
+    # longest first
+    order = sorted(SOURCES, key=lambda f: -os.path.getsize(os.path.join(CSRC, f)))
+    with ThreadPoolExecutor(max_workers=min(len(order), os.cpu_count() or 1)) as ex:
+        objs = dict(zip(order, ex.map(compile_one, order)))
     tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-I", INCLUDE, "-I", CSRC, *srcs, "-o", tmp]
+    cmd = [HIPCC, *FLAGS, *[objs[s] for s in SOURCES], "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)

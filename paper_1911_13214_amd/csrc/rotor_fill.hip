@@ -61,23 +61,11 @@
 // finished by the middle kernels.  A small table is instead filled in the
 // streamed order: one launch per diagonal d over all its pairs (diag_kernel,
 // or diag_split_kernel with the splits of a pair spread over four waves).
-#include <utility>
-
-#include "rotor_internal.h"
+#include "rotor_paths.h"
 
 namespace rotor {
 namespace {
 
-constexpr int64_t kInf = INT64_MAX;
-constexpr int kT = kBlock;  // block side, in stages
-constexpr int kSub = 8;  // per-wave register tile side
-// An edge workgroup is one wave holding kEdgeBudgets budgets per lane, 64
-// apart: 128 consecutive budgets, whose loads it issues together (measured on
-// MI355X at L = 500, M = 5000, against one budget per lane in 128-thread
-// workgroups: edges 13.70 -> 13.24 ms; 128-thread workgroups of two budgets
-// per lane 13.53 ms, three or four budgets per lane 14.0-14.4 ms).
-constexpr int kEdgeThreads = 64;
-constexpr int kEdgeBudgets = 2;
 // The automatic schedule fills small tables diagonal by diagonal: measured on
 // MI355X, that is faster up to about 2e9 split candidates for one chain
 // (L = 250 at M = 500) and 4e8 for a batch, whose blocked launches are wider,
@@ -88,237 +76,6 @@ constexpr uint64_t kStreamMaxCandidates1 = 2000000000ull;
 constexpr uint64_t kStreamMaxCandidatesN = 400000000ull;
 constexpr int kStreamBelowBudgets = 64;
 constexpr int kSplitMinD = 16;  // streamed diagonals from this length spread their splits over four waves
-constexpr uint32_t kAllSplit = 0xFFFF;  // split field of a C_2 candidate
-constexpr uint32_t kInf32 = 0xFFFFFFFFu;
-constexpr uint64_t kNarrowBound = 0xFFFFFFFFull;  // V_D below: the narrow path
-
-// The parameters of one chain as given (stage l at index l-1).
-struct ChainParams {
-    const int64_t *uf, *ub, *wa, *wabar, *of, *ob;
-};
-
-__device__ inline ChainParams chain_params(const int64_t *__restrict__ params, int L, int c)
-{
-    const int64_t *p = params + (int64_t)c * ROTOR_N_ROWS * L;
-    return {p + ROTOR_ROW_UF * L, p + ROTOR_ROW_UB * L, p + ROTOR_ROW_WA * L,
-            p + ROTOR_ROW_WABAR * L, p + ROTOR_ROW_OF * L, p + ROTOR_ROW_OB * L};
-}
-
-// What the fill kernels read of a chain: the times as given and the two
-// sizes that shift operand budgets, w_a and w_abar, as prep_kernel clamped
-// them into [0, M + 1] (stage l at index l-1).  In the domain the clamp
-// changes nothing the recurrence sees (a shift beyond M puts every operand
-// out of reach either way); outside it, every shifted budget m - w stays
-// within [m - M - 1, m], so an operand is only ever loaded at a budget in
-// [0, M], whatever the parameter values.
-// The sizes are read through the constant address space: written by an
-// earlier kernel and read-only during the fill, they then take scalar loads
-// like the parameters, which the compiler could not assume for a workspace
-// pointer the kernel also writes through.
-typedef const __attribute__((address_space(4))) int32_t *const_i32;
-typedef const __attribute__((address_space(4))) int64_t *const_i64;
-struct ChainRows {
-    const int64_t *uf, *ub;
-    const_i32 wa, wabar;
-};
-
-__device__ inline ChainRows chain_rows(const int64_t *__restrict__ params, const Work &w, int L, int c)
-{
-    const int64_t *p = params + (int64_t)c * ROTOR_N_ROWS * L;
-    const_i32 sh = (const_i32)(w.shift + (int64_t)c * 2 * L);
-    return {p + ROTOR_ROW_UF * L, p + ROTOR_ROW_UB * L, sh, sh + L};
-}
-
-typedef const __attribute__((address_space(1))) int64_t *global_c64;
-typedef const __attribute__((address_space(1))) uint32_t *global_c32;
-typedef __attribute__((address_space(1))) uint64_t *global_u64;
-
-// Load budget m of a table row: global address space, 32-bit byte offset
-// (M < 2^28).
-__device__ inline int64_t load64(const int64_t *row, int m)
-{
-    return *(global_c64)((const char *)row + (uint32_t)m * 8u);
-}
-__device__ inline uint32_t load32(const uint32_t *row, int m)
-{
-    return *(global_c32)((const char *)row + (uint32_t)m * 4u);
-}
-
-__device__ inline uint32_t sat_add(uint32_t a, uint32_t b) { return __builtin_elementwise_add_sat(a, b); }
-__device__ inline uint64_t umin(uint64_t a, uint64_t b) { return b < a ? b : a; }
-
-// Per-chain views of the workspace.
-struct ChainWork {
-    const int64_t *pre;    // [L+1] prefix sums of u_f
-    const int32_t *gnone;  // [rows] m_none(s, t), t > s
-    const int32_t *gall;   // [rows] m_all(s, t)
-    uint32_t *shadow;      // [rows][pitch] compact copy of the costs (narrow block-diagonals)
-    const int32_t *pbits;  // [nb] per block-diagonal D: the largest S with (V_D + 1) << S <= 2^32 - 1,
-                           // or -1 if V_D >= 2^32 - 1 (64-bit path)
-    int16_t *half;         // [16 L][hpitch] 2-byte copy of the diagonal blocks' cells
-    int64_t hpitch;
-    // whether the pairs of block-diagonal D take the narrow path
-    __device__ bool narrow(int D) const { return pbits[D] >= 0; }
-    // whether the diagonal blocks' costs fit the 2-byte copy: (V_0 + 1) << 17
-    // <= 2^32 - 1, i.e. V_0 <= 2^15 - 2, so finite values stay positive as
-    // int16 and infinity is stored as -1 (0xFFFF)
-    __device__ bool diag16() const { return pbits[0] >= 17; }
-    // row of the pair (s, t) of a diagonal block in the 2-byte copy:
-    // 16 (s - 1) + (t - 1) mod 16
-    __device__ int16_t *half_row(int s, int t) const
-    {
-        return half + ((int64_t)(s - 1) * kT + (t - 1) % kT) * hpitch;
-    }
-};
-
-// Block-diagonal of the pair (s, t): D = J - I for s in block I, t in block J.
-__device__ inline int block_diag(int s, int t) { return (t - 1) / kT - (s - 1) / kT; }
-
-__device__ inline ChainWork chain_work(const Work &w, int L, int64_t rows, int64_t pitch, int c)
-{
-    ChainWork cw;
-    cw.pre = w.pre + (int64_t)c * (L + 1);
-    cw.gnone = w.gnone + (int64_t)c * rows;
-    cw.gall = w.gall + (int64_t)c * rows;
-    cw.shadow = w.shadow + (int64_t)c * rows * pitch;
-    cw.pbits = w.pbits + (int64_t)c * ((L + kT - 1) / kT);
-    cw.hpitch = half_pitch_of(pitch);
-    cw.half = w.half + (int64_t)c * L * kT * cw.hpitch;
-    return cw;
-}
-
-// ---------------------------------------------------------------------------
-// Value paths.  X is the left operand with its u_f prefix, Y the shifted
-// right operand; relax() folds one candidate into an accumulator.
-
-// A stored cost shifted into the value field of a wide key.
-__device__ inline uint64_t key_of(int64_t v)
-{
-    const uint64_t t = (uint64_t)v << 16;
-    const uint32_t hi = min((uint32_t)(t >> 32), 1u << 30);
-    return ((uint64_t)hi << 32) | (uint32_t)t;
-}
-
-struct Wide {
-    typedef int64_t Raw;
-    typedef uint64_t X;
-    typedef uint64_t Y;
-    struct Acc {
-        uint64_t key;
-    };
-    static constexpr bool kShadow = false;
-    static constexpr uint64_t kShiftedOut = 1ull << 62;
-    static constexpr int kBytes = 8;  // bytes per cell of the table it reads
-    __device__ static const char *table(const int64_t *tab, const uint32_t *) { return (const char *)tab; }
-    __device__ static Raw load_at(const char *row, int m) { return *(global_c64)(row + (uint32_t)m * 8u); }
-    __device__ static Raw load(const int64_t *crow, const uint32_t *, int m) { return load64(crow, m); }
-    __device__ static void init(Acc &a) { a.key = ~0ull; }
-    // ok = false: the budget of Y was shifted below 0, the candidate is infinite
-    __device__ static X xop(Raw x, uint64_t prefix, uint32_t sp, bool ok)
-    {
-        return key_of(x) + (ok ? ((prefix << 16) | sp) : kShiftedOut);
-    }
-    __device__ static Y yop(Raw y) { return key_of(y); }
-    __device__ static void relax(Acc &a, X x, Y y, uint32_t) { a.key = umin(a.key, x + y); }
-    // the stored middle partial counts u_f from the first middle split on
-    __device__ static void merge_stored(Acc &a, int64_t stored, uint64_t prefix)
-    {
-        a.key = umin(a.key, (uint64_t)stored + (prefix << 16));
-    }
-    __device__ static void relax_all(Acc &a, Raw y, uint64_t ufub)
-    {
-        a.key = umin(a.key, key_of(y) + ((ufub << 16) | kAllSplit));
-    }
-    __device__ static int64_t stored(const Acc &a) { return (int64_t)a.key; }
-    // fold in the stored() form of a result over larger splits
-    __device__ static void merge_later(Acc &a, int64_t later) { a.key = umin(a.key, (uint64_t)later); }
-    __device__ static bool finite(const Acc &a) { return a.key < (1ull << 62); }
-    __device__ static int64_t value(const Acc &a) { return (int64_t)(a.key >> 16); }
-    __device__ static uint32_t split(const Acc &a) { return (uint32_t)(a.key & 0xFFFF); }
-};
-
-struct Narrow {
-    typedef uint32_t Raw;
-    typedef uint32_t X;
-    typedef uint32_t Y;
-    struct Acc {
-        uint32_t val;
-        uint32_t sp;
-    };
-    static constexpr bool kShadow = true;
-    static constexpr int kBytes = 4;
-    __device__ static const char *table(const int64_t *, const uint32_t *shadow) { return (const char *)shadow; }
-    __device__ static Raw load_at(const char *row, int m) { return *(global_c32)(row + (uint32_t)m * 4u); }
-    __device__ static Raw load(const int64_t *, const uint32_t *srow, int m) { return load32(srow, m); }
-    __device__ static void init(Acc &a)
-    {
-        a.val = kInf32;
-        a.sp = 0;
-    }
-    __device__ static X xop(Raw x, uint64_t prefix, uint32_t, bool ok)
-    {
-        return sat_add(x, ok ? (uint32_t)prefix : kInf32);
-    }
-    __device__ static Y yop(Raw y) { return y; }
-    // splits are visited in increasing s': a strict < keeps the smallest
-    __device__ static void relax(Acc &a, X x, Y y, uint32_t sp)
-    {
-        const uint32_t v = sat_add(x, y);
-        const bool b = v < a.val;
-        a.val = b ? v : a.val;
-        a.sp = b ? sp : a.sp;
-    }
-    __device__ static void merge_stored(Acc &a, int64_t stored, uint64_t prefix)
-    {
-        const uint32_t v = sat_add((uint32_t)((uint64_t)stored >> 32), (uint32_t)prefix);
-        const bool b = v < a.val;
-        a.val = b ? v : a.val;
-        a.sp = b ? (uint32_t)stored : a.sp;
-    }
-    __device__ static void relax_all(Acc &a, Raw y, uint64_t ufub)
-    {
-        const uint32_t v = sat_add(y, (uint32_t)ufub);
-        const bool b = v < a.val;
-        a.val = b ? v : a.val;
-        a.sp = b ? kAllSplit : a.sp;
-    }
-    __device__ static int64_t stored(const Acc &a) { return (int64_t)(((uint64_t)a.val << 32) | a.sp); }
-    // fold in the stored() form of a result over larger splits: strict <
-    __device__ static void merge_later(Acc &a, int64_t later)
-    {
-        const uint32_t v = (uint32_t)((uint64_t)later >> 32);
-        const bool b = v < a.val;
-        a.val = b ? v : a.val;
-        a.sp = b ? (uint32_t)later : a.sp;
-    }
-    __device__ static bool finite(const Acc &a) { return a.val != kInf32; }
-    __device__ static int64_t value(const Acc &a) { return (int64_t)a.val; }
-    __device__ static uint32_t split(const Acc &a) { return a.sp; }
-};
-
-// Final cost and decision of a cell, and its compact copy on the narrow path.
-// idx is relative to the chain's tables.  On the narrow path the fill never
-// reads the int64 cost or the decision of a finished cell back, so they are
-// stored non-temporally and leave the caches to the operands (measured on
-// MI355X: 25.4 -> 24.7 ms at L = 500, M = 5000); the 64-bit path reads its
-// cells as operands and stores them normally.
-template <class P>
-__device__ inline void store_cell(int64_t *cost, int16_t *dec, uint32_t *shadow, int64_t idx,
-                                  const typename P::Acc &a)
-{
-    const bool fin = P::finite(a);
-    const uint32_t sp = P::split(a);
-    const int64_t v = fin ? P::value(a) : kInf;
-    const int16_t d = fin ? (sp == kAllSplit ? (int16_t)0 : (int16_t)sp) : (int16_t)-1;
-    if constexpr (P::kShadow) {
-        __builtin_nontemporal_store(v, &cost[idx]);
-        __builtin_nontemporal_store(d, &dec[idx]);
-        shadow[idx] = fin ? (uint32_t)v : kInf32;
-    } else {
-        cost[idx] = v;
-        dec[idx] = d;
-    }
-}
 
 // ---------------------------------------------------------------------------
 
@@ -633,20 +390,6 @@ __device__ __forceinline__ void relax_run_nb(typename P::Acc (&acc)[NB], const C
         RelaxRunNB<P, kRun, NB>::go(n < kRun ? n : kRun, acc, r, m, k0, cur, prefix);
 }
 
-// Operand loads of the narrow path from the compact copy (4 bytes) or from
-// the 2-byte copy of the diagonal blocks (a sign-extending load: finite
-// values there are below 2^15, and the infinity 0xFFFF becomes 0xFFFFFFFF).
-typedef const __attribute__((address_space(1))) int16_t *global_c16;
-struct Load32 {
-    __device__ static uint32_t at(const char *row, int m) { return *(global_c32)(row + (uint32_t)m * 4u); }
-};
-struct Load16 {
-    __device__ static uint32_t at(const char *row, int m)
-    {
-        return (uint32_t)(int32_t) * (global_c16)(row + (uint32_t)m * 2u);
-    }
-};
-
 // Cursor of a narrow run whose X and Y rows come from different copies: X
 // moves xstep bytes per split, Y ystep bytes, and ystep shrinks by ydec.
 struct MixedCursor {
@@ -907,24 +650,6 @@ __global__ __launch_bounds__(256) void diag_split_kernel(const int64_t *__restri
         diag_split_body<Narrow>(r, cw, L, M, m, pitch, s, t, wave, part, tab, dtab);
     else
         diag_split_body<Wide>(r, cw, L, M, m, pitch, s, t, wave, part, tab, dtab);
-}
-
-// Whether the middle products of block-diagonal D of a chain, whose middle
-// split range has span + 1 splits, use packed keys.
-__device__ inline bool middle_packed(const ChainWork &cw, int D, int span)
-{
-    const int S = span > 0 ? 32 - __clz(span) : 0;
-    return cw.narrow(D) && S <= cw.pbits[D];
-}
-
-// A narrow block-diagonal whose middle range is too wide for one packed key
-// takes packed runs of 2^pbits[D] splits instead (middle_packed_kernel), if
-// runs are 128 splits or more; each run's result goes to the cost table as
-// (value << 32) | s', the form middle_kernel stores.
-constexpr int kMinRunBits = 7;
-__device__ inline bool middle_runs(const ChainWork &cw, int D, int span)
-{
-    return cw.narrow(D) && !middle_packed(cw, D, span) && cw.pbits[D] >= kMinRunBits;
 }
 
 // Middle splits of every block (I, I + D) of one block-diagonal.  A workgroup
@@ -1553,292 +1278,7 @@ __global__ __launch_bounds__(kEdgeThreads) void edge_kernel(const int64_t *__res
         edge_body<Narrow, false>(r, cw, L, M, m0, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
 }
 
-// ---------------------------------------------------------------------------
-// Edges by rows.  The edge splits of a cell (s, t) of block (I, J) read, for
-// a low split k, X(s, k) in the diagonal block I (the same for every cell of
-// row s) and Y(k + 1, t) further down column t of the block; for a high split
-// k, X(s, k) further left in row s of the block and Y(k + 1, t) in the
-// diagonal block J.  Row s therefore needs only the rows below it and its
-// own cells to the left, at the same budget: one launch per row, bottom-up
-// (a = 16(I + 1) - s low splits, the same in every block of the
-// block-diagonal), and one workgroup walks a block's row at its budgets from
-// left to right, keeping the finished cells of the row, with their u_f
-// prefix, in registers as the X operands of the high splits, and the row's
-// diagonal-block operands X(s, k) of the low splits loaded once for all 16
-// cells.  Each candidate then streams one operand: a 4-byte cell of the
-// block for a low split, a 2-byte diagonal-block cell for a high one, about
-// half the bytes of the anti-diagonal rounds, in 16 launches instead of 30.
-// But a wave walks 16 cells in turn, with at most about 45 loads in flight,
-// and a launch has 16 times fewer waves than a round: the rows pay off only
-// when a launch holds many blocks (a batch of chains), and the
-// anti-diagonal rounds take the others.  Measured on MI355X: the batch of
-// 256 chains of L = 64, M = 640 (768 blocks in the first launch) edges 4.89
-// -> 4.41 ms; the single chain of L = 500, M = 5000 (31 blocks or fewer)
-// 12.9 -> 16.2 ms if it took them.
-constexpr int kRowBudgets = 1;  // budgets per lane, 64 apart (two spill registers)
-constexpr int kRowMinBlocks = 256;  // blocks of all chains in one launch
-constexpr int kRowAhead = 1;  // cells whose loads are in flight ahead of the one relaxed
-
-// f(std::integral_constant<int, i>) for each i of the sequence, in order
-template <class F, int... Is>
-__device__ __forceinline__ void static_for(F &&f, std::integer_sequence<int, Is...>)
-{
-    (f(std::integral_constant<int, Is>{}), ...);
-}
-
-// A cell of a diagonal block as the value path reads it: from the 2-byte
-// copy with H, else from the table the path reads.
-template <class P, bool H>
-__device__ __forceinline__ typename P::Raw diag_load(const ChainWork &cw, const int64_t *tab, int L, int64_t pitch,
-                                                     int s, int t, int m)
-{
-    if constexpr (H) {
-        return Load16::at((const char *)cw.half_row(s, t), m);
-    } else {
-        const int64_t o = row_of(L, s, t) * pitch;
-        return P::load(tab + o, cw.shadow + o, m);
-    }
-}
-
-// A finished cell's cost in the form the path loads it (infinity included).
-template <class P>
-__device__ __forceinline__ typename P::Raw final_raw(const typename P::Acc &a)
-{
-    if constexpr (P::kShadow)
-        return a.val;
-    else
-        return P::finite(a) ? P::value(a) : kInf;
-}
-
-// Row s = k_lo - A of block (I, J) at the lane's budgets, cells
-// t_first .. t_last (the corner, when the middle kernel finished it, is
-// only read).  Splits are met in increasing order: low, the stored middle
-// partial, high.  The row's scalars (shift sizes, prefix sums, gates) are
-// loaded first, all at once; then the loads of cell j + kRowAhead are
-// issued before cell j is relaxed and stored, in one straight-line body
-// (columns past L read the last column and store nothing).  Scheduling
-// barriers keep that order: a load may not pass an earlier store to the
-// same table, and hoisting more loads would hold the whole row's operands
-// in registers.
-template <class P, bool H, bool PP, int A>
-__device__ __forceinline__ void row_body(const ChainRows &r, const ChainWork &cw, int L, int M, int m0, int64_t pitch,
-                                         int s, int J, int t_first, int t_last, int64_t *tab, int16_t *dtab)
-{
-    constexpr int NB = kRowBudgets;
-    const int k_lo = s + A;  // 16(I + 1)
-    const int k_hi = J * kT;
-    // the lane's budgets m0 + b * 64; those past M load budget M and store nothing
-    int m[NB];
-#pragma unroll
-    for (int b = 0; b < NB; ++b)
-        m[b] = min(m0 + b * kEdgeThreads, M);
-    // prefix sums and gates through the constant address space (written by
-    // prep_kernel, read-only here): scalar loads
-    const const_i64 pre = (const_i64)cw.pre;
-    const const_i32 gall_c = (const_i32)cw.gall, gnone_c = (const_i32)cw.gnone;
-    const int64_t pre_s = pre[s - 1];
-    // per low split k = s + i: w_a^k and the u_f prefix from s to k; per
-    // column j (t = min(k_hi + 1 + j, L)): w_a^t, the prefix to t, the gates
-    int w_lo[A > 0 ? A : 1];
-    uint64_t p_lo[A > 0 ? A : 1];
-#pragma unroll
-    for (int i = 0; i < A; ++i) {
-        w_lo[i] = r.wa[s + i - 1];
-        p_lo[i] = (uint64_t)(pre[s + i] - pre_s);
-    }
-    int w_t[kT];
-    uint64_t p_t[kT];
-    int32_t g_all[kT], g_none[kT];
-#pragma unroll
-    for (int j = 0; j < kT; ++j) {
-        const int t = min(k_hi + 1 + j, L);
-        w_t[j] = r.wa[t - 1];
-        p_t[j] = (uint64_t)(pre[t] - pre_s);
-        const int64_t crow = row_of(L, s, t);
-        g_all[j] = gall_c[crow];
-        g_none[j] = gnone_c[crow];
-    }
-    // the stored middle partial counts u_f from k_lo on
-    const uint64_t pre_lo = (uint64_t)(pre[k_lo - 1] - pre_s);
-    const int wab = r.wabar[s - 1];
-    const uint64_t ufub = (uint64_t)(r.uf[s - 1] + r.ub[s - 1]);
-    // PP: the middle partial is a packed key in the compact copy (else
-    // (value << 32) | s' or a 64-bit key in the cost table)
-    const int S = k_hi > k_lo ? 32 - __clz(k_hi - k_lo) : 0;
-    // X of the low splits k = s .. k_lo - 1, with the u_f prefix from s
-    typename P::X xl[A > 0 ? A : 1][NB];
-#pragma unroll
-    for (int i = 0; i < A; ++i) {
-        const int k = s + i;
-#pragma unroll
-        for (int b = 0; b < NB; ++b)
-            xl[i][b] = P::xop(diag_load<P, H>(cw, tab, L, pitch, s, k, m[b]), p_lo[i], (uint32_t)(k + 1),
-                              m[b] >= w_lo[i]);
-    }
-    // the corner (A = 0, first column) when the middle kernel finished it
-    const bool corner_done = A == 0 && t_first > k_hi + 1;
-    // X of the high splits: the row's finished cells, with the u_f prefix
-    typename P::X xh[kT - 1][NB];
-    // the operands of each cell: the stored partial, C_2's, the splits'
-    struct Loads {
-        uint32_t key[NB];
-        int64_t stored64[NB];
-        typename P::Raw c2[NB];
-        typename P::Raw yl[A > 0 ? A : 1][NB];
-        typename P::Raw yh[kT - 1][NB];
-    } ld[kT];
-    auto load_j = [&](auto jc) {
-        constexpr int j = decltype(jc)::value;
-        const int t = min(k_hi + 1 + j, L);  // columns past L read the last one
-        const int64_t cell = row_of(L, s, t) * pitch;
-        if constexpr (j == 0 && A == 0) {
-            if (corner_done) {
-                // the corner's final cost, as X of the high splits
-#pragma unroll
-                for (int b = 0; b < NB; ++b)
-                    ld[0].c2[b] = P::load(tab + cell, cw.shadow + cell, m[b]);
-                return;
-            }
-        }
-        const int64_t below = row_of(L, s + 1, t) * pitch;
-#pragma unroll
-        for (int b = 0; b < NB; ++b) {
-            if constexpr (PP)
-                ld[j].key[b] = __builtin_nontemporal_load(cw.shadow + cell + m[b]);
-            else
-                ld[j].stored64[b] = load64(tab + cell, m[b]);
-            const int ri = m[b] - wab;
-            ld[j].c2[b] = P::load(tab + below, cw.shadow + below, m[b] >= g_all[j] && ri >= 0 ? ri : m[b]);
-        }
-#pragma unroll
-        for (int i = 0; i < A; ++i) {
-            const int64_t yrow = row_of(L, s + i + 1, t) * pitch;
-#pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                const int ri = m[b] - w_lo[i];
-                ld[j].yl[i][b] = P::load(tab + yrow, cw.shadow + yrow, ri >= 0 ? ri : m[b]);
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < j; ++i) {
-            // split k = k_hi + 1 + i, Y at (k + 1, t) (within the block for every t <= L)
-            const int k1 = min(k_hi + 2 + i, t);
-#pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                const int ri = m[b] - w_t[i];
-                ld[j].yh[i][b] = diag_load<P, H>(cw, tab, L, pitch, k1, t, ri >= 0 ? ri : m[b]);
-            }
-        }
-    };
-    auto comp_j = [&](auto jc) {
-        constexpr int j = decltype(jc)::value;
-        const int t = k_hi + 1 + j;
-        if constexpr (j == 0 && A == 0) {
-            if (corner_done) {
-#pragma unroll
-                for (int b = 0; b < NB; ++b)
-                    xh[0][b] = P::xop(ld[0].c2[b], p_t[0], (uint32_t)(t + 1), m[b] >= w_t[0]);
-                return;
-            }
-        }
-#pragma unroll
-        for (int b = 0; b < NB; ++b) {
-            typename P::Acc a;
-            P::init(a);
-#pragma unroll
-            for (int i = 0; i < A; ++i)
-                P::relax(a, xl[i][b], P::yop(ld[j].yl[i][b]), (uint32_t)(s + i + 1));
-            int64_t stored;
-            if constexpr (!PP) {
-                stored = ld[j].stored64[b];
-            } else {
-                const uint32_t key = ld[j].key[b];
-                const uint32_t split = (uint32_t)(k_lo + 1) + (key & ((1u << S) - 1u));
-                stored = key == kInf32 ? (int64_t)((uint64_t)kInf32 << 32)
-                                       : (int64_t)(((uint64_t)(key >> S) << 32) | split);
-            }
-            P::merge_stored(a, stored, pre_lo);
-#pragma unroll
-            for (int i = 0; i < j; ++i)
-                P::relax(a, xh[i][b], P::yop(ld[j].yh[i][b]), (uint32_t)(k_hi + 2 + i));
-            if (m[b] < g_none[j])
-                P::init(a);
-            if (m[b] >= g_all[j] && m[b] >= wab)
-                P::relax_all(a, ld[j].c2[b], ufub);
-            if constexpr (j + 1 < kT)
-                xh[j][b] = P::xop(final_raw<P>(a), p_t[j], (uint32_t)(t + 1), m[b] >= w_t[j]);
-            const int mb = m0 + b * kEdgeThreads;
-            if (t <= t_last && mb <= M)
-                store_cell<P>(tab, dtab, cw.shadow, row_of(L, s, t) * pitch + mb, a);
-        }
-    };
-    static_for([&](auto jc) {
-        constexpr int j = decltype(jc)::value;
-        if constexpr (j < kRowAhead)
-            load_j(std::integral_constant<int, j>{});
-    }, std::make_integer_sequence<int, kT>{});
-    static_for([&](auto jc) {
-        constexpr int j = decltype(jc)::value;
-        __builtin_amdgcn_sched_barrier(0);
-        if constexpr (j + kRowAhead < kT)
-            load_j(std::integral_constant<int, j + kRowAhead>{});
-        __builtin_amdgcn_sched_barrier(0);
-        comp_j(jc);
-    }, std::make_integer_sequence<int, kT>{});
-}
-
-// Row 16(I + 1) - A of every block (I, I + delta) of one block-diagonal; a
-// workgroup is one wave at 64 kRowBudgets consecutive budgets of one block.
-// With `finish`, the middle kernels finished the corner (row 16I + 16,
-// column 16J + 1).
-template <int A>
-__global__ __launch_bounds__(kEdgeThreads) void edge_row_kernel(const int64_t *__restrict__ params, int L, int M,
-                                                                int64_t pitch, int64_t rows, int delta, int finish,
-                                                                int64_t *__restrict__ cost,
-                                                                int16_t *__restrict__ dec, Work w)
-{
-    const int c = blockIdx.z;
-    const int I = blockIdx.y;
-    const int J = I + delta;
-    const int s = (I + 1) * kT - A;
-    const int m0 = blockIdx.x * (kEdgeThreads * kRowBudgets) + threadIdx.x;
-    if (m0 > M)
-        return;
-    const int t_first = J * kT + 1 + (A == 0 && finish ? 1 : 0);
-    const int t_last = min(J * kT + kT, L);
-    const ChainRows r = chain_rows(params, w, L, c);
-    const ChainWork cw = chain_work(w, L, rows, pitch, c);
-    int64_t *tab = cost + (int64_t)c * rows * pitch;
-    int16_t *dtab = dec + (int64_t)c * rows * pitch;
-    const bool packed = middle_packed(cw, delta, (delta - 1) * kT);
-    if (!cw.narrow(delta))
-        row_body<Wide, false, false, A>(r, cw, L, M, m0, pitch, s, J, t_first, t_last, tab, dtab);
-    else if (cw.diag16() && packed)
-        row_body<Narrow, true, true, A>(r, cw, L, M, m0, pitch, s, J, t_first, t_last, tab, dtab);
-    else if (cw.diag16())
-        row_body<Narrow, true, false, A>(r, cw, L, M, m0, pitch, s, J, t_first, t_last, tab, dtab);
-    else if (packed)
-        row_body<Narrow, false, true, A>(r, cw, L, M, m0, pitch, s, J, t_first, t_last, tab, dtab);
-    else
-        row_body<Narrow, false, false, A>(r, cw, L, M, m0, pitch, s, J, t_first, t_last, tab, dtab);
-}
-
-// edge_row_kernel<a> for a launch-time a in [0, A]
-template <int A>
-void launch_edge_row(int a, dim3 grid, hipStream_t stream, const Tables &tb, int delta, int finish, const Work &w)
-{
-    if (a == A)
-        edge_row_kernel<A><<<grid, kEdgeThreads, 0, stream>>>(tb.params, tb.L, tb.M, tb.pitch, tb.rows, delta,
-                                                               finish, tb.cost, tb.dec, w);
-    else if constexpr (A > 0)
-        launch_edge_row<A - 1>(a, grid, stream, tb, delta, finish, w);
-}
-
 hipError_t check() { return hipGetLastError(); }
-
-// Whether the edges of a block-diagonal with `blocks` blocks over all chains
-// go by rows (16 launches) rather than by anti-diagonals (30 or 31).
-bool row_edges(int64_t blocks) { return blocks >= kRowMinBlocks; }
 
 // Pairs (s, s + d) inside one diagonal block of side kT, over all blocks.
 uint64_t in_block_pairs(int L, int d)
@@ -1964,7 +1404,6 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
         const bool rows = schedule == ROTOR_SCHEDULE_BLOCKED_ROWS ||
                           (schedule != ROTOR_SCHEDULE_BLOCKED_ROUNDS && row_edges((int64_t)(nb - delta) * tb.n_chains));
         if (rows) {
-            const unsigned mb_row = (unsigned)((tb.M + kEdgeThreads * kRowBudgets) / (kEdgeThreads * kRowBudgets));
             for (int a = 0; a < kT; ++a) {
                 uint64_t c1 = 0, cells = 0;
                 for (int I = 0; I + delta < nb; ++I) {
@@ -1976,7 +1415,7 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
                 }
                 if ((e = before(kEdge)) != hipSuccess)
                     return e;
-                launch_edge_row<kT - 1>(a, dim3(mb_row, nb - delta, tb.n_chains), stream, tb, delta, finish, w);
+                launch_edge_row(a, nb - delta, stream, tb, delta, finish, w);
                 if ((e = launched(kEdge, c1, cells, cells)) != hipSuccess)
                     return e;
             }

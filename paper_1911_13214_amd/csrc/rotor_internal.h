@@ -94,6 +94,13 @@ struct LaunchObserver {
 hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_t stream,
                        LaunchObserver *obs = nullptr);
 
+// Edges of the blocked fill by rows: whether a block-diagonal with `blocks`
+// blocks over all chains takes them, and the launch of row 16(I + 1) - a of
+// its `blocks` blocks (I, I + delta) per chain (finish: the middle kernels
+// finished the corners).
+bool row_edges(int64_t blocks);
+void launch_edge_row(int a, int blocks, hipStream_t stream, const Tables &tb, int delta, int finish, const Work &w);
+
 // Enqueue the sequence walk (one workgroup per budget).
 hipError_t launch_reconstruct(const int64_t *params, int L, int M, int64_t pitch, int64_t rows,
                               const int16_t *dec_chain, int n_budgets, const int64_t *budgets, int64_t cap,

@@ -1,0 +1,11 @@
+// Row edges with 4 to 7 low splits (see rotor_rows.h).
+#include "rotor_rows.h"
+
+namespace rotor {
+
+void launch_edge_row_1(int a, dim3 grid, hipStream_t stream, const Tables &tb, int delta, int finish, const Work &w)
+{
+    launch_edge_row_range<4, 7>(a, grid, stream, tb, delta, finish, w);
+}
+
+}  // namespace rotor
