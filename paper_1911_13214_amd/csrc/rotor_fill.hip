@@ -61,6 +61,8 @@
 // finished by the middle kernels.  A small table is instead filled in the
 // streamed order: one launch per diagonal d over all its pairs (diag_kernel,
 // or diag_split_kernel with the splits of a pair spread over four waves).
+#include <type_traits>
+
 #include "rotor_paths.h"
 
 namespace rotor {
@@ -180,10 +182,12 @@ __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ pa
                 const int x = I * kT, yb = I + D + 1, y = min(yb * kT, L);
                 vmax = max(vmax, ppb[yb] - ppb[I] - (int64_t)(y - x) * pre[x] + bb[yb] - bb[I]);
             }
-            // (V_D + 1) << S <= 2^32 - 1 leaves S >= 0 bits on the narrow path
+            // (V_D + 1) << S <= 2^32 - 1 leaves S >= 0 bits on the narrow path;
+            // -2 marks a 64-bit block-diagonal whose middle keys are exact as
+            // doubles, -1 the others
             int bits = (uint64_t)vmax < kNarrowBound
                            ? 63 - __clzll((long long)(0xFFFFFFFFull / ((uint64_t)vmax + 1)))
-                           : -1;
+                           : (uint64_t)vmax < kF64Bound ? -2 : -1;
             // D = 0 has no middle products; its width only says whether the
             // 2-byte copy of the diagonal blocks is used (>= 17), which only
             // the edges of a chain of two blocks or more read
@@ -652,62 +656,6 @@ __global__ __launch_bounds__(256) void diag_split_kernel(const int64_t *__restri
         diag_split_body<Wide>(r, cw, L, M, m, pitch, s, t, wave, part, tab, dtab);
 }
 
-// Middle splits of every block (I, I + D) of one block-diagonal.  A workgroup
-// is one block at 64 budgets; its four waves hold the four 8 x 8 quarters of
-// the block, one accumulator per pair and lane.  For each middle split k the
-// wave loads X for its 8 rows and Y for its 8 columns (the waves sharing rows
-// or columns meet in L1/L2) and relaxes 64 accumulators; two register sets
-// alternate so the loads of split k+1 are in flight during the updates of k.
-// The prefix of u_f starts at the first middle split; edge_kernel adds the
-// part from s.  Partials are stored in the cost table, where edge_kernel
-// finishes the cells.
-template <class P>
-struct MiddleTile {
-    int64_t xrow[kSub];  // element offset of row (s0 + i, k)
-    int64_t yrow;        // element offset of row (k + 1, t0)
-    int64_t ystep[kSub]; // row of (k + 1, t0 + j) relative to yrow, in elements
-    const int64_t *tab;
-    const uint32_t *shadow;
-    int mc;
-
-    __device__ void load(int ri, typename P::Raw (&rx)[kSub], typename P::Raw (&ry)[kSub]) const
-    {
-#pragma unroll
-        for (int i = 0; i < kSub; ++i)
-            rx[i] = P::load(tab + xrow[i], shadow + xrow[i], mc);
-        const int yi = ri >= 0 ? ri : 0;
-#pragma unroll
-        for (int j = 0; j < kSub; ++j)
-            ry[j] = P::load(tab + yrow + ystep[j], shadow + yrow + ystep[j], yi);
-    }
-    __device__ void advance(int L, int k, int64_t pitch)  // from split k to k + 1
-    {
-#pragma unroll
-        for (int i = 0; i < kSub; ++i)
-            xrow[i] += pitch;
-        yrow += (int64_t)(L - k - 1) * pitch;
-    }
-};
-
-template <class P>
-__device__ inline void middle_update(typename P::Acc (&acc)[kSub][kSub], const typename P::Raw (&rx)[kSub],
-                                     const typename P::Raw (&ry)[kSub], uint64_t prefix, uint32_t sp, bool ok)
-{
-    typename P::X x[kSub];
-    typename P::Y y[kSub];
-#pragma unroll
-    for (int i = 0; i < kSub; ++i)
-        x[i] = P::xop(rx[i], prefix, sp, ok);
-#pragma unroll
-    for (int j = 0; j < kSub; ++j)
-        y[j] = P::yop(ry[j]);
-#pragma unroll
-    for (int i = 0; i < kSub; ++i)
-#pragma unroll
-        for (int j = 0; j < kSub; ++j)
-            P::relax(acc[i][j], x[i], y[j], sp);
-}
-
 // The corner cell (16I + 16, 16J + 1) of a block (I, J) has no low or high
 // splits: its middle result, whose u_f prefix starts at its own s, is its
 // whole C_1.  The middle kernels finish it (gates, C_2, final stores), so the
@@ -728,119 +676,18 @@ __device__ inline void finish_corner(const ChainRows &r, const ChainWork &cw, in
     store_cell<P>(tab, dtab, cw.shadow, cell * pitch + m, acc);
 }
 
-template <class P>
-__device__ inline void middle_body(const ChainRows &r, const ChainWork &cw, int L, int M, int m, int64_t pitch,
-                                   int s0, int t0, int nt, int k_lo, int k_hi, int ka, int kb, int n_part,
-                                   int64_t *tab, int16_t *dtab)
-{
-    MiddleTile<P> tl;
-#pragma unroll
-    for (int i = 0; i < kSub; ++i)
-        tl.xrow[i] = row_of(L, s0 + i, ka) * pitch;
-#pragma unroll
-    for (int j = 0; j < kSub; ++j)
-        tl.ystep[j] = (int64_t)(j < nt ? j : nt - 1) * pitch;  // columns past L read the last one
-    tl.yrow = row_of(L, ka + 1, t0) * pitch;
-    tl.tab = tab;
-    tl.shadow = cw.shadow;
-    tl.mc = m <= M ? m : M;
 
-    typename P::Acc acc[kSub][kSub];
-#pragma unroll
-    for (int i = 0; i < kSub; ++i)
-#pragma unroll
-        for (int j = 0; j < kSub; ++j)
-            P::init(acc[i][j]);
 
-    uint64_t prefix = (uint64_t)(cw.pre[ka - 1] - cw.pre[k_lo - 1]);  // u_f from k_lo on
-    typename P::Raw ax[kSub], ay[kSub], bx[kSub], by[kSub];
-    int k = ka;
-    int ra = tl.mc - r.wa[k - 1];
-    tl.load(ra, ax, ay);
-    for (; k + 1 <= kb; k += 2) {
-        tl.advance(L, k, pitch);
-        const int rb = tl.mc - r.wa[k];
-        tl.load(rb, bx, by);
-        prefix += (uint64_t)r.uf[k - 1];
-        middle_update<P>(acc, ax, ay, prefix, (uint32_t)(k + 1), ra >= 0);
-        if (k + 2 <= kb) {
-            tl.advance(L, k + 1, pitch);
-            ra = tl.mc - r.wa[k + 1];
-            tl.load(ra, ax, ay);
-        }
-        prefix += (uint64_t)r.uf[k];
-        middle_update<P>(acc, bx, by, prefix, (uint32_t)(k + 2), rb >= 0);
-    }
-    if (k == kb) {
-        prefix += (uint64_t)r.uf[k - 1];
-        middle_update<P>(acc, ax, ay, prefix, (uint32_t)(k + 1), ra >= 0);
-    }
-    if (m > M)
-        return;
-    if (n_part > 1) {
-        // a run of a cut range: the stored forms (value << 32) | s' and
-        // (value << 16) | s' order by value, then split, as unsigned words
-#pragma unroll
-        for (int i = 0; i < kSub; ++i)
-#pragma unroll
-            for (int j = 0; j < kSub; ++j)
-                if (j < nt)
-                    atomicMin((unsigned long long *)&tab[row_of(L, s0 + i, t0 + j) * pitch + m],
-                              (unsigned long long)P::stored(acc[i][j]));
-        return;
-    }
-    // the wave whose last row is 16I + 16 and first column 16J + 1 holds the
-    // corner
-    const bool corner = s0 + kSub - 1 == k_lo && t0 == k_hi + 1;
-#pragma unroll
-    for (int i = 0; i < kSub; ++i)
-#pragma unroll
-        for (int j = 0; j < kSub; ++j) {
-            if (i == kSub - 1 && j == 0 && corner)
-                finish_corner<P>(r, cw, L, m, pitch, k_lo, k_hi + 1, acc[i][j], tab, dtab);
-            else if (j < nt)
-                tab[row_of(L, s0 + i, t0 + j) * pitch + m] = P::stored(acc[i][j]);
-        }
-}
-
-__global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__ params, int L, int M,
-                                                     int64_t pitch, int64_t rows, int delta, int n_part,
-                                                     int64_t *__restrict__ cost, int16_t *__restrict__ dec, Work w)
-{
-    const int c = blockIdx.z;
-    const int I = blockIdx.y;
-    const int J = I + delta;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int chunks = gridDim.x / n_part;
-    const int part = blockIdx.x / chunks;
-    const int m = (blockIdx.x - part * chunks) * 64 + (threadIdx.x & 63);
-    const int s0 = I * kT + (wave >> 1) * kSub + 1;
-    const int t0 = J * kT + (wave & 1) * kSub + 1;
-    if (t0 > L)
-        return;
-    const int nt = min(kSub, L - t0 + 1);
-    const ChainRows r = chain_rows(params, w, L, c);
-    const ChainWork cw = chain_work(w, L, rows, pitch, c);
-    int64_t *tab = cost + (int64_t)c * rows * pitch;
-    int16_t *dtab = dec + (int64_t)c * rows * pitch;
-    const int k_lo = (I + 1) * kT;
-    const int k_hi = J * kT;
-    if (middle_packed(cw, delta, k_hi - k_lo) || middle_runs(cw, delta, k_hi - k_lo))
-        return;  // middle_packed_kernel takes this block-diagonal
-    // this workgroup's part of the middle splits, as in middle_packed_kernel
-    const int part_len = (k_hi - k_lo + n_part) / n_part;
-    const int ka = k_lo + part * part_len;
-    const int kb = min(k_hi, ka + part_len - 1);
-    if (ka > kb)
-        return;
-    if (cw.narrow(delta))
-        middle_body<Narrow>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, ka, kb, n_part, tab, dtab);
-    else
-        middle_body<Wide>(r, cw, L, M, m, pitch, s0, t0, nt, k_lo, k_hi, ka, kb, n_part, tab, dtab);
-}
-
-// Packed middle products (same blocks, workgroups and register tiles as
-// middle_kernel, operands staged in LDS).  With S the bit width of
+// Middle splits of every block (I, I + D) of one block-diagonal
+// (middle_packed_kernel, middle_kernel).  A workgroup is one block at 64
+// budgets; its four waves hold the four 8 x 8 quarters of the block, one
+// accumulator per pair and lane.  For each middle split k the 16 X rows and
+// 16 Y rows of the block at the workgroup's budgets are copied into LDS
+// (each row fetched once per workgroup), and each wave relaxes its 64
+// accumulators with its 8 X and 8 Y operands.  The prefix of u_f starts at
+// the first middle split; the edges add the part from s.
+//
+// Packed middle products.  With S the bit width of
 // k - k_lo, a loaded value v becomes v << S by a rotation that leaves
 // 0xFFFFFFFF (infinity) unchanged; X also gets (prefix << S) | (k - k_lo) by
 // a saturating add, Y nothing more, so a candidate is sat(x + y) and the
@@ -1158,6 +1005,283 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
                 __builtin_nontemporal_store(acc[i][j], &cw.shadow[row_of(L, s0 + i, t0 + j) * pitch + m]);
             }
         }
+}
+
+// The middle products of the chains and block-diagonals that take neither
+// packed keys nor packed runs: (value, split) pairs on the narrow path
+// (operands from the compact copy, 4 bytes) and 64-bit keys on the wide path
+// (operands from the int64 table, copied as two dwords per budget).  Same
+// blocks, register tiles, ring of two-split stages and DMA copies into LDS
+// as middle_packed_kernel; the partial, counting u_f from the first middle
+// split, goes to the cost table in the stored() form ((value << 32) | s' or
+// the 64-bit key), merged by atomic minimum when the range is cut
+// (n_part > 1, slots set to all ones by fill_partials), and the corner cell
+// is finished here otherwise.
+//
+// With F (a block-diagonal whose bound V_D is below 2^38) the accumulators
+// are exact doubles instead: a candidate of split k is the key
+// value * 2^15 + (k - k_lo), below 2^53, so one double add and one double
+// minimum relax it (two instructions against four for the (value, split)
+// pairs or the 64-bit keys; the part issues double additions and minima at
+// the rate of 32-bit integer ones), and the minimum key is the smallest
+// value with, among equal values, the smallest split.  An operand at
+// infinity (0xFFFFFFFF, INT64_MAX) gives a key at or above the largest
+// finite one plus one, a budget shifted below 0 the key +inf.
+// Minimum of two doubles that are never NaN: v_min_f64 itself (the
+// compiler's minnum quiets its operands first, one more instruction per
+// candidate)
+__device__ __forceinline__ double min_f64(double a, double b)
+{
+    double r;
+    asm("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+
+__device__ inline double f64_finite_bound(bool narrow)
+{
+    // narrow: the infinity 0xFFFFFFFF as a value; 64-bit: 2^53
+    return narrow ? 4294967295.0 * 32768.0 : 9007199254740992.0;
+}
+
+// The stored() form of the path P for a double key of the middle range
+// starting at split k_lo + 1.
+template <class P>
+__device__ inline int64_t f64_stored(double key, int k_lo)
+{
+    if (!(key < f64_finite_bound(P::kShadow)))
+        return P::kShadow ? (int64_t)((uint64_t)kInf32 << 32) : (int64_t)(1ull << 62);
+    const double q = __builtin_floor(key * (1.0 / 32768.0));
+    const uint64_t v = (uint64_t)q;
+    const uint32_t split = (uint32_t)(k_lo + 1) + (uint32_t)(key - q * 32768.0);
+    return P::kShadow ? (int64_t)((v << 32) | split) : (int64_t)((v << 16) | split);
+}
+
+template <class P>
+__device__ inline typename P::Acc f64_acc(double key, int k_lo)
+{
+    typename P::Acc a;
+    P::init(a);
+    P::merge_later(a, f64_stored<P>(key, k_lo));
+    return a;
+}
+
+template <class P, bool F>
+__device__ __forceinline__ void middle_lds_body(const ChainRows &r, const ChainWork &cw, int L, int M, int m,
+                                                int64_t pitch, int I, int J, int wave, int ka, int kb, int k_lo,
+                                                int k_hi, int n_part, int64_t *tab, int16_t *dtab, uint32_t *ring)
+{
+    constexpr int EW = P::kBytes / 4;          // dwords per element
+    constexpr int kSW = kSplitWords * EW;      // dwords per split slot: 32 rows of 64 elements
+    const int lane = threadIdx.x & 63;
+    const int mc = min(m, M);
+    const int m0 = m - lane;                   // the workgroup's first budget
+    const int n_stages = (kb - ka + kStage) / kStage;
+    const int s0 = I * kT + (wave >> 1) * kSub + 1;
+    const int t0 = J * kT + (wave & 1) * kSub + 1;
+    const int nt = t0 <= L ? min(kSub, L - t0 + 1) : 0;
+    // rows this wave copies: waves 0, 1 the X rows (s, k) of s = 16I+1+8w ..,
+    // waves 2, 3 the Y rows (k+1, t) of t = 16J+1+8(w-2) .. (past L: row L);
+    // a row of 64 elements takes EW copies of 64 dwords, copy e taking
+    // elements 32e .. 32e + 31 (two lanes per element) when EW = 2
+    const bool copies_x = wave < 2;
+    const int first = copies_x ? I * kT + 1 + wave * kSub : J * kT + 1 + (wave - 2) * kSub;
+    const char *const base = P::table(tab, cw.shadow);
+    const int64_t row_bytes = pitch * P::kBytes;
+    const char *src[kDmaPerSplit];
+#pragma unroll
+    for (int i = 0; i < kDmaPerSplit; ++i)
+        src[i] = base + (copies_x ? row_of(L, first + i, ka) : row_of(L, ka + 1, min(first + i, L))) * row_bytes;
+    // the element and dword each lane copies in copy e
+    int elem_budget[EW];
+    uint32_t dword_off[EW];
+#pragma unroll
+    for (int e = 0; e < EW; ++e) {
+        const int el = EW == 1 ? lane : 32 * e + (lane >> 1);
+        elem_budget[e] = min(m0 + el, M);
+        dword_off[e] = EW == 1 ? 0u : 4u * (uint32_t)(lane & 1);
+    }
+    int k_copy = ka;  // next split to copy
+    uint32_t *const dst0 = ring + (copies_x ? wave * kSub : kT + (wave - 2) * kSub) * 64 * EW;
+    int fill = 0;  // ring stage filled next
+    // copies of one stage; splits past kb copy split kb again, so every
+    // stage issues the same number of copies
+    auto issue = [&]() {
+        uint32_t *dst = dst0 + fill * (kStage * kSW);
+#pragma unroll
+        for (int p = 0; p < kStage; ++p) {
+            const int k = k_copy;
+            const int w_k = r.wa[k - 1];
+#pragma unroll
+            for (int e = 0; e < EW; ++e) {
+                const int mb = elem_budget[e];
+                const int ri = mb - w_k;
+                const uint32_t off = (uint32_t)P::kBytes * (uint32_t)(copies_x ? mb : (ri >= 0 ? ri : mb)) +
+                                     dword_off[e];
+#pragma unroll
+                for (int i = 0; i < kDmaPerSplit; ++i)
+                    __builtin_amdgcn_global_load_lds((global_void *)(src[i] + off),
+                                                     (lds_void *)(dst + p * kSW + i * 64 * EW + e * 64), 4, 0, 0);
+            }
+            if (k < kb) {
+                // to split k + 1: X rows advance one row, Y rows L - k - 1 rows
+                const int64_t step = copies_x ? row_bytes : (int64_t)(L - k - 1) * row_bytes;
+#pragma unroll
+                for (int i = 0; i < kDmaPerSplit; ++i)
+                    src[i] += step;
+                ++k_copy;
+            }
+        }
+        fill = fill + 1 == kRing ? 0 : fill + 1;
+    };
+
+    typedef typename std::conditional<F, double, typename P::Acc>::type Acc;
+    Acc acc[kSub][kSub];
+#pragma unroll
+    for (int i = 0; i < kSub; ++i)
+#pragma unroll
+        for (int j = 0; j < kSub; ++j) {
+            if constexpr (F)
+                acc[i][j] = __builtin_inf();
+            else
+                P::init(acc[i][j]);
+        }
+#pragma unroll
+    for (int st = 0; st < kRing - 1; ++st)
+        if (st < n_stages)
+            issue();
+    uint64_t prefix = (uint64_t)(cw.pre[ka - 1] - cw.pre[k_lo - 1]);  // u_f from k_lo on
+    typedef typename P::Raw Raw;
+    const Raw *const x_lds0 = (const Raw *)(ring + (wave >> 1) * kSub * 64 * EW) + lane;
+    const Raw *const y_lds0 = (const Raw *)(ring + (kT + (wave & 1) * kSub) * 64 * EW) + lane;
+    int read = 0;  // ring stage read next
+    int k = ka;
+    for (int it = 0; it < n_stages; ++it) {
+        // this wave's copies of stage it have landed, and so (after the
+        // barrier) have every wave's; the stage refilled below was read by
+        // every wave before it reached the barrier
+        ring_wait<kRing - 2>(n_stages - 1 - it);
+        if (it + kRing - 1 < n_stages)
+            issue();
+        const Raw *x_lds = x_lds0 + read * (kStage * kSplitWords);
+        const Raw *y_lds = y_lds0 + read * (kStage * kSplitWords);
+        read = read + 1 == kRing ? 0 : read + 1;
+        typedef typename std::conditional<F, double, typename P::X>::type XT;
+        typedef typename std::conditional<F, double, typename P::Y>::type YT;
+        XT x[kStage][kSub];
+        YT y[kStage][kSub];
+        uint32_t sp[kStage];
+#pragma unroll
+        for (int p = 0; p < kStage; ++p, ++k) {
+            const bool real = k <= kb;
+            const int kk = real ? k : kb;
+            const int ri = mc - r.wa[kk - 1];
+            prefix += real ? (uint64_t)r.uf[k - 1] : 0;
+            sp[p] = (uint32_t)(k + 1);
+            if constexpr (F) {
+                const double add = real && ri >= 0 ? (double)((prefix << 15) + (uint64_t)(k - k_lo)) : __builtin_inf();
+                // scaled by ldexp, which the compiler does not fuse into the
+                // candidates' additions
+#pragma unroll
+                for (int i = 0; i < kSub; ++i)
+                    x[p][i] = __builtin_ldexp((double)x_lds[p * kSplitWords + i * 64], 15) + add;
+#pragma unroll
+                for (int j = 0; j < kSub; ++j)
+                    y[p][j] = __builtin_ldexp((double)y_lds[p * kSplitWords + j * 64], 15);
+            } else {
+#pragma unroll
+                for (int i = 0; i < kSub; ++i)
+                    x[p][i] = P::xop(x_lds[p * kSplitWords + i * 64], prefix, sp[p], real && ri >= 0);
+#pragma unroll
+                for (int j = 0; j < kSub; ++j)
+                    y[p][j] = P::yop(y_lds[p * kSplitWords + j * 64]);
+            }
+        }
+        // splits in increasing order (the narrow pairs keep the first minimum)
+#pragma unroll
+        for (int p = 0; p < kStage; ++p)
+#pragma unroll
+            for (int i = 0; i < kSub; ++i)
+#pragma unroll
+                for (int j = 0; j < kSub; ++j) {
+                    if constexpr (F)
+                        acc[i][j] = min_f64(acc[i][j], x[p][i] + y[p][j]);
+                    else
+                        P::relax(acc[i][j], x[p][i], y[p][j], sp[p]);
+                }
+    }
+    if (m > M || nt == 0)
+        return;
+    auto stored = [&](const Acc &a) -> int64_t {
+        if constexpr (F)
+            return f64_stored<P>(a, k_lo);
+        else
+            return P::stored(a);
+    };
+    if (n_part > 1) {
+        // a run of a cut range: the stored forms (value << 32) | s' and
+        // (value << 16) | s' order by value, then split, as unsigned words
+#pragma unroll
+        for (int i = 0; i < kSub; ++i)
+#pragma unroll
+            for (int j = 0; j < kSub; ++j)
+                if (j < nt)
+                    atomicMin((unsigned long long *)&tab[row_of(L, s0 + i, t0 + j) * pitch + m],
+                              (unsigned long long)stored(acc[i][j]));
+        return;
+    }
+    // the wave whose last row is 16I + 16 and first column 16J + 1 holds the
+    // corner
+    const bool corner = s0 + kSub - 1 == k_lo && t0 == k_hi + 1;
+#pragma unroll
+    for (int i = 0; i < kSub; ++i)
+#pragma unroll
+        for (int j = 0; j < kSub; ++j) {
+            if (i == kSub - 1 && j == 0 && corner) {
+                if constexpr (F)
+                    finish_corner<P>(r, cw, L, m, pitch, k_lo, k_hi + 1, f64_acc<P>(acc[i][j], k_lo), tab, dtab);
+                else
+                    finish_corner<P>(r, cw, L, m, pitch, k_lo, k_hi + 1, acc[i][j], tab, dtab);
+            } else if (j < nt) {
+                tab[row_of(L, s0 + i, t0 + j) * pitch + m] = stored(acc[i][j]);
+            }
+        }
+}
+
+__global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__ params, int L, int M,
+                                                     int64_t pitch, int64_t rows, int delta, int n_part,
+                                                     int64_t *__restrict__ cost, int16_t *__restrict__ dec, Work w)
+{
+    // a ring of 64-bit elements (the narrow path uses the first half)
+    __shared__ __align__(16) uint32_t ring[kRing * kStage * kSplitWords * 2];
+    const Tile tile = xcd_tile();
+    const int c = tile.z;
+    const int I = tile.y;
+    const int J = I + delta;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int chunks = gridDim.x / n_part;
+    const int part = tile.x / chunks;
+    const int m = (tile.x - part * chunks) * 64 + (threadIdx.x & 63);
+    const ChainWork cw = chain_work(w, L, rows, pitch, c);
+    const int k_lo = (I + 1) * kT;
+    const int k_hi = J * kT;
+    // uniform over the workgroup: every wave returns or none does
+    if (middle_packed(cw, delta, k_hi - k_lo) || middle_runs(cw, delta, k_hi - k_lo))
+        return;  // middle_packed_kernel takes this block-diagonal
+    // this workgroup's part of the middle splits, as in middle_packed_kernel
+    const int part_len = (k_hi - k_lo + n_part) / n_part;
+    const int ka = k_lo + part * part_len;
+    const int kb = min(k_hi, ka + part_len - 1);
+    if (ka > kb)
+        return;
+    const ChainRows r = chain_rows(params, w, L, c);
+    int64_t *tab = cost + (int64_t)c * rows * pitch;
+    int16_t *dtab = dec + (int64_t)c * rows * pitch;
+    if (cw.narrow(delta))
+        middle_lds_body<Narrow, true>(r, cw, L, M, m, pitch, I, J, wave, ka, kb, k_lo, k_hi, n_part, tab, dtab, ring);
+    else if (cw.f64_keys(delta))
+        middle_lds_body<Wide, true>(r, cw, L, M, m, pitch, I, J, wave, ka, kb, k_lo, k_hi, n_part, tab, dtab, ring);
+    else
+        middle_lds_body<Wide, false>(r, cw, L, M, m, pitch, I, J, wave, ka, kb, k_lo, k_hi, n_part, tab, dtab, ring);
 }
 
 // Edge splits, C_2 and the gates for the cells a + b = q of every block

@@ -23,6 +23,9 @@ constexpr int kEdgeBudgets = 2;
 constexpr uint32_t kAllSplit = 0xFFFF;  // split field of a C_2 candidate
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
 constexpr uint64_t kNarrowBound = 0xFFFFFFFFull;  // V_D below: the narrow path
+// V_D below: the middle products' keys value * 2^15 + (split offset) stay
+// below 2^53, exact as doubles
+constexpr uint64_t kF64Bound = 1ull << 38;
 
 // The parameters of one chain as given (stage l at index l-1).
 struct ChainParams {
@@ -86,11 +89,14 @@ struct ChainWork {
     const int32_t *gall;   // [rows] m_all(s, t)
     uint32_t *shadow;      // [rows][pitch] compact copy of the costs (narrow block-diagonals)
     const int32_t *pbits;  // [nb] per block-diagonal D: the largest S with (V_D + 1) << S <= 2^32 - 1,
-                           // or -1 if V_D >= 2^32 - 1 (64-bit path)
+                           // or, if V_D >= 2^32 - 1 (64-bit path), -2 while V_D < 2^38, else -1
     int16_t *half;         // [16 L][hpitch] 2-byte copy of the diagonal blocks' cells
     int64_t hpitch;
     // whether the pairs of block-diagonal D take the narrow path
     __device__ bool narrow(int D) const { return pbits[D] >= 0; }
+    // whether the middle keys value * 2^15 + (split offset) of block-diagonal
+    // D are exact as doubles (V_D < 2^38)
+    __device__ bool f64_keys(int D) const { return pbits[D] != -1; }
     // whether the diagonal blocks' costs fit the 2-byte copy: (V_0 + 1) << 17
     // <= 2^32 - 1, i.e. V_0 <= 2^15 - 2, so finite values stay positive as
     // int16 and infinity is stored as -1 (0xFFFF)
