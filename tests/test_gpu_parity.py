@@ -370,8 +370,10 @@ def test_timed_solve_matches_and_counts_the_work(cfg):
     assert stats["prep"]["launches"] == 1
 
 
-# the narrow (4-byte) value path takes block-diagonals whose cost bound is below this
+# the narrow (4-byte) value path takes block-diagonals whose cost bound is
+# below NARROW_BOUND; the 64-bit path's middle keys are doubles below F64_BOUND
 NARROW_BOUND = (1 << 32) - 1
+F64_BOUND = 1 << 38
 
 
 def cost_bound(p):
@@ -517,6 +519,46 @@ def test_value_path_per_block_diagonal(shift, schedule):
     assert cost_bound(p[0]) >= NARROW_BOUND and narrow == list(range(len(narrow))) and 0 < len(narrow) < nb
     say(f"value path per block-diagonal shift={shift} narrow={narrow} {schedule}")
     _, cost, dec = solve_on_gpu(p, M, schedule=schedule)
+    assert_same(p, M, cost, dec)
+
+
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_double_keys_per_block_diagonal(schedule):
+    # Costs x 2^20: every block-diagonal on the 64-bit path, the first ones
+    # with bounds below 2^38, whose middle keys value * 2^15 + split offset
+    # are exact as doubles, the later ones with 64-bit integer keys.
+    L, M = 160, 240
+    p = scaled_chain(8, L, 20)
+    vd = block_diagonal_bounds(p[0], L)
+    f64 = [D for D in sorted(vd) if vd[D] < F64_BOUND]
+    assert min(vd.values()) >= NARROW_BOUND and f64 == list(range(1, len(f64) + 1)) and 0 < len(f64) < len(vd)
+    say(f"double keys per block-diagonal f64={f64} {schedule}")
+    _, cost, dec = solve_on_gpu(p, M, schedule=schedule)
+    assert_same(p, M, cost, dec)
+
+
+@pytest.mark.parametrize("bound", [NARROW_BOUND - 1, NARROW_BOUND, F64_BOUND - 1, F64_BOUND])
+@pytest.mark.parametrize("edges", EDGE_ORDERS)
+def test_value_paths_at_their_limits(bound, edges):
+    # Block-diagonal D takes the 4-byte values when its bound V_D is below
+    # 2^32 - 1, double keys when it is below 2^38, else 64-bit keys.  Three
+    # blocks of 16 stages with u_f = c, u_b = 2c, w_a = 1, w_abar = 2: D = 2
+    # is the whole chain, its bound put on each side of both limits through
+    # u_b of stage 1, and the oracle shows the top cell reaching it (the
+    # schedule that recomputes every forward step, at the smallest budgets).
+    L, M = 48, 120
+    c = bound // 1272 - 1  # the whole chain's bound is 1176 c + 48 u_b
+    p = np.zeros((1, 6, L), dtype=np.int64)
+    p[0, chaingen.UF], p[0, chaingen.UB] = c, 2 * c
+    p[0, chaingen.WA], p[0, chaingen.WABAR] = 1, 2
+    p[0, chaingen.UB, 0] = 2 * c + bound - 1272 * c
+    vd = block_diagonal_bounds(p[0], L)
+    assert vd[2] == bound and vd[1] < bound // 2
+    C, _ = oracle_tables(p, M)
+    top = C[orc.row(L, 1, L)]
+    assert top[top != orc.INF].max() == bound
+    say(f"value paths at their limits V_2={bound} {edges}")
+    _, cost, dec = solve_on_gpu(p, M, schedule=edges)
     assert_same(p, M, cost, dec)
 
 
