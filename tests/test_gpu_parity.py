@@ -410,8 +410,8 @@ def test_wide_value_path(L, M, seed, schedule):
 @pytest.mark.parametrize("L,M,seed", [(70, 300, 5), (90, 200, 6)])
 @pytest.mark.parametrize("edges", EDGE_ORDERS)
 def test_narrow_chain_beyond_packed_keys(L, M, seed, edges):
-    # costs below 2^30 (compact copy) but too large to leave the split field
-    # room once the middle range has 16 splits or more: the first
+    # costs below 2^30 (compact copy, 4-byte values) but too large to leave
+    # the split field room once the middle range has 16 splits or more: the first
     # block-diagonal takes packed keys, the later ones the (value, split) pairs
     # (their own bounds too leave too few bits)
     p = scaled_chain(seed, L, 12)
@@ -509,7 +509,7 @@ def test_value_path_per_block_diagonal(shift, schedule):
     # A chain whose cost bound is past 2^32 - 2 while the bounds of its shorter
     # sub-chains are not: the pairs of the first block-diagonals take the
     # 4-byte path (compact copy, saturating adds), the later ones the 64-bit
-    # keys, in both fill orders.
+    # keys, in the three orders.
     L, M = 160, 240
     p = scaled_chain(8, L, shift)
     nb = (L + 15) // 16
