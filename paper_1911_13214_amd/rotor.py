@@ -179,8 +179,9 @@ def rotor_solve(d_params, n_chains: int, L: int, M: int, d_cost, d_dec, d_work, 
 
 def rotor_solve_schedule(d_params, n_chains: int, L: int, M: int, d_cost, d_dec, d_work, schedule: str,
                          stream=None):
-    """rotor_solve with an explicit fill order: "auto", "blocked" or
-    "diagonal" (same tables, different speed)."""
+    """rotor_solve with an explicit fill order, a key of SCHEDULES: "auto",
+    "blocked" (edges by rounds or rows, chosen per block-diagonal), "rows",
+    "rounds" or "diagonal" (same tables, different speed)."""
     p, c, d, w, wb = _solve_ptrs(d_params, n_chains, L, M, d_cost, d_dec, d_work)
     _check(lib().rotor_solve_schedule(p, n_chains, L, M, c, d, w, wb, _stream_ptr(stream), SCHEDULES[schedule]),
            "rotor_solve_schedule")
