@@ -146,7 +146,8 @@ ROTOR_API int64_t rotor_row_index(int32_t L, int32_t s, int32_t t);
 ROTOR_API int32_t rotor_check_params(const int64_t *h_params, int32_t n_chains, int32_t L, int64_t M);
 
 /* Bytes of device workspace rotor_solve needs for these sizes: per-pair
- * gates, prefix sums, a few words per block of 16 stages, a domain status
+ * gates and saturation budgets, prefix sums, a few words per block of 16
+ * stages, a domain status
  * word per chain, a compact 4-byte-per-cell copy of the cost table (about
  * 40% of cost_bytes + dec_bytes) and, for chains of more than 16 stages, a
  * 2-byte copy of the cells of the 16 x 16 diagonal blocks.  Host only.

@@ -9,6 +9,18 @@
 // u_f^s + u_b^s + C(s+1, t, m - w_abar^s).  Every term lies on a strictly
 // shorter sub-chain.  Ties go to the smallest s', then to C_1 over C_2.
 //
+// Saturated budgets.  No schedule of [s, t] takes less than its least time
+// LT(s, t) = sum_{j=s}^{t} (u_f^j + u_b^j), every stage forward once and
+// backward once, so C >= LT.  C_2 reaches it when m >= m_all(s, t) and
+// C(s+1, t, m - w_abar^s) = LT(s+1, t); with G(t, t) = m_all(t, t) and
+// G(s, t) = max(m_all(s, t), G(s+1, t) + w_abar^s), induction on t - s
+// gives C(s, t, m) = LT(s, t) for every m >= G(s, t).  A C_1 candidate runs
+// stages s .. s'-1 forward twice, so it is at least LT(s, t) + u_f^s: when
+// u_f^s > 0 the decision there is C_2 alone.  prep_kernel writes G for every
+// pair, and a workgroup whose budgets are all at or above G(s, t) (with
+// u_f^s > 0) stores LT(s, t) and C_2 without loading an operand: the result
+// the relaxation would reach, at the cost of the stores.
+//
 // Value paths, chosen per block-diagonal by prep_kernel from a bound on
 // every finite cost: stage j runs forward at most t - j + 1 times in any
 // schedule of the family for [s, t] (induction on the recurrence), so
@@ -88,12 +100,14 @@ constexpr int kSplitMinD = 16;  // streamed diagonals from this length spread th
 // delta^s stored) and m_none(s, t) (peak of F_ck^s and F_none^{s+1..t-1} with
 // delta^t stored), Section 4.2; delta has the size of a.  The maximum over
 // s < j < t in m_none is a running maximum along t: a wave prefix maximum
-// per step plus the carry of the steps before.  Gates above INT32_MAX are
+// per step plus the carry of the steps before.  Workgroup s - 1 also writes
+// the saturation budgets G(s, t) of its row (head of this file), from two
+// more running maxima along t.  Gates above INT32_MAX are
 // clamped: any gate above M < 2^28 is never met.  Workgroup s - 1 also
 // writes the shift sizes w_a^s and w_abar^s clamped into [0, M + 1] (see
 // ChainRows).  The last workgroup of a chain checks its parameters against
-// the domain, scans u_f with one wave and bounds the costs of each
-// block-diagonal.
+// the domain, scans u_f and u_f + u_b with one wave and bounds the costs of
+// each block-diagonal.
 __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ params, int L, int M, int64_t rows,
                                                   Work w)
 {
@@ -108,26 +122,36 @@ __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ pa
         const bool in_domain = chain_in_domain(params + (int64_t)c * ROTOR_N_ROWS * L, L, lane);
         if (lane == 0)
             w.status[c] = in_domain ? ROTOR_OK : ROTOR_EDOMAIN;
-        // lane l sums a segment of stages, then the segment sums are scanned
+        // prefix sums of u_f and of u_f + u_b: lane l sums a segment of
+        // stages, then the segment sums are scanned
         const int seg = (L + 63) / 64;
         const int lo = min(L, lane * seg), hi = min(L, lo + seg);
-        uint64_t su = 0;
-        for (int l = lo; l < hi; ++l)
+        uint64_t su = 0, sa = 0;
+        for (int l = lo; l < hi; ++l) {
             su += (uint64_t)r.uf[l];
-        uint64_t incl = su;
+            sa += (uint64_t)r.uf[l] + (uint64_t)r.ub[l];
+        }
+        uint64_t incl = su, incla = sa;
         for (int off = 1; off < 64; off *= 2) {
-            const uint64_t v = __shfl_up(incl, off);
-            if (lane >= off)
+            const uint64_t v = __shfl_up(incl, off), va = __shfl_up(incla, off);
+            if (lane >= off) {
                 incl += v;
+                incla += va;
+            }
         }
         int64_t *pre = w.pre + (int64_t)c * (L + 1);
-        uint64_t run = incl - su;
+        int64_t *preall = w.preall + (int64_t)c * (L + 1);
+        uint64_t run = incl - su, runa = incla - sa;
         for (int l = lo; l < hi; ++l) {
             run += (uint64_t)r.uf[l];
+            runa += (uint64_t)r.uf[l] + (uint64_t)r.ub[l];
             pre[l + 1] = (int64_t)run;
+            preall[l + 1] = (int64_t)runa;
         }
-        if (lane == 0)
+        if (lane == 0) {
             pre[0] = 0;
+            preall[0] = 0;
+        }
         // Value path and packed key width of every block-diagonal D from V_D,
         // the largest over I of V over [16I + 1, min(16(I + D + 1), L)].  With
         // PP and B the sums of P and of u_b up to a stage,
@@ -206,27 +230,56 @@ __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ pa
     }
     int32_t *gn = w.gnone + (int64_t)c * rows;
     int32_t *ga = w.gall + (int64_t)c * rows;
+    int32_t *gs = w.gsat + (int64_t)c * rows;
     const int64_t first = r.wa[s - 1] + r.of[s - 1];
     const int64_t bwd = r.wa[s - 1] + r.wabar[s - 1] + r.ob[s - 1];
     const int64_t fpart = r.wabar[s - 1] + r.of[s - 1];
     int64_t carry = 0;  // max over s < j < t0 of w_a^{j-1} + w_a^j + o_f^j
+    // G(s, t) = max over s <= j <= t of m_all(j, t) + R(j), with
+    // R(j) = sum_{s <= i < j} w_abar^i and m_all(j, t) = max(w_a^t + A_j, B_j),
+    // A_j = w_abar^j + o_f^j, B_j = w_a^j + w_abar^j + o_b^j: so
+    // G(s, t) = max(w_a^t + max_j (A_j + R(j)), max_j (B_j + R(j))), two
+    // running maxima along t like the one of m_none (-1: none yet; every term
+    // is >= 0 in the domain)
+    int64_t car_r = 0, car_a = -1, car_b = -1;
     int64_t row = row_of(L, s, s);
     for (int t0 = s; t0 <= L; t0 += 64, row += 64) {
         const int t = t0 + lane;
+        const bool in = t <= L;
         // the term of j = t - 1, which m_none(s, t) includes when s < t - 1
-        int64_t incl = t <= L && t >= s + 2 ? r.wa[t - 3] + r.wa[t - 2] + r.of[t - 2] : 0;
+        int64_t incl = in && t >= s + 2 ? r.wa[t - 3] + r.wa[t - 2] + r.of[t - 2] : 0;
+        const int64_t wab_t = in ? r.wabar[t - 1] : 0;
+        int64_t rsum = wab_t;  // becomes sum_{t0 <= i <= t} w_abar^i
         for (int off = 1; off < 64; off *= 2) {
-            const int64_t v = __shfl_up(incl, off);
-            if (lane >= off)
+            const int64_t v = __shfl_up(incl, off), vr = __shfl_up(rsum, off);
+            if (lane >= off) {
                 incl = max(incl, v);
+                rsum += vr;
+            }
         }
+        const int64_t rt = car_r + rsum - wab_t;  // R(t)
+        int64_t ma = in ? wab_t + r.of[t - 1] + rt : -1;
+        int64_t mb = in ? r.wa[t - 1] + wab_t + r.ob[t - 1] + rt : -1;
+        for (int off = 1; off < 64; off *= 2) {
+            const int64_t va = __shfl_up(ma, off), vb = __shfl_up(mb, off);
+            if (lane >= off) {
+                ma = max(ma, va);
+                mb = max(mb, vb);
+            }
+        }
+        ma = max(car_a, ma);
+        mb = max(car_b, mb);
         const int64_t jmax = max(carry, incl);
-        if (t <= L) {
+        if (in) {
             const int64_t wt = r.wa[t - 1];
             ga[row + lane] = clamp32(max(wt + fpart, bwd));
             gn[row + lane] = t > s ? clamp32(wt + max(first, jmax)) : 0;
+            gs[row + lane] = clamp32(max(wt + ma, mb));
         }
         carry = max(carry, __shfl(incl, 63));
+        car_r += __shfl(rsum, 63);
+        car_a = __shfl(ma, 63);
+        car_b = __shfl(mb, 63);
     }
 }
 
@@ -507,10 +560,30 @@ struct MixedRunNB<XL, YL, 0, NB> {
 // copy, where the rows (s'+1, t) are 16 rows apart.
 template <class P, bool H>
 __device__ __forceinline__ void diag_body(const ChainRows &r, const ChainWork &cw, int L, int M, int m0, int64_t pitch,
-                                          int s, int t, int64_t *tab, int16_t *dtab)
+                                          int s, int t, bool sat, int64_t *tab, int16_t *dtab)
 {
     constexpr int NB = kEdgeBudgets;
     const int64_t cell = row_of(L, s, t);
+    // the final stores of budget set b, with the 2-byte copy of a diagonal
+    // block's cell
+    auto store = [&](int b, const typename P::Acc &a) {
+        const int mb = m0 + b * kEdgeThreads;
+        if (mb <= M) {
+            store_cell<P>(tab, dtab, cw.shadow, cell * pitch + mb, a);
+            if constexpr (P::kShadow) {
+                if (cw.diag16() && block_diag(s, t) == 0)
+                    cw.half_row(s, t)[mb] = P::finite(a) ? (int16_t)P::value(a) : (int16_t)-1;
+            }
+        }
+    };
+    // every budget of the workgroup saturated
+    if (sat) {
+        const typename P::Acc a = P::all_only(least_time(cw, s, t));
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+            store(b, a);
+        return;
+    }
     // the lane's budgets m0 + b * kEdgeThreads; those past M load budget M
     // and store nothing
     int m[NB];
@@ -553,14 +626,7 @@ __device__ __forceinline__ void diag_body(const ChainRows &r, const ChainWork &c
             P::init(acc[b]);
         if (all_ok[b])
             P::relax_all(acc[b], c2[b], ufub);
-        const int mb = m0 + b * kEdgeThreads;
-        if (mb <= M) {
-            store_cell<P>(tab, dtab, cw.shadow, cell * pitch + mb, acc[b]);
-            if constexpr (P::kShadow) {
-                if (cw.diag16() && block_diag(s, t) == 0)
-                    cw.half_row(s, t)[mb] = P::finite(acc[b]) ? (int16_t)P::value(acc[b]) : (int16_t)-1;
-            }
-        }
+        store(b, acc[b]);
     }
 }
 
@@ -583,12 +649,15 @@ __global__ __launch_bounds__(kEdgeThreads) void diag_kernel(const int64_t *__res
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
     const int D = block_diag(s, t);
-    if (!cw.narrow(D))
-        diag_body<Wide, false>(r, cw, L, M, m0, pitch, s, t, tab, dtab);
-    else if (D == 0 && cw.diag16())
-        diag_body<Narrow, true>(r, cw, L, M, m0, pitch, s, t, tab, dtab);
+    // the path and the saturation test first: their scalar loads go together
+    const bool narrow = cw.narrow(D), d16 = cw.diag16();
+    const bool sat = saturated(r, cw, s, row_of(L, s, t), blockIdx.x * (kEdgeThreads * kEdgeBudgets));
+    if (!narrow)
+        diag_body<Wide, false>(r, cw, L, M, m0, pitch, s, t, sat, tab, dtab);
+    else if (D == 0 && d16)
+        diag_body<Narrow, true>(r, cw, L, M, m0, pitch, s, t, sat, tab, dtab);
     else
-        diag_body<Narrow, false>(r, cw, L, M, m0, pitch, s, t, tab, dtab);
+        diag_body<Narrow, false>(r, cw, L, M, m0, pitch, s, t, sat, tab, dtab);
 }
 
 // Streamed order for the longer diagonals: the d splits of each pair are
@@ -599,11 +668,19 @@ __global__ __launch_bounds__(kEdgeThreads) void diag_kernel(const int64_t *__res
 // each with a quarter of the dependent loads.
 template <class P>
 __device__ __forceinline__ void diag_split_body(const ChainRows &r, const ChainWork &cw, int L, int M, int m,
-                                                int64_t pitch, int s, int t, int wave, int64_t (*part)[64],
+                                                int64_t pitch, int s, int t, int wave, bool sat, int64_t (*part)[64],
                                                 int64_t *tab, int16_t *dtab)
 {
     const int mc = m <= M ? m : M;  // lanes past M load in bounds and store nothing
     const int lane = threadIdx.x & 63;
+    const int64_t cell = row_of(L, s, t);
+    // every budget of the workgroup saturated (the same test in its four
+    // waves, so all of them leave before the barrier)
+    if (sat) {
+        if (wave == 0 && m <= M)
+            store_cell<P>(tab, dtab, cw.shadow, cell * pitch + m, P::all_only(least_time(cw, s, t)));
+        return;
+    }
     const int d = t - s;
     const int chunk = (d + 3) / 4;
     const int k0 = s + wave * chunk;
@@ -623,7 +700,6 @@ __device__ __forceinline__ void diag_split_body(const ChainRows &r, const ChainW
 #pragma unroll
     for (int v = 1; v < 4; ++v)
         P::merge_later(acc, part[v][lane]);
-    const int64_t cell = row_of(L, s, t);
     const int ri = m - r.wabar[s - 1];
     const bool all_ok = m >= cw.gall[cell] && ri >= 0;
     const int64_t below = row_of(L, s + 1, t) * pitch;
@@ -650,10 +726,12 @@ __global__ __launch_bounds__(256) void diag_split_kernel(const int64_t *__restri
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
-    if (cw.narrow(block_diag(s, t)))
-        diag_split_body<Narrow>(r, cw, L, M, m, pitch, s, t, wave, part, tab, dtab);
+    const bool narrow = cw.narrow(block_diag(s, t));
+    const bool sat = saturated(r, cw, s, row_of(L, s, t), blockIdx.x * 64);
+    if (narrow)
+        diag_split_body<Narrow>(r, cw, L, M, m, pitch, s, t, wave, sat, part, tab, dtab);
     else
-        diag_split_body<Wide>(r, cw, L, M, m, pitch, s, t, wave, part, tab, dtab);
+        diag_split_body<Wide>(r, cw, L, M, m, pitch, s, t, wave, sat, part, tab, dtab);
 }
 
 // The corner cell (16I + 16, 16J + 1) of a block (I, J) has no low or high
@@ -761,6 +839,37 @@ __device__ __forceinline__ void ring_wait(int later)
     }
 }
 
+// Whether the middle products of block (I, J) at the 64 budgets from `base`
+// are needed by no cell: every cell of the block is saturated (head of this
+// file) at every budget of the edge workgroups that hold those budgets, from
+// the first budget of a 128-budget edge workgroup on (the row edges' 64-budget
+// workgroups start no lower), so the edges store least times there without
+// reading a middle partial.  In the domain G(s, t) >= G(s + 1, t), so the
+// block's first row bounds the others.  Uniform over the workgroup.
+__device__ inline bool block_saturated(const ChainRows &r, const ChainWork &cw, int L, int I, int J, int base)
+{
+    const int b = base & ~(kEdgeThreads * kEdgeBudgets - 1);
+    const int s = I * kT + 1;  // block I is whole: J > I
+    const const_i32 g = (const_i32)cw.gsat;
+    bool ok = true;
+#pragma unroll
+    for (int i = 0; i < kT; ++i) {
+        const int t = min(J * kT + 1 + i, L);
+        ok &= (r.uf[s + i - 1] > 0) & (b >= g[row_of(L, s, t)]);
+    }
+    return ok;
+}
+
+// The corner cell of block (I, J) at budget m when its block is saturated:
+// the least time and C_2, stored by the middle kernel that finishes corners.
+template <class P>
+__device__ inline void store_saturated_corner(const ChainWork &cw, int L, int m, int64_t pitch, int I, int J,
+                                              int64_t *tab, int16_t *dtab)
+{
+    const int s = (I + 1) * kT, t = J * kT + 1;
+    store_cell<P>(tab, dtab, cw.shadow, row_of(L, s, t) * pitch + m, P::all_only(least_time(cw, s, t)));
+}
+
 // The partial slots of the cells of every block of block-diagonal delta, set
 // to infinity before a cut middle range merges into them: the packed key in
 // the compact copy, or the stored form in the cost table.
@@ -817,13 +926,19 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     const int kb = min(k_hi, ka + part_len - 1);
     if (ka > kb)
         return;
+    const ChainRows r = chain_rows(params, w, L, c);
+    if (block_saturated(r, cw, L, I, J, m - lane)) {
+        if (n_part == 1 && wave == 0 && m <= M)
+            store_saturated_corner<Narrow>(cw, L, m, pitch, I, J, cost + (int64_t)c * rows * pitch,
+                                           dec + (int64_t)c * rows * pitch);
+        return;
+    }
     const int s0 = I * kT + (wave >> 1) * kSub + 1;
     const int t0 = J * kT + (wave & 1) * kSub + 1;
     const int nt = t0 <= L ? min(kSub, L - t0 + 1) : 0;
     // key split bits: the whole range's, or those of a run of 2^S splits
     const int S = full ? (k_hi > k_lo ? 32 - __clz(k_hi - k_lo) : 0) : cw.pbits[delta];
     const int R = full ? INT_MAX : 1 << S;  // splits per run, a multiple of kStage
-    const ChainRows r = chain_rows(params, w, L, c);
     const int mc = m <= M ? m : M;
     const int n_stages = (kb - ka + kStage) / kStage;
 
@@ -1276,6 +1391,15 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
     const ChainRows r = chain_rows(params, w, L, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
+    if (block_saturated(r, cw, L, I, J, m - (threadIdx.x & 63))) {
+        if (n_part == 1 && wave == 0 && m <= M) {
+            if (cw.narrow(delta))
+                store_saturated_corner<Narrow>(cw, L, m, pitch, I, J, tab, dtab);
+            else
+                store_saturated_corner<Wide>(cw, L, m, pitch, I, J, tab, dtab);
+        }
+        return;
+    }
     if (cw.narrow(delta))
         middle_lds_body<Narrow, true>(r, cw, L, M, m, pitch, I, J, wave, ka, kb, k_lo, k_hi, n_part, tab, dtab, ring);
     else if (cw.f64_keys(delta))
@@ -1292,10 +1416,21 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
 // 2-byte copy.
 template <class P, bool H>
 __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &cw, int L, int M, int m0, int64_t pitch,
-                                          int s, int t, int k_lo, int k_hi, int64_t *tab, int16_t *dtab)
+                                          int s, int t, int k_lo, int k_hi, bool sat, int64_t *tab, int16_t *dtab)
 {
     constexpr int NB = kEdgeBudgets;
     const int64_t cell = row_of(L, s, t);
+    // every budget of the workgroup saturated
+    if (sat) {
+        const typename P::Acc a = P::all_only(least_time(cw, s, t));
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const int mb = m0 + b * kEdgeThreads;
+            if (mb <= M)
+                store_cell<P>(tab, dtab, cw.shadow, cell * pitch + mb, a);
+        }
+        return;
+    }
     // the lane's budgets m0 + b * kEdgeThreads; those past M load budget M
     // and store nothing
     int m[NB];
@@ -1394,12 +1529,15 @@ __global__ __launch_bounds__(kEdgeThreads) void edge_kernel(const int64_t *__res
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
-    if (!cw.narrow(delta))
-        edge_body<Wide, false>(r, cw, L, M, m0, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
-    else if (cw.diag16())
-        edge_body<Narrow, true>(r, cw, L, M, m0, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
+    // the path and the saturation test first: their scalar loads go together
+    const bool narrow = cw.narrow(delta), d16 = cw.diag16();
+    const bool sat = saturated(r, cw, s, row_of(L, s, t), blockIdx.x * (kEdgeThreads * kEdgeBudgets));
+    if (!narrow)
+        edge_body<Wide, false>(r, cw, L, M, m0, pitch, s, t, (I + 1) * kT, J * kT, sat, tab, dtab);
+    else if (d16)
+        edge_body<Narrow, true>(r, cw, L, M, m0, pitch, s, t, (I + 1) * kT, J * kT, sat, tab, dtab);
     else
-        edge_body<Narrow, false>(r, cw, L, M, m0, pitch, s, t, (I + 1) * kT, J * kT, tab, dtab);
+        edge_body<Narrow, false>(r, cw, L, M, m0, pitch, s, t, (I + 1) * kT, J * kT, sat, tab, dtab);
 }
 
 hipError_t check() { return hipGetLastError(); }
@@ -1424,10 +1562,12 @@ Work work_view(void *base, int n_chains, int L, int64_t pitch)
     char *b = (char *)base;
     Work w;
     w.pre = (int64_t *)(b + wl.pre);
+    w.preall = (int64_t *)(b + wl.preall);
     w.pbits = (int32_t *)(b + wl.pbits);
     w.bsum = (int64_t *)(b + wl.bsum);
     w.gnone = (int32_t *)(b + wl.gnone);
     w.gall = (int32_t *)(b + wl.gall);
+    w.gsat = (int32_t *)(b + wl.gsat);
     w.status = (int32_t *)(b + wl.status);
     w.shift = (int32_t *)(b + wl.shift);
     w.shadow = (uint32_t *)(b + wl.shadow);

@@ -25,11 +25,13 @@ WorkLayout work_layout(int n_chains, int L, int64_t pitch)
     const uint64_t nb = (uint64_t)((L + kBlock - 1) / kBlock);
     WorkLayout wl;
     wl.pre = 0;
-    wl.pbits = align(wl.pre + 8ull * nc * (uint64_t)(L + 1));
+    wl.preall = align(wl.pre + 8ull * nc * (uint64_t)(L + 1));
+    wl.pbits = align(wl.preall + 8ull * nc * (uint64_t)(L + 1));
     wl.bsum = align(wl.pbits + 4ull * nc * nb);
     wl.gnone = align(wl.bsum + 16ull * nc * (nb + 1));
     wl.gall = align(wl.gnone + 4ull * nc * rows);
-    wl.status = align(wl.gall + 4ull * nc * rows);
+    wl.gsat = align(wl.gall + 4ull * nc * rows);
+    wl.status = align(wl.gsat + 4ull * nc * rows);
     wl.shift = align(wl.status + 4ull * nc);
     wl.shadow = align(wl.shift + 8ull * nc * (uint64_t)L);
     wl.half = align(wl.shadow + 4ull * nc * rows * (uint64_t)pitch);

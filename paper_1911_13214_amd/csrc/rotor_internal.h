@@ -21,19 +21,23 @@ struct Tables {
     int64_t rows;           // L(L+1)/2
 };
 
-// Device workspace of a fill: prefix sums of u_f, per block-diagonal value
-// path and packed key width and the sums they are computed from, the gates
-// m_none and m_all of every pair, a domain status word per chain, the sizes
+// Device workspace of a fill: prefix sums of u_f and of u_f + u_b, per
+// block-diagonal value path and packed key width and the sums they are
+// computed from, the gates m_none and m_all of every pair and the budget
+// G(s, t) from which C_2 reaches the least time (rotor_fill.hip), a domain
+// status word per chain, the sizes
 // by which operand budgets are shifted (clamped, see prep_kernel), a compact
 // uint32 copy of the cost table (written and read by the pairs whose costs
 // stay below 2^32 - 1), and a 2-byte copy of the cells of the diagonal blocks
 // (chains whose costs there stay below 2^15).
 struct Work {
     int64_t *pre;      // [n_chains][L + 1]
+    int64_t *preall;   // [n_chains][L + 1]: prefix sums of u_f + u_b
     int32_t *pbits;    // [n_chains][nb], nb = ceil(L / 16): packed key bits of block-diagonal D, -1: 64-bit path
     int64_t *bsum;     // [n_chains][2][nb + 1]: sums of prefix sums of u_f, and of u_b, to block ends
     int32_t *gnone;    // [n_chains][rows]
     int32_t *gall;     // [n_chains][rows]
+    int32_t *gsat;     // [n_chains][rows]: G(s, t), clamped like the gates
     int32_t *status;   // [n_chains]: ROTOR_OK, or ROTOR_EDOMAIN if the chain's parameters are outside the domain
     int32_t *shift;    // [n_chains][2][L]: w_a and w_abar of every stage, clamped into [0, M + 1]
     uint32_t *shadow;  // [n_chains][rows][pitch]

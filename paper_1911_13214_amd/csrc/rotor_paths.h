@@ -85,8 +85,10 @@ __device__ inline uint64_t umin(uint64_t a, uint64_t b) { return b < a ? b : a; 
 // Per-chain views of the workspace.
 struct ChainWork {
     const int64_t *pre;    // [L+1] prefix sums of u_f
+    const int64_t *preall; // [L+1] prefix sums of u_f + u_b
     const int32_t *gnone;  // [rows] m_none(s, t), t > s
     const int32_t *gall;   // [rows] m_all(s, t)
+    const int32_t *gsat;   // [rows] G(s, t), the budget from which C_2 reaches the least time
     uint32_t *shadow;      // [rows][pitch] compact copy of the costs (narrow block-diagonals)
     const int32_t *pbits;  // [nb] per block-diagonal D: the largest S with (V_D + 1) << S <= 2^32 - 1,
                            // or, if V_D >= 2^32 - 1 (64-bit path), -2 while V_D < 2^38, else -1
@@ -116,8 +118,10 @@ __device__ inline ChainWork chain_work(const Work &w, int L, int64_t rows, int64
 {
     ChainWork cw;
     cw.pre = w.pre + (int64_t)c * (L + 1);
+    cw.preall = w.preall + (int64_t)c * (L + 1);
     cw.gnone = w.gnone + (int64_t)c * rows;
     cw.gall = w.gall + (int64_t)c * rows;
+    cw.gsat = w.gsat + (int64_t)c * rows;
     cw.shadow = w.shadow + (int64_t)c * rows * pitch;
     cw.pbits = w.pbits + (int64_t)c * ((L + kT - 1) / kT);
     cw.hpitch = half_pitch_of(pitch);
@@ -171,6 +175,8 @@ struct Wide {
     // fold in the stored() form of a result over larger splits
     __device__ static void merge_later(Acc &a, int64_t later) { a.key = umin(a.key, (uint64_t)later); }
     __device__ static bool finite(const Acc &a) { return a.key < (1ull << 62); }
+    // the result of a cell whose C_2 alone reaches the finite value v
+    __device__ static Acc all_only(int64_t v) { return {((uint64_t)v << 16) | kAllSplit}; }
     __device__ static int64_t value(const Acc &a) { return (int64_t)(a.key >> 16); }
     __device__ static uint32_t split(const Acc &a) { return (uint32_t)(a.key & 0xFFFF); }
 };
@@ -230,6 +236,7 @@ struct Narrow {
         a.sp = b ? (uint32_t)later : a.sp;
     }
     __device__ static bool finite(const Acc &a) { return a.val != kInf32; }
+    __device__ static Acc all_only(int64_t v) { return {(uint32_t)v, kAllSplit}; }
     __device__ static int64_t value(const Acc &a) { return (int64_t)a.val; }
     __device__ static uint32_t split(const Acc &a) { return a.sp; }
 };
@@ -256,6 +263,25 @@ __device__ inline void store_cell(int64_t *cost, int16_t *dec, uint32_t *shadow,
         cost[idx] = v;
         dec[idx] = d;
     }
+}
+
+// Saturated budgets (head of rotor_fill.hip): whether every budget from
+// `base` on of the pair (s, t), whose row is `cell`, has the least time as
+// its cost and C_2 as its decision.  Uniform over a wave when base is.
+__device__ inline bool saturated(const ChainRows &r, const ChainWork &cw, int s, int64_t cell, int base)
+{
+    // both loads unconditional, so that they are issued together
+    const int64_t uf = r.uf[s - 1];
+    const int32_t g = ((const_i32)cw.gsat)[cell];
+    return (uf > 0) & (base >= g);
+}
+
+// The least time of the pair (s, t): every stage forward once and backward
+// once, sum_{j=s}^{t} (u_f^j + u_b^j).
+__device__ inline int64_t least_time(const ChainWork &cw, int s, int t)
+{
+    const const_i64 pa = (const_i64)cw.preall;
+    return pa[t] - pa[s - 1];
 }
 
 // Operand loads of the narrow path from the compact copy (4 bytes) or from

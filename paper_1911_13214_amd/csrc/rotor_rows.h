@@ -270,6 +270,32 @@ __global__ __launch_bounds__(kEdgeThreads) void edge_row_kernel(const int64_t *_
     const ChainWork cw = chain_work(w, L, rows, pitch, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
+    // every budget of the workgroup saturated in every cell of the row
+    // (head of rotor_fill.hip): least times and C_2, nothing loaded
+    if (r.uf[s - 1] > 0) {
+        const int base = blockIdx.x * (kEdgeThreads * kRowBudgets);
+        const const_i32 gsat = (const_i32)cw.gsat;
+        bool all = true;
+        for (int t = t_first; t <= t_last; ++t)
+            all = all && base >= gsat[row_of(L, s, t)];
+        if (all) {
+            for (int t = t_first; t <= t_last; ++t) {
+                const int64_t idx = row_of(L, s, t) * pitch;
+                const int64_t lt = least_time(cw, s, t);
+#pragma unroll
+                for (int b = 0; b < kRowBudgets; ++b) {
+                    const int mb = m0 + b * kEdgeThreads;
+                    if (mb > M)
+                        continue;
+                    if (cw.narrow(delta))
+                        store_cell<Narrow>(tab, dtab, cw.shadow, idx + mb, Narrow::all_only(lt));
+                    else
+                        store_cell<Wide>(tab, dtab, cw.shadow, idx + mb, Wide::all_only(lt));
+                }
+            }
+            return;
+        }
+    }
     const bool packed = middle_packed(cw, delta, (delta - 1) * kT);
     if (!cw.narrow(delta))
         row_body<Wide, false, false, A>(r, cw, L, M, m0, pitch, s, J, t_first, t_last, tab, dtab);

@@ -72,17 +72,17 @@ def test_layout_rejects_bad_sizes(args):
 def test_workspace_size(n_chains, L, M):
     pitch, rows, cb, db = rotor.rotor_layout(n_chains, L, M)
     ws = rotor.rotor_workspace_bytes(n_chains, L, M)
-    # a 4-byte copy of every cell plus per-pair gates and per-stage prefixes,
-    # per block of 16 stages a key width and two sums, per chain a status
-    # word and two 4-byte shift sizes per stage, and (two blocks or more) a
-    # 2-byte copy of the diagonal blocks: 16 rows per stage of pitch rounded
-    # to 64
+    # a 4-byte copy of every cell plus three per-pair budgets (two gates and
+    # the saturation budget) and two per-stage prefixes, per block of 16
+    # stages a key width and two sums, per chain a status word and two 4-byte
+    # shift sizes per stage, and (two blocks or more) a 2-byte copy of the
+    # diagonal blocks: 16 rows per stage of pitch rounded to 64
     nb = (L + 15) // 16
     half = 2 * n_chains * L * 16 * ((pitch + 63) // 64 * 64) if nb >= 2 else 0
-    need = n_chains * rows * (4 * pitch + 8) + n_chains * 8 * (L + 1) + n_chains * (4 * nb + 16 * (nb + 1)) + half
+    need = n_chains * rows * (4 * pitch + 12) + n_chains * 16 * (L + 1) + n_chains * (4 * nb + 16 * (nb + 1)) + half
     need += n_chains * (4 + 8 * L)
     assert ws >= need
-    assert ws <= need + 10 * 256
+    assert ws <= need + 12 * 256
     assert ws % 256 == 0
 
 

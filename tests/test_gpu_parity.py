@@ -562,6 +562,27 @@ def test_value_paths_at_their_limits(bound, edges):
     assert_same(p, M, cost, dec)
 
 
+@pytest.mark.parametrize("schedule", SCHEDULES)
+def test_saturated_budgets(schedule):
+    # From G(s, t) on (the peak of storing every activation) a cell holds the
+    # least time sum(u_f + u_b), and C_2 when u_f^s > 0: the kernels store
+    # that without loading operands, by edge workgroup of 128 budgets, by row
+    # of 64 and by middle block.  Here G spreads over the whole budget range
+    # (pairs of 2 to 100 stages, M = 999), crossing the workgroups' bounds;
+    # the second chain has u_f = 0 on about one stage in five, where C_1 can
+    # tie C_2 and no shortcut applies; the third has every size 0 but one.
+    L, M = 100, 999
+    p = chaingen.random_chains(3, L, seed=77)
+    rng = np.random.default_rng(77)
+    p[1, chaingen.UF, rng.random(L) < 0.2] = 0
+    p[2, chaingen.WA:] = 0
+    p[2, chaingen.WABAR, 50] = 7
+    say(f"saturated budgets L={L} M={M} {schedule}")
+    _, cost, dec = solve_on_gpu(p, M, schedule=schedule)
+    for c in range(3):
+        assert_same(p, M, cost, dec, c)
+
+
 @pytest.mark.parametrize("v0", [32752, 32766, 32767, 32768, 33600])
 @pytest.mark.parametrize("edges", EDGE_ORDERS)
 def test_two_byte_copy_of_the_diagonal_blocks_at_its_limit(v0, edges):

@@ -159,6 +159,62 @@ def test_no_recomputation_closed_form(cfg):
     assert checked > 0
 
 
+def saturation_budgets(params):
+    """G(s, t) = max(m_all(s, t), G(s+1, t) + w_abar^s), G(t, t) = m_all(t, t):
+    the budget from which C_2 reaches the least time (the fill's saturated
+    budgets), with m_all(s, t) = max(w_a^t + w_abar^s + o_f^s,
+    w_a^s + w_abar^s + o_b^s), Section 4.2."""
+    uf, ub, wa, wab, of, ob = (params[0, r].astype(np.int64) for r in range(6))
+    L = params.shape[-1]
+    G = {}
+    for t in range(1, L + 1):
+        for s in range(t, 0, -1):
+            m_all = max(wa[t - 1] + wab[s - 1] + of[s - 1], wa[s - 1] + wab[s - 1] + ob[s - 1])
+            G[s, t] = m_all if s == t else max(m_all, G[s + 1, t] + wab[s - 1])
+    return G
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_saturation_budgets_are_the_store_all_peak(cfg):
+    # the recursion equals the peak of the schedule that stores every
+    # activation (F_all^s .. F_all^t, B^t .. B^s), replayed by the simulator
+    params, L, M, _, _ = chaingen.config(cfg)
+    ch = model.Chain(params)
+    G = saturation_budgets(params)
+    for s in range(1, L + 1):
+        for t in range(s, L + 1):
+            assert G[s, t] == model.all_fall_peak(ch, s, t), (s, t)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_saturated_budgets_take_c2(seed):
+    # From G(s, t) on the cost is the least time sum(u_f + u_b) whatever the
+    # u_f (C_2 reaches it, nothing goes lower); with u_f^s > 0 every C_1
+    # candidate runs stage s forward twice, so the decision is C_2 (0).  Zero
+    # u_f on some stages lets C_1 tie there.
+    rng = np.random.default_rng(seed)
+    L, M = int(rng.integers(2, 30)), int(rng.integers(50, 400))
+    params = chaingen.random_chains(1, L, seed=400 + seed)
+    if seed % 2:
+        params[0, 0, rng.random(L) < 0.4] = 0
+    C, D = orc.solve(params, M)
+    G = saturation_budgets(params)
+    lt = np.concatenate([[0], np.cumsum(params[0, 0] + params[0, 1])])
+    checked = decided = 0
+    for s in range(1, L + 1):
+        for t in range(s, L + 1):
+            g = G[s, t]
+            if g > M:
+                continue
+            r = orc.row(L, s, t)
+            assert (C[r, g:] == lt[t] - lt[s - 1]).all(), (s, t)
+            checked += 1
+            if params[0, 0, s - 1] > 0:
+                assert (D[r, g:] == 0).all(), (s, t)
+                decided += 1
+    assert checked > 0 and decided > 0
+
+
 @pytest.mark.parametrize("cfg", [1, 2, 3])
 def test_feasibility_threshold(cfg):
     params, L, M, _, _ = chaingen.config(cfg)
