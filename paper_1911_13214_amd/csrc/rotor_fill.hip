@@ -231,6 +231,18 @@ __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ pa
     int32_t *gn = w.gnone + (int64_t)c * rows;
     int32_t *ga = w.gall + (int64_t)c * rows;
     int32_t *gs = w.gsat + (int64_t)c * rows;
+    // The last row s = 16(I + 1) of a block I holds the least G of each
+    // block (I, J), J > I (G(s, t) >= G(s + 1, t) in the domain), and its
+    // first row s = 16I + 1 the largest: reduced per block J in LDS.
+    __shared__ int32_t seg[(ROTOR_MAX_L + kT - 1) / kT];
+    const int nb = (L + kT - 1) / kT;
+    const int I = (s - 1) / kT;
+    const bool last_row = s % kT == 0 && I + 1 < nb, first_row = s % kT == 1 && I + 1 < nb;
+    if (last_row || first_row) {
+        for (int J = lane; J < nb; J += 64)
+            seg[J] = last_row ? INT32_MAX : INT32_MIN;
+        __syncthreads();
+    }
     const int64_t first = r.wa[s - 1] + r.of[s - 1];
     const int64_t bwd = r.wa[s - 1] + r.wabar[s - 1] + r.ob[s - 1];
     const int64_t fpart = r.wabar[s - 1] + r.of[s - 1];
@@ -272,14 +284,30 @@ __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ pa
         const int64_t jmax = max(carry, incl);
         if (in) {
             const int64_t wt = r.wa[t - 1];
+            const int32_t g = clamp32(max(wt + ma, mb));
             ga[row + lane] = clamp32(max(wt + fpart, bwd));
             gn[row + lane] = t > s ? clamp32(wt + max(first, jmax)) : 0;
-            gs[row + lane] = clamp32(max(wt + ma, mb));
+            gs[row + lane] = g;
+            const int J = (t - 1) / kT;
+            if (last_row && J > I)
+                atomicMin(&seg[J], g);
+            if (first_row && J > I)
+                atomicMax(&seg[J], g);
         }
         carry = max(carry, __shfl(incl, 63));
         car_r += __shfl(rsum, 63);
         car_a = __shfl(ma, 63);
         car_b = __shfl(mb, 63);
+    }
+    if (last_row || first_row) {
+        __syncthreads();
+        // the largest G bounds the block only where every row has u_f > 0
+        bool pos = true;
+        for (int i = 0; i < kT; ++i)
+            pos = pos && r.uf[I * kT + i] > 0;
+        int32_t *gb = w.gblk + ((int64_t)c * 2 + (first_row ? 1 : 0)) * nb * nb + (int64_t)I * nb;
+        for (int J = I + 1 + lane; J < nb; J += 64)
+            gb[J - I] = first_row && !pos ? INT32_MAX : seg[J];
     }
 }
 
@@ -844,20 +872,11 @@ __device__ __forceinline__ void ring_wait(int later)
 // file) at every budget of the edge workgroups that hold those budgets, from
 // the first budget of a 128-budget edge workgroup on (the row edges' 64-budget
 // workgroups start no lower), so the edges store least times there without
-// reading a middle partial.  In the domain G(s, t) >= G(s + 1, t), so the
-// block's first row bounds the others.  Uniform over the workgroup.
-__device__ inline bool block_saturated(const ChainRows &r, const ChainWork &cw, int L, int I, int J, int base)
+// reading a middle partial.  prep_kernel keeps the largest G of each block,
+// or INT32_MAX when some row has u_f = 0.  Uniform over the workgroup.
+__device__ inline bool block_saturated(const ChainWork &cw, int I, int J, int base)
 {
-    const int b = base & ~(kEdgeThreads * kEdgeBudgets - 1);
-    const int s = I * kT + 1;  // block I is whole: J > I
-    const const_i32 g = (const_i32)cw.gsat;
-    bool ok = true;
-#pragma unroll
-    for (int i = 0; i < kT; ++i) {
-        const int t = min(J * kT + 1 + i, L);
-        ok &= (r.uf[s + i - 1] > 0) & (b >= g[row_of(L, s, t)]);
-    }
-    return ok;
+    return (base & ~(kEdgeThreads * kEdgeBudgets - 1)) >= block_gmax(cw, I, J - I);
 }
 
 // The corner cell of block (I, J) at budget m when its block is saturated:
@@ -927,7 +946,7 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     if (ka > kb)
         return;
     const ChainRows r = chain_rows(params, w, L, c);
-    if (block_saturated(r, cw, L, I, J, m - lane)) {
+    if (block_saturated(cw, I, J, m - lane)) {
         if (n_part == 1 && wave == 0 && m <= M)
             store_saturated_corner<Narrow>(cw, L, m, pitch, I, J, cost + (int64_t)c * rows * pitch,
                                            dec + (int64_t)c * rows * pitch);
@@ -1391,7 +1410,7 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
     const ChainRows r = chain_rows(params, w, L, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
-    if (block_saturated(r, cw, L, I, J, m - (threadIdx.x & 63))) {
+    if (block_saturated(cw, I, J, m - (threadIdx.x & 63))) {
         if (n_part == 1 && wave == 0 && m <= M) {
             if (cw.narrow(delta))
                 store_saturated_corner<Narrow>(cw, L, m, pitch, I, J, tab, dtab);
@@ -1531,7 +1550,8 @@ __global__ __launch_bounds__(kEdgeThreads) void edge_kernel(const int64_t *__res
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
     // the path and the saturation test first: their scalar loads go together
     const bool narrow = cw.narrow(delta), d16 = cw.diag16();
-    const bool sat = saturated(r, cw, s, row_of(L, s, t), blockIdx.x * (kEdgeThreads * kEdgeBudgets));
+    const bool sat =
+        saturated_in_block(r, cw, I, delta, s, row_of(L, s, t), blockIdx.x * (kEdgeThreads * kEdgeBudgets));
     if (!narrow)
         edge_body<Wide, false>(r, cw, L, M, m0, pitch, s, t, (I + 1) * kT, J * kT, sat, tab, dtab);
     else if (d16)
@@ -1568,6 +1588,7 @@ Work work_view(void *base, int n_chains, int L, int64_t pitch)
     w.gnone = (int32_t *)(b + wl.gnone);
     w.gall = (int32_t *)(b + wl.gall);
     w.gsat = (int32_t *)(b + wl.gsat);
+    w.gblk = (int32_t *)(b + wl.gblk);
     w.status = (int32_t *)(b + wl.status);
     w.shift = (int32_t *)(b + wl.shift);
     w.shadow = (uint32_t *)(b + wl.shadow);

@@ -54,7 +54,7 @@ uint64_t table_elems(int32_t n_chains, int32_t L, int64_t M);
 // the shift sizes the fill reads, the compact uint32 copy of the cost table
 // and the 2-byte copy of the diagonal blocks' cells.
 struct WorkLayout {
-    uint64_t pre, preall, pbits, bsum, gnone, gall, gsat, status, shift, shadow, half, total;
+    uint64_t pre, preall, pbits, bsum, gnone, gall, gsat, gblk, status, shift, shadow, half, total;
 };
 WorkLayout work_layout(int n_chains, int L, int64_t pitch);
 

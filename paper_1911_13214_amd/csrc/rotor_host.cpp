@@ -31,7 +31,8 @@ WorkLayout work_layout(int n_chains, int L, int64_t pitch)
     wl.gnone = align(wl.bsum + 16ull * nc * (nb + 1));
     wl.gall = align(wl.gnone + 4ull * nc * rows);
     wl.gsat = align(wl.gall + 4ull * nc * rows);
-    wl.status = align(wl.gsat + 4ull * nc * rows);
+    wl.gblk = align(wl.gsat + 4ull * nc * rows);
+    wl.status = align(wl.gblk + 8ull * nc * nb * nb);
     wl.shift = align(wl.status + 4ull * nc);
     wl.shadow = align(wl.shift + 8ull * nc * (uint64_t)L);
     wl.half = align(wl.shadow + 4ull * nc * rows * (uint64_t)pitch);

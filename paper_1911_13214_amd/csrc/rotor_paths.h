@@ -89,6 +89,9 @@ struct ChainWork {
     const int32_t *gnone;  // [rows] m_none(s, t), t > s
     const int32_t *gall;   // [rows] m_all(s, t)
     const int32_t *gsat;   // [rows] G(s, t), the budget from which C_2 reaches the least time
+    const int32_t *gblk;   // [2][nb][nb] per block (I, I + D), D >= 1: least G of its cells, then the
+                           // largest (INT32_MAX if some row has u_f = 0)
+    int nb;
     uint32_t *shadow;      // [rows][pitch] compact copy of the costs (narrow block-diagonals)
     const int32_t *pbits;  // [nb] per block-diagonal D: the largest S with (V_D + 1) << S <= 2^32 - 1,
                            // or, if V_D >= 2^32 - 1 (64-bit path), -2 while V_D < 2^38, else -1
@@ -122,6 +125,8 @@ __device__ inline ChainWork chain_work(const Work &w, int L, int64_t rows, int64
     cw.gnone = w.gnone + (int64_t)c * rows;
     cw.gall = w.gall + (int64_t)c * rows;
     cw.gsat = w.gsat + (int64_t)c * rows;
+    cw.nb = (L + kT - 1) / kT;
+    cw.gblk = w.gblk + (int64_t)c * 2 * cw.nb * cw.nb;
     cw.shadow = w.shadow + (int64_t)c * rows * pitch;
     cw.pbits = w.pbits + (int64_t)c * ((L + kT - 1) / kT);
     cw.hpitch = half_pitch_of(pitch);
@@ -274,6 +279,25 @@ __device__ inline bool saturated(const ChainRows &r, const ChainWork &cw, int s,
     const int64_t uf = r.uf[s - 1];
     const int32_t g = ((const_i32)cw.gsat)[cell];
     return (uf > 0) & (base >= g);
+}
+
+// The least and the largest G of the cells of block (I, I + D), D >= 1.
+__device__ inline int32_t block_gmin(const ChainWork &cw, int I, int D)
+{
+    return ((const_i32)cw.gblk)[(int64_t)I * cw.nb + D];
+}
+__device__ inline int32_t block_gmax(const ChainWork &cw, int I, int D)
+{
+    return ((const_i32)cw.gblk)[((int64_t)cw.nb + I) * cw.nb + D];
+}
+
+// saturated() for a cell of block (I, I + D), D >= 1, tried only when some
+// cell of the block is saturated from `base` on: a block read by every
+// workgroup of the block, then the cell's own bound.
+__device__ inline bool saturated_in_block(const ChainRows &r, const ChainWork &cw, int I, int D, int s,
+                                          int64_t cell, int base)
+{
+    return base >= block_gmin(cw, I, D) && saturated(r, cw, s, cell, base);
 }
 
 // The least time of the pair (s, t): every stage forward once and backward

@@ -271,9 +271,10 @@ __global__ __launch_bounds__(kEdgeThreads) void edge_row_kernel(const int64_t *_
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
     // every budget of the workgroup saturated in every cell of the row
-    // (head of rotor_fill.hip): least times and C_2, nothing loaded
-    if (r.uf[s - 1] > 0) {
-        const int base = blockIdx.x * (kEdgeThreads * kRowBudgets);
+    // (head of rotor_fill.hip): least times and C_2, nothing loaded; tried
+    // only when some cell of the block is saturated there
+    const int base = blockIdx.x * (kEdgeThreads * kRowBudgets);
+    if (base >= block_gmin(cw, I, delta) && r.uf[s - 1] > 0) {
         const const_i32 gsat = (const_i32)cw.gsat;
         bool all = true;
         for (int t = t_first; t <= t_last; ++t)
