@@ -840,6 +840,9 @@ constexpr int kSplitWords = 2 * kT * 64;
 constexpr int kDmaPerSplit = 8;  // row copies per wave and split
 constexpr int kDmaPerStage = kDmaPerSplit * kStage;
 static_assert(kRing >= 2 && (kRing - 2) * kDmaPerStage <= 63, "vmcnt holds at most 63");
+// Stages of the packed kernel issue fewer copies where operand rows are
+// saturated, so its ring waits for all of them (vmcnt(0)): two stages.
+static_assert(kRing == 2, "middle_packed_kernel counts on a ring of two stages");
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef const __attribute__((address_space(1))) void global_void;
@@ -974,19 +977,76 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     int k_copy = ka;  // next split to copy
     uint32_t *const dst0 = ring + (copies_x ? wave * kSub : kT + (wave - 2) * kSub) * 64;
     int fill = 0;  // ring stage filled next
-    // copies of one stage; splits past kb copy split kb again, so every
-    // stage issues the same number of copies
+    // Saturated operand rows (head of this file): a row whose budgets here
+    // (shifted by w_a^k for Y) all lie at or above its G holds its least time
+    // at each of them, which the wave can write into the ring instead of
+    // copying the row.  X rows (first + i, k) are all saturated when the
+    // first is (G(s, k) >= G(s + 1, k)); this wave takes that for the splits
+    // ka .. kx, up to the first that is not.  Y rows (k + 1, t) for the
+    // splits ky .. kb, from the last split that is not: G(k + 1, t) falls as
+    // k grows.  Both bounds are found once, 64 splits per step.
+    const int base = m - lane;
+    const int first_c = min(first, L);
+    int kx = ka - 1, ky = kb + 1;
+    if (copies_x) {
+        const int32_t *g_row = cw.gsat + row_of(L, first, ka);  // G(first, k) at g_row[k - ka]
+        for (int k0 = ka; k0 <= kb; k0 += 64) {
+            const int k = k0 + lane;
+            const uint64_t bad = __ballot(k <= kb && g_row[k - ka] > base);
+            if (bad) {
+                kx = k0 + __ffsll((long long)bad) - 2;
+                break;
+            }
+            kx = min(kb, k0 + 63);
+        }
+    } else {
+        const int32_t *wa_v = w.shift + (int64_t)c * 2 * L;  // clamped w_a, as r.wa
+        for (int k0 = kb; k0 >= ka; k0 -= 64) {
+            const int k = k0 - lane;
+            bool bad = false;
+            if (k >= ka) {
+                const int32_t *g = cw.gsat + row_of(L, k + 1, first_c);
+                int32_t gm = g[0];
+#pragma unroll
+                for (int i = 1; i < kDmaPerSplit; ++i)
+                    gm = max(gm, g[min(first + i, L) - first_c]);
+                bad = base - wa_v[k - 1] < gm;
+            }
+            const uint64_t b = __ballot(bad);
+            if (b) {
+                ky = k0 - (__ffsll((long long)b) - 1) + 1;
+                break;
+            }
+            ky = max(ka, k0 - 63);
+        }
+    }
+    // the prefixes of u_f + u_b at the rows' other ends (X: s - 1, Y: t),
+    // 32 bits suffice for a least time below 2^32 - 1
+    const const_i64 pa = (const_i64)cw.preall;
+    uint32_t pfx[kDmaPerSplit];
+#pragma unroll
+    for (int i = 0; i < kDmaPerSplit; ++i)
+        pfx[i] = (uint32_t)pa[copies_x ? first + i - 1 : min(first + i, L)];
+    // copies of one stage (splits past kb copy split kb again); the ring's
+    // barrier waits for every copy and LDS write of the wave
     auto issue = [&]() {
         uint32_t *dst = dst0 + fill * (kStage * kSplitWords);
 #pragma unroll
         for (int p = 0; p < kStage; ++p) {
             const int k = k_copy;
-            const int ri = mc - r.wa[k - 1];
-            const uint32_t off = 4u * (uint32_t)(copies_x ? mc : (ri >= 0 ? ri : mc));
+            if (copies_x ? k <= kx : k >= ky) {
+                const uint32_t pk = (uint32_t)pa[k];
 #pragma unroll
-            for (int i = 0; i < kDmaPerSplit; ++i)
-                __builtin_amdgcn_global_load_lds((global_void *)(src[i] + off),
-                                                 (lds_void *)(dst + p * kSplitWords + i * 64), 4, 0, 0);
+                for (int i = 0; i < kDmaPerSplit; ++i)
+                    dst[p * kSplitWords + i * 64 + lane] = copies_x ? pk - pfx[i] : pfx[i] - pk;
+            } else {
+                const int ri = mc - r.wa[k - 1];
+                const uint32_t off = 4u * (uint32_t)(copies_x ? mc : (ri >= 0 ? ri : mc));
+#pragma unroll
+                for (int i = 0; i < kDmaPerSplit; ++i)
+                    __builtin_amdgcn_global_load_lds((global_void *)(src[i] + off),
+                                                     (lds_void *)(dst + p * kSplitWords + i * 64), 4, 0, 0);
+            }
             if (k < kb) {
                 // to split k + 1: X rows advance one row, Y rows L - k - 1 rows
                 const int64_t step = copies_x ? row_bytes : (int64_t)(L - k - 1) * row_bytes;
