@@ -237,7 +237,7 @@ __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ pa
     __shared__ int32_t seg[(ROTOR_MAX_L + kT - 1) / kT];
     const int nb = (L + kT - 1) / kT;
     const int I = (s - 1) / kT;
-    const bool last_row = s % kT == 0 && I + 1 < nb, first_row = s % kT == 1 && I + 1 < nb;
+    const bool last_row = s % kT == 0 && I + 1 < nb, first_row = s % kT == 1;
     if (last_row || first_row) {
         for (int J = lane; J < nb; J += 64)
             seg[J] = last_row ? INT32_MAX : INT32_MIN;
@@ -291,7 +291,7 @@ __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ pa
             const int J = (t - 1) / kT;
             if (last_row && J > I)
                 atomicMin(&seg[J], g);
-            if (first_row && J > I)
+            if (first_row)
                 atomicMax(&seg[J], g);
         }
         carry = max(carry, __shfl(incl, 63));
@@ -302,12 +302,23 @@ __global__ __launch_bounds__(64) void prep_kernel(const int64_t *__restrict__ pa
     if (last_row || first_row) {
         __syncthreads();
         // the largest G bounds the block only where every row has u_f > 0
+        const int rows_i = min(kT, L - I * kT);
         bool pos = true;
-        for (int i = 0; i < kT; ++i)
+        int64_t wmax = 0;
+        for (int i = 0; i < rows_i; ++i) {
             pos = pos && r.uf[I * kT + i] > 0;
+            wmax = max(wmax, r.wa[I * kT + i]);
+        }
         int32_t *gb = w.gblk + ((int64_t)c * 2 + (first_row ? 1 : 0)) * nb * nb + (int64_t)I * nb;
         for (int J = I + 1 + lane; J < nb; J += 64)
             gb[J - I] = first_row && !pos ? INT32_MAX : seg[J];
+        if (first_row && lane == 0) {
+            // the diagonal block I (D = 0): its largest G (values only, any
+            // u_f), and that plus the largest w_a of its stages in the other
+            // plane
+            gb[0] = seg[I];
+            w.gblk[(int64_t)c * 2 * nb * nb + (int64_t)I * nb] = clamp32((int64_t)seg[I] + wmax);
+        }
     }
 }
 
@@ -577,6 +588,66 @@ template <class XL, class YL, int NB>
 struct MixedRunNB<XL, YL, 0, NB> {
     __device__ __forceinline__ static void go(int, Narrow::Acc (&)[NB], const ChainRows &, const int (&)[NB], int,
                                               MixedCursor &, uint64_t &)
+    {
+    }
+};
+
+// relax_mixed_nb for a run whose X (CX) or Y (!CX) operands are saturated
+// rows (head of this file): each is the least time of its pair at every
+// budget here, pa[k] - pa_s (X = (s, k), pa_s = pa[s - 1]) or pa_s - pa[k]
+// (Y = (k + 1, t), pa_s = pa[t]), so only the other operand is loaded.  The
+// cursor moves as in relax_mixed_nb.
+template <class XL, class YL, bool CX, int N, int NB>
+__device__ __forceinline__ void relax_mixed_sat_nb(Narrow::Acc (&acc)[NB], const ChainRows &r, const int (&m)[NB],
+                                                   int k0, MixedCursor &cur, uint64_t &prefix, const_i64 pa,
+                                                   int64_t pa_s)
+{
+    uint32_t rv[N][NB], c[N];
+    int wa[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const int k = k0 + i;
+        wa[i] = r.wa[k - 1];
+        c[i] = (uint32_t)(CX ? pa[k] - pa_s : pa_s - pa[k]);
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const int ri = m[b] - wa[i];
+            if constexpr (CX)
+                rv[i][b] = YL::at(cur.y, ri >= 0 ? ri : m[b]);
+            else
+                rv[i][b] = XL::at(cur.x, m[b]);
+        }
+        cur.x += cur.xstep;
+        cur.y += cur.ystep;
+        cur.ystep -= cur.ydec;
+    }
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const int k = k0 + i;
+        prefix += (uint64_t)r.uf[k - 1];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const uint32_t rx = CX ? c[i] : rv[i][b], ry = CX ? rv[i][b] : c[i];
+            Narrow::relax(acc[b], Narrow::xop(rx, prefix, 0, m[b] >= wa[i]), ry, (uint32_t)(k + 1));
+        }
+    }
+}
+
+template <class XL, class YL, bool CX, int N, int NB>
+struct MixedSatRunNB {
+    __device__ __forceinline__ static void go(int n, Narrow::Acc (&acc)[NB], const ChainRows &r, const int (&m)[NB],
+                                              int k0, MixedCursor &cur, uint64_t &prefix, const_i64 pa, int64_t pa_s)
+    {
+        if (n == N)
+            relax_mixed_sat_nb<XL, YL, CX, N, NB>(acc, r, m, k0, cur, prefix, pa, pa_s);
+        else
+            MixedSatRunNB<XL, YL, CX, N - 1, NB>::go(n, acc, r, m, k0, cur, prefix, pa, pa_s);
+    }
+};
+template <class XL, class YL, bool CX, int NB>
+struct MixedSatRunNB<XL, YL, CX, 0, NB> {
+    __device__ __forceinline__ static void go(int, Narrow::Acc (&)[NB], const ChainRows &, const int (&)[NB], int,
+                                              MixedCursor &, uint64_t &, const_i64, int64_t)
     {
     }
 };
@@ -1516,6 +1587,12 @@ __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &c
 #pragma unroll
     for (int b = 0; b < NB; ++b)
         m[b] = min(m0 + b * kEdgeThreads, M);
+    // the diagonal-block operands saturated at every budget of the workgroup
+    // (from its first, lane 0's): X of the low splits in block I, Y of the
+    // high splits in block J (shifted by at most the block's largest w_a)
+    const int base = __builtin_amdgcn_readfirstlane(m0);
+    const bool xsat = base >= diag_block_gmax(cw, (s - 1) / kT);
+    const bool ysat = base >= diag_block_gyshift(cw, (t - 1) / kT);
     // loads that depend on nothing go first: the stored middle partial (a
     // packed key in the compact copy, or (value << 32) | s' in the cost
     // table) and the C_2 operand (the lane's own budget when C_2 is out of
@@ -1544,10 +1621,15 @@ __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &c
     uint64_t prefix = 0;
     const int64_t rb = pitch * 4, hb = cw.hpitch * 2;
     if constexpr (H) {
-        // X rows (s, k) of the 2-byte copy are consecutive
+        // X rows (s, k) of the 2-byte copy are consecutive; all saturated
+        // (xsat) when the largest G of diagonal block I is reached
         MixedCursor low{(const char *)cw.half_row(s, s), (const char *)(cw.shadow + row_of(L, s + 1, t) * pitch), hb,
                         (int64_t)(L - s - 1) * rb, rb};
-        MixedRunNB<Load16, Load32, kT - 1, NB>::go(k_lo - s, acc, r, m, s, low, prefix);
+        if (xsat)
+            MixedSatRunNB<Load16, Load32, true, kT - 1, NB>::go(k_lo - s, acc, r, m, s, low, prefix,
+                                                                 (const_i64)cw.preall, ((const_i64)cw.preall)[s - 1]);
+        else
+            MixedRunNB<Load16, Load32, kT - 1, NB>::go(k_lo - s, acc, r, m, s, low, prefix);
     } else {
         RowCursor low = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, s);
         relax_run_nb<P, NB>(acc, r, m, s, k_lo - s, low, prefix);
@@ -1567,10 +1649,16 @@ __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &c
     // high splits k = 16J + 1 .. t - 1: X from this block, Y from block (J, J)
     prefix += (uint64_t)(cw.pre[k_hi] - cw.pre[k_lo - 1]);
     if constexpr (H) {
-        // Y rows (k + 1, t) of the 2-byte copy are 16 rows apart
+        // Y rows (k + 1, t) of the 2-byte copy are 16 rows apart; all
+        // saturated (ysat) when the largest G of diagonal block J plus the
+        // largest w_a^k of its stages is reached
         MixedCursor high{(const char *)(cw.shadow + row_of(L, s, k_hi + 1) * pitch),
                          (const char *)cw.half_row(k_hi + 2, t), rb, kT * hb, 0};
-        MixedRunNB<Load32, Load16, kT - 1, NB>::go(t - k_hi - 1, acc, r, m, k_hi + 1, high, prefix);
+        if (ysat)
+            MixedSatRunNB<Load32, Load16, false, kT - 1, NB>::go(t - k_hi - 1, acc, r, m, k_hi + 1, high, prefix,
+                                                                  (const_i64)cw.preall, ((const_i64)cw.preall)[t]);
+        else
+            MixedRunNB<Load32, Load16, kT - 1, NB>::go(t - k_hi - 1, acc, r, m, k_hi + 1, high, prefix);
     } else {
         RowCursor high = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, k_hi + 1);
         relax_run_nb<P, NB>(acc, r, m, k_hi + 1, t - k_hi - 1, high, prefix);

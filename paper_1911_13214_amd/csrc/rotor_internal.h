@@ -39,7 +39,9 @@ struct Work {
     int32_t *gall;     // [n_chains][rows]
     int32_t *gsat;     // [n_chains][rows]: G(s, t), clamped like the gates
     int32_t *gblk;     // [n_chains][2][nb][nb]: per block (I, I + D), D >= 1, the least G of its
-                       // cells, then the largest (INT32_MAX if some row has u_f = 0)
+                       // cells, then the largest (INT32_MAX if some row has u_f = 0); per
+                       // diagonal block (D = 0) its largest G plus its largest w_a, then its
+                       // largest G
     int32_t *status;   // [n_chains]: ROTOR_OK, or ROTOR_EDOMAIN if the chain's parameters are outside the domain
     int32_t *shift;    // [n_chains][2][L]: w_a and w_abar of every stage, clamped into [0, M + 1]
     uint32_t *shadow;  // [n_chains][rows][pitch]

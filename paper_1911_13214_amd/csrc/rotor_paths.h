@@ -90,7 +90,8 @@ struct ChainWork {
     const int32_t *gall;   // [rows] m_all(s, t)
     const int32_t *gsat;   // [rows] G(s, t), the budget from which C_2 reaches the least time
     const int32_t *gblk;   // [2][nb][nb] per block (I, I + D), D >= 1: least G of its cells, then the
-                           // largest (INT32_MAX if some row has u_f = 0)
+                           // largest (INT32_MAX if some row has u_f = 0); D = 0: the diagonal block's
+                           // largest G plus its largest w_a, then its largest G
     int nb;
     uint32_t *shadow;      // [rows][pitch] compact copy of the costs (narrow block-diagonals)
     const int32_t *pbits;  // [nb] per block-diagonal D: the largest S with (V_D + 1) << S <= 2^32 - 1,
@@ -290,6 +291,11 @@ __device__ inline int32_t block_gmax(const ChainWork &cw, int I, int D)
 {
     return ((const_i32)cw.gblk)[((int64_t)cw.nb + I) * cw.nb + D];
 }
+
+// For the diagonal block I (D = 0): the largest G of its pairs, whatever
+// the u_f; and that plus the largest w_a of its stages.
+__device__ inline int32_t diag_block_gmax(const ChainWork &cw, int I) { return block_gmax(cw, I, 0); }
+__device__ inline int32_t diag_block_gyshift(const ChainWork &cw, int I) { return block_gmin(cw, I, 0); }
 
 // saturated() for a cell of block (I, I + D), D >= 1, tried only when some
 // cell of the block is saturated from `base` on: a block read by every
