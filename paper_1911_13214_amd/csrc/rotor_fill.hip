@@ -486,6 +486,75 @@ __device__ __forceinline__ void relax_run_nb(typename P::Acc (&acc)[NB], const C
         RelaxRunNB<P, kRun, NB>::go(n < kRun ? n : kRun, acc, r, m, k0, cur, prefix);
 }
 
+// relax_fixed_nb for a run whose X (CX) or Y (!CX) operands are saturated
+// rows (head of this file): each is the least time of its pair at every
+// budget here, pa[k] - pa_s (X = (s, k), pa_s = pa[s - 1]) or pa_s - pa[k]
+// (Y = (k + 1, t), pa_s = pa[t]), so only the other operand is loaded.  The
+// cursor moves as in relax_fixed_nb.
+template <class P, bool CX, int N, int NB>
+__device__ __forceinline__ void relax_sat_fixed_nb(typename P::Acc (&acc)[NB], const ChainRows &r,
+                                                   const int (&m)[NB], int k0, RowCursor &cur, uint64_t &prefix,
+                                                   const_i64 pa, int64_t pa_s)
+{
+    typename P::Raw rv[N][NB], c[N];
+    int wa[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const int k = k0 + i;
+        wa[i] = r.wa[k - 1];
+        c[i] = (typename P::Raw)(CX ? pa[k] - pa_s : pa_s - pa[k]);
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const int ri = m[b] - wa[i];
+            rv[i][b] = CX ? P::load_at(cur.y, ri >= 0 ? ri : m[b]) : P::load_at(cur.x, m[b]);
+        }
+        cur.x += cur.row_bytes;
+        cur.y += cur.ystep;
+        cur.ystep -= cur.row_bytes;
+    }
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const int k = k0 + i;
+        prefix += (uint64_t)r.uf[k - 1];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const typename P::Raw rx = CX ? c[i] : rv[i][b], ry = CX ? rv[i][b] : c[i];
+            P::relax(acc[b], P::xop(rx, prefix, (uint32_t)(k + 1), m[b] >= wa[i]), P::yop(ry), (uint32_t)(k + 1));
+        }
+    }
+}
+
+template <class P, bool CX, int N, int NB>
+struct RelaxSatRunNB {
+    __device__ __forceinline__ static void go(int n, typename P::Acc (&acc)[NB], const ChainRows &r,
+                                              const int (&m)[NB], int k0, RowCursor &cur, uint64_t &prefix,
+                                              const_i64 pa, int64_t pa_s)
+    {
+        if (n == N)
+            relax_sat_fixed_nb<P, CX, N, NB>(acc, r, m, k0, cur, prefix, pa, pa_s);
+        else
+            RelaxSatRunNB<P, CX, N - 1, NB>::go(n, acc, r, m, k0, cur, prefix, pa, pa_s);
+    }
+};
+template <class P, bool CX, int NB>
+struct RelaxSatRunNB<P, CX, 0, NB> {
+    __device__ __forceinline__ static void go(int, typename P::Acc (&)[NB], const ChainRows &, const int (&)[NB], int,
+                                              RowCursor &, uint64_t &, const_i64, int64_t)
+    {
+    }
+};
+
+// relax_run_nb with saturated X (CX) or Y operands, in runs of 8 splits
+template <class P, bool CX, int NB>
+__device__ __forceinline__ void relax_sat_run_nb(typename P::Acc (&acc)[NB], const ChainRows &r, const int (&m)[NB],
+                                                 int k0, int n, RowCursor &cur, uint64_t &prefix, const_i64 pa,
+                                                 int64_t pa_s)
+{
+    constexpr int kRun = 8;
+    for (; n > 0; n -= kRun, k0 += kRun)
+        RelaxSatRunNB<P, CX, kRun, NB>::go(n < kRun ? n : kRun, acc, r, m, k0, cur, prefix, pa, pa_s);
+}
+
 // Cursor of a narrow run whose X and Y rows come from different copies: X
 // moves xstep bytes per split, Y ystep bytes, and ystep shrinks by ydec.
 struct MixedCursor {
@@ -1632,7 +1701,11 @@ __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &c
             MixedRunNB<Load16, Load32, kT - 1, NB>::go(k_lo - s, acc, r, m, s, low, prefix);
     } else {
         RowCursor low = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, s);
-        relax_run_nb<P, NB>(acc, r, m, s, k_lo - s, low, prefix);
+        if (xsat)
+            relax_sat_run_nb<P, true, NB>(acc, r, m, s, k_lo - s, low, prefix, (const_i64)cw.preall,
+                                          ((const_i64)cw.preall)[s - 1]);
+        else
+            relax_run_nb<P, NB>(acc, r, m, s, k_lo - s, low, prefix);
     }
     // middle splits: the stored partial counts u_f from k_lo on
     const int S = k_hi > k_lo ? 32 - __clz(k_hi - k_lo) : 0;
@@ -1661,7 +1734,11 @@ __device__ __forceinline__ void edge_body(const ChainRows &r, const ChainWork &c
             MixedRunNB<Load32, Load16, kT - 1, NB>::go(t - k_hi - 1, acc, r, m, k_hi + 1, high, prefix);
     } else {
         RowCursor high = row_cursor<P>(tab, cw.shadow, L, pitch, s, t, k_hi + 1);
-        relax_run_nb<P, NB>(acc, r, m, k_hi + 1, t - k_hi - 1, high, prefix);
+        if (ysat)
+            relax_sat_run_nb<P, false, NB>(acc, r, m, k_hi + 1, t - k_hi - 1, high, prefix, (const_i64)cw.preall,
+                                           ((const_i64)cw.preall)[t]);
+        else
+            relax_run_nb<P, NB>(acc, r, m, k_hi + 1, t - k_hi - 1, high, prefix);
     }
     const int32_t gnone = cw.gnone[cell];
     const uint64_t ufub = (uint64_t)(r.uf[s - 1] + r.ub[s - 1]);
@@ -1700,10 +1777,12 @@ __global__ __launch_bounds__(kEdgeThreads) void edge_kernel(const int64_t *__res
     const bool narrow = cw.narrow(delta), d16 = cw.diag16();
     const bool sat =
         saturated_in_block(r, cw, I, delta, s, row_of(L, s, t), blockIdx.x * (kEdgeThreads * kEdgeBudgets));
-    if (!narrow)
-        edge_body<Wide, false>(r, cw, L, M, m0, pitch, s, t, (I + 1) * kT, J * kT, sat, tab, dtab);
-    else if (d16)
+    // the 2-byte path first and marked likely, so that the code of the
+    // other two paths does not sit in its way
+    if (__builtin_expect(narrow && d16, 1))
         edge_body<Narrow, true>(r, cw, L, M, m0, pitch, s, t, (I + 1) * kT, J * kT, sat, tab, dtab);
+    else if (!narrow)
+        edge_body<Wide, false>(r, cw, L, M, m0, pitch, s, t, (I + 1) * kT, J * kT, sat, tab, dtab);
     else
         edge_body<Narrow, false>(r, cw, L, M, m0, pitch, s, t, (I + 1) * kT, J * kT, sat, tab, dtab);
 }
