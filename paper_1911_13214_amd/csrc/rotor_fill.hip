@@ -1053,6 +1053,54 @@ __global__ __launch_bounds__(256) void fill_partials_kernel(int L, int M, int64_
         cost[((int64_t)c * rows + row_of(L, s, t)) * pitch + m] = -1;  // all ones: above every stored form
 }
 
+// Saturated operand rows of the middle products (head of this file): a row
+// whose budgets here (shifted by w_a^k for Y) all lie at or above its G holds
+// its least time at each of them, which the wave can write into the ring
+// instead of copying the row.  X rows (first + i, k), i < 8, are all
+// saturated when the first is (G(s, k) >= G(s + 1, k)); the wave takes that
+// for the splits ka .. kx, up to the first that is not.  Y rows (k + 1, t),
+// t = first .. first + 7 (at most L), for the splits ky .. kb, from the last
+// that is not: G(k + 1, t) falls as k grows.  Both bounds are found once,
+// 64 splits per step; wa_v holds the clamped w_a of the chain.
+__device__ inline void saturated_splits(const ChainWork &cw, const int32_t *wa_v, int L, bool copies_x, int first,
+                                        int ka, int kb, int base, int lane, int &kx, int &ky)
+{
+    kx = ka - 1;
+    ky = kb + 1;
+    const int first_c = min(first, L);
+    if (copies_x) {
+        const int32_t *g_row = cw.gsat + row_of(L, first, ka);  // G(first, k) at g_row[k - ka]
+        for (int k0 = ka; k0 <= kb; k0 += 64) {
+            const int k = k0 + lane;
+            const uint64_t bad = __ballot(k <= kb && g_row[k - ka] > base);
+            if (bad) {
+                kx = k0 + __ffsll((long long)bad) - 2;
+                break;
+            }
+            kx = min(kb, k0 + 63);
+        }
+    } else {
+        for (int k0 = kb; k0 >= ka; k0 -= 64) {
+            const int k = k0 - lane;
+            bool bad = false;
+            if (k >= ka) {
+                const int32_t *g = cw.gsat + row_of(L, k + 1, first_c);
+                int32_t gm = g[0];
+#pragma unroll
+                for (int i = 1; i < kDmaPerSplit; ++i)
+                    gm = max(gm, g[min(first + i, L) - first_c]);
+                bad = base - wa_v[k - 1] < gm;
+            }
+            const uint64_t b = __ballot(bad);
+            if (b) {
+                ky = k0 - (__ffsll((long long)b) - 1) + 1;
+                break;
+            }
+            ky = max(ka, k0 - 63);
+        }
+    }
+}
+
 // With n_part > 1 (block-diagonals of few blocks, whose launches would leave
 // most CUs idle), the middle split range of a block is cut into n_part runs
 // taken by different workgroups (x = part * chunks + chunk).  Their keys
@@ -1117,49 +1165,10 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     int k_copy = ka;  // next split to copy
     uint32_t *const dst0 = ring + (copies_x ? wave * kSub : kT + (wave - 2) * kSub) * 64;
     int fill = 0;  // ring stage filled next
-    // Saturated operand rows (head of this file): a row whose budgets here
-    // (shifted by w_a^k for Y) all lie at or above its G holds its least time
-    // at each of them, which the wave can write into the ring instead of
-    // copying the row.  X rows (first + i, k) are all saturated when the
-    // first is (G(s, k) >= G(s + 1, k)); this wave takes that for the splits
-    // ka .. kx, up to the first that is not.  Y rows (k + 1, t) for the
-    // splits ky .. kb, from the last split that is not: G(k + 1, t) falls as
-    // k grows.  Both bounds are found once, 64 splits per step.
+    // saturated operand rows: X for the splits ka .. kx, Y for ky .. kb
     const int base = m - lane;
-    const int first_c = min(first, L);
-    int kx = ka - 1, ky = kb + 1;
-    if (copies_x) {
-        const int32_t *g_row = cw.gsat + row_of(L, first, ka);  // G(first, k) at g_row[k - ka]
-        for (int k0 = ka; k0 <= kb; k0 += 64) {
-            const int k = k0 + lane;
-            const uint64_t bad = __ballot(k <= kb && g_row[k - ka] > base);
-            if (bad) {
-                kx = k0 + __ffsll((long long)bad) - 2;
-                break;
-            }
-            kx = min(kb, k0 + 63);
-        }
-    } else {
-        const int32_t *wa_v = w.shift + (int64_t)c * 2 * L;  // clamped w_a, as r.wa
-        for (int k0 = kb; k0 >= ka; k0 -= 64) {
-            const int k = k0 - lane;
-            bool bad = false;
-            if (k >= ka) {
-                const int32_t *g = cw.gsat + row_of(L, k + 1, first_c);
-                int32_t gm = g[0];
-#pragma unroll
-                for (int i = 1; i < kDmaPerSplit; ++i)
-                    gm = max(gm, g[min(first + i, L) - first_c]);
-                bad = base - wa_v[k - 1] < gm;
-            }
-            const uint64_t b = __ballot(bad);
-            if (b) {
-                ky = k0 - (__ffsll((long long)b) - 1) + 1;
-                break;
-            }
-            ky = max(ka, k0 - 63);
-        }
-    }
+    int kx, ky;
+    saturated_splits(cw, w.shift + (int64_t)c * 2 * L, L, copies_x, first, ka, kb, base, lane, kx, ky);
     // the prefixes of u_f + u_b at the rows' other ends (X: s - 1, Y: t),
     // 32 bits suffice for a least time below 2^32 - 1
     const const_i64 pa = (const_i64)cw.preall;
