@@ -79,7 +79,10 @@ __device__ __forceinline__ typename P::Raw final_raw(const typename P::Acc &a)
 // barriers keep that order: a load may not pass an earlier store to the
 // same table, and hoisting more loads would hold the whole row's operands
 // in registers.
-template <class P, bool H, bool PP, int A>
+// With YS the Y operands of the high splits (diagonal block J) are all
+// saturated at the workgroup's budgets (head of rotor_fill.hip): least times,
+// not loaded.
+template <class P, bool H, bool PP, int A, bool YS>
 __device__ __forceinline__ void row_body(const ChainRows &r, const ChainWork &cw, int L, int M, int m0, int64_t pitch,
                                          int s, int J, int t_first, int t_last, int64_t *tab, int16_t *dtab)
 {
@@ -182,10 +185,18 @@ __device__ __forceinline__ void row_body(const ChainRows &r, const ChainWork &cw
         for (int i = 0; i < j; ++i) {
             // split k = k_hi + 1 + i, Y at (k + 1, t) (within the block for every t <= L)
             const int k1 = min(k_hi + 2 + i, t);
+            if constexpr (YS) {
+                const const_i64 pa = (const_i64)cw.preall;
+                const typename P::Raw lt = (typename P::Raw)(pa[t] - pa[k1 - 1]);
 #pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                const int ri = m[b] - w_t[i];
-                ld[j].yh[i][b] = diag_load<P, H>(cw, tab, L, pitch, k1, t, ri >= 0 ? ri : m[b]);
+                for (int b = 0; b < NB; ++b)
+                    ld[j].yh[i][b] = lt;
+            } else {
+#pragma unroll
+                for (int b = 0; b < NB; ++b) {
+                    const int ri = m[b] - w_t[i];
+                    ld[j].yh[i][b] = diag_load<P, H>(cw, tab, L, pitch, k1, t, ri >= 0 ? ri : m[b]);
+                }
             }
         }
     };
@@ -298,16 +309,20 @@ __global__ __launch_bounds__(kEdgeThreads) void edge_row_kernel(const int64_t *_
         }
     }
     const bool packed = middle_packed(cw, delta, (delta - 1) * kT);
-    if (!cw.narrow(delta))
-        row_body<Wide, false, false, A>(r, cw, L, M, m0, pitch, s, J, t_first, t_last, tab, dtab);
+    // the high splits' Y rows, in diagonal block J, all saturated here
+    const bool ysat = base >= diag_block_gyshift(cw, J);
+    if (cw.narrow(delta) && cw.diag16() && packed && ysat)
+        row_body<Narrow, true, true, A, true>(r, cw, L, M, m0, pitch, s, J, t_first, t_last, tab, dtab);
+    else if (!cw.narrow(delta))
+        row_body<Wide, false, false, A, false>(r, cw, L, M, m0, pitch, s, J, t_first, t_last, tab, dtab);
     else if (cw.diag16() && packed)
-        row_body<Narrow, true, true, A>(r, cw, L, M, m0, pitch, s, J, t_first, t_last, tab, dtab);
+        row_body<Narrow, true, true, A, false>(r, cw, L, M, m0, pitch, s, J, t_first, t_last, tab, dtab);
     else if (cw.diag16())
-        row_body<Narrow, true, false, A>(r, cw, L, M, m0, pitch, s, J, t_first, t_last, tab, dtab);
+        row_body<Narrow, true, false, A, false>(r, cw, L, M, m0, pitch, s, J, t_first, t_last, tab, dtab);
     else if (packed)
-        row_body<Narrow, false, true, A>(r, cw, L, M, m0, pitch, s, J, t_first, t_last, tab, dtab);
+        row_body<Narrow, false, true, A, false>(r, cw, L, M, m0, pitch, s, J, t_first, t_last, tab, dtab);
     else
-        row_body<Narrow, false, false, A>(r, cw, L, M, m0, pitch, s, J, t_first, t_last, tab, dtab);
+        row_body<Narrow, false, false, A, false>(r, cw, L, M, m0, pitch, s, J, t_first, t_last, tab, dtab);
 }
 
 // edge_row_kernel<a> for a launch-time a in [A0, A1]
