@@ -726,11 +726,10 @@ struct MixedSatRunNB<XL, YL, CX, 0, NB> {
 // L - s' rows after the row of (s', t).  With H (a pair inside a diagonal
 // block, narrow path, ChainWork::diag16) every operand comes from the 2-byte
 // copy, where the rows (s'+1, t) are 16 rows apart.
-template <class P, bool H>
+template <class P, bool H, int NB>
 __device__ __forceinline__ void diag_body(const ChainRows &r, const ChainWork &cw, int L, int M, int m0, int64_t pitch,
                                           int s, int t, bool sat, int64_t *tab, int16_t *dtab)
 {
-    constexpr int NB = kEdgeBudgets;
     const int64_t cell = row_of(L, s, t);
     // the final stores of budget set b, with the 2-byte copy of a diagonal
     // block's cell
@@ -800,6 +799,10 @@ __device__ __forceinline__ void diag_body(const ChainRows &r, const ChainWork &c
 
 // The pairs (s, s + d): inside the 16 x 16 diagonal blocks only (blocked
 // fill), or all of them (streamed fill of a small table, one launch per d).
+// NB budgets per lane: kDiagBudgets for the diagonal blocks of the blocked
+// order, kEdgeBudgets for the streamed order (small tables, where more and
+// smaller workgroups are faster).
+template <int NB>
 __global__ __launch_bounds__(kEdgeThreads) void diag_kernel(const int64_t *__restrict__ params, int L, int M,
                                                    int64_t pitch, int64_t rows, int d, int whole,
                                                    int64_t *__restrict__ cost, int16_t *__restrict__ dec, Work w)
@@ -809,7 +812,7 @@ __global__ __launch_bounds__(kEdgeThreads) void diag_kernel(const int64_t *__res
     const int t = s + d;
     if (!whole && (s - 1) / kT != (t - 1) / kT)
         return;
-    const int m0 = blockIdx.x * (kEdgeThreads * kEdgeBudgets) + threadIdx.x;
+    const int m0 = blockIdx.x * (kEdgeThreads * NB) + threadIdx.x;
     if (m0 > M)
         return;
     const ChainRows r = chain_rows(params, w, L, c);
@@ -819,13 +822,13 @@ __global__ __launch_bounds__(kEdgeThreads) void diag_kernel(const int64_t *__res
     const int D = block_diag(s, t);
     // the path and the saturation test first: their scalar loads go together
     const bool narrow = cw.narrow(D), d16 = cw.diag16();
-    const bool sat = saturated(r, cw, s, row_of(L, s, t), blockIdx.x * (kEdgeThreads * kEdgeBudgets));
+    const bool sat = saturated(r, cw, s, row_of(L, s, t), blockIdx.x * (kEdgeThreads * NB));
     if (!narrow)
-        diag_body<Wide, false>(r, cw, L, M, m0, pitch, s, t, sat, tab, dtab);
+        diag_body<Wide, false, NB>(r, cw, L, M, m0, pitch, s, t, sat, tab, dtab);
     else if (D == 0 && d16)
-        diag_body<Narrow, true>(r, cw, L, M, m0, pitch, s, t, sat, tab, dtab);
+        diag_body<Narrow, true, NB>(r, cw, L, M, m0, pitch, s, t, sat, tab, dtab);
     else
-        diag_body<Narrow, false>(r, cw, L, M, m0, pitch, s, t, sat, tab, dtab);
+        diag_body<Narrow, false, NB>(r, cw, L, M, m0, pitch, s, t, sat, tab, dtab);
 }
 
 // Streamed order for the longer diagonals: the d splits of each pair are
@@ -1844,6 +1847,7 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
     const unsigned mb256 = (unsigned)((tb.M + 1 + 255) / 256);
     const unsigned mb64 = (unsigned)((tb.M + 1 + 63) / 64);
     const unsigned mb_edge = (unsigned)((tb.M + kEdgeThreads * kEdgeBudgets) / (kEdgeThreads * kEdgeBudgets));
+    const unsigned mb_diag = (unsigned)((tb.M + kEdgeThreads * kDiagBudgets) / (kEdgeThreads * kDiagBudgets));
     auto launched = [&](KernelClass k, uint64_t c1, uint64_t c2, uint64_t cells) -> hipError_t {
         hipError_t e = check();
         if (e == hipSuccess && obs)
@@ -1877,9 +1881,12 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
         if (streamed && d >= kSplitMinD)
             diag_split_kernel<<<dim3(mb64, L - d, tb.n_chains), 256, 0, stream>>>(tb.params, L, tb.M, tb.pitch,
                                                                                   tb.rows, d, tb.cost, tb.dec, w);
+        else if (streamed)
+            diag_kernel<kEdgeBudgets><<<dim3(mb_edge, L - d, tb.n_chains), kEdgeThreads, 0, stream>>>(
+                tb.params, L, tb.M, tb.pitch, tb.rows, d, 1, tb.cost, tb.dec, w);
         else
-            diag_kernel<<<dim3(mb_edge, L - d, tb.n_chains), kEdgeThreads, 0, stream>>>(tb.params, L, tb.M, tb.pitch, tb.rows,
-                                                                             d, streamed ? 1 : 0, tb.cost, tb.dec, w);
+            diag_kernel<kDiagBudgets><<<dim3(mb_diag, L - d, tb.n_chains), kEdgeThreads, 0, stream>>>(
+                tb.params, L, tb.M, tb.pitch, tb.rows, d, 0, tb.cost, tb.dec, w);
         const uint64_t pairs = streamed ? (uint64_t)(L - d) : in_block_pairs(L, d);
         if ((e = launched(kDiag, pairs * d, pairs, pairs)) != hipSuccess)
             return e;

@@ -20,6 +20,12 @@ constexpr int kSub = 8;  // per-wave register tile side
 // per lane 13.53 ms, three or four budgets per lane 14.0-14.4 ms).
 constexpr int kEdgeThreads = 64;
 constexpr int kEdgeBudgets = 2;
+// diag_kernel's workgroups in the blocked order (one wave, like the edges')
+// hold four budgets per lane, 256 consecutive budgets (measured on MI355X:
+// the batch of 256 chains of L = 64, M = 640, 0.67 -> 0.54 ms of diagonal
+// blocks; the edges lose with four, 10.4 -> 12.3 ms at L = 500, M = 5000, and
+// so do the small tables of the streamed order, 3-6%)
+constexpr int kDiagBudgets = 4;
 constexpr uint32_t kAllSplit = 0xFFFF;  // split field of a C_2 candidate
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
 constexpr uint64_t kNarrowBound = 0xFFFFFFFFull;  // V_D below: the narrow path
