@@ -378,11 +378,11 @@ __device__ __forceinline__ void relax_fixed(typename P::Acc &acc, const ChainRow
     int ri[N];
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-        ri[i] = m - r.wa[k0 + i - 1];
+        const int w = r.wa[k0 + i - 1];
+        ri[i] = m - w;
         rx[i] = P::load_at(cur.x, m);
-        // a budget shifted below 0 reads the lane's own budget (in bounds);
-        // xop discards the candidate
-        ry[i] = P::load_at(cur.y, ri[i] >= 0 ? ri[i] : m);
+        // a budget shifted below 0 reads budget 0; xop discards the candidate
+        ry[i] = P::load_off(cur.y, shifted_off<P::kBytes>((uint32_t)m * P::kBytes, w));
         cur.x += cur.row_bytes;
         cur.y += cur.ystep;
         cur.ystep -= cur.row_bytes;
@@ -436,9 +436,8 @@ __device__ __forceinline__ void relax_fixed_nb(typename P::Acc (&acc)[NB], const
         wa[i] = r.wa[k0 + i - 1];
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
-            const int ri = m[b] - wa[i];
             rx[i][b] = P::load_at(cur.x, m[b]);
-            ry[i][b] = P::load_at(cur.y, ri >= 0 ? ri : m[b]);
+            ry[i][b] = P::load_off(cur.y, shifted_off<P::kBytes>((uint32_t)m[b] * P::kBytes, wa[i]));
         }
         cur.x += cur.row_bytes;
         cur.y += cur.ystep;
@@ -505,8 +504,8 @@ __device__ __forceinline__ void relax_sat_fixed_nb(typename P::Acc (&acc)[NB], c
         c[i] = (typename P::Raw)(CX ? pa[k] - pa_s : pa_s - pa[k]);
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
-            const int ri = m[b] - wa[i];
-            rv[i][b] = CX ? P::load_at(cur.y, ri >= 0 ? ri : m[b]) : P::load_at(cur.x, m[b]);
+            rv[i][b] = CX ? P::load_off(cur.y, shifted_off<P::kBytes>((uint32_t)m[b] * P::kBytes, wa[i]))
+                          : P::load_at(cur.x, m[b]);
         }
         cur.x += cur.row_bytes;
         cur.y += cur.ystep;
@@ -575,10 +574,11 @@ __device__ __forceinline__ void relax_mixed(Narrow::Acc &acc, const ChainRows &r
     int ri[N];
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-        ri[i] = m - r.wa[k0 + i - 1];
+        const int w = r.wa[k0 + i - 1];
+        ri[i] = m - w;
         rx[i] = XL::at(cur.x, m);
-        // a budget shifted below 0 reads the lane's own budget (in bounds)
-        ry[i] = YL::at(cur.y, ri[i] >= 0 ? ri[i] : m);
+        // a budget shifted below 0 reads budget 0; xop discards the candidate
+        ry[i] = YL::at_off(cur.y, shifted_off<YL::kBytes>((uint32_t)m * YL::kBytes, w));
         cur.x += cur.xstep;
         cur.y += cur.ystep;
         cur.ystep -= cur.ydec;
@@ -623,10 +623,8 @@ __device__ __forceinline__ void relax_mixed_nb(Narrow::Acc (&acc)[NB], const Cha
         wa[i] = r.wa[k0 + i - 1];
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
-            const int ri = m[b] - wa[i];
             rx[i][b] = XL::at(cur.x, m[b]);
-            // a budget shifted below 0 reads the lane's own budget (in bounds)
-            ry[i][b] = YL::at(cur.y, ri >= 0 ? ri : m[b]);
+            ry[i][b] = YL::at_off(cur.y, shifted_off<YL::kBytes>((uint32_t)m[b] * YL::kBytes, wa[i]));
         }
         cur.x += cur.xstep;
         cur.y += cur.ystep;
@@ -680,9 +678,8 @@ __device__ __forceinline__ void relax_mixed_sat_nb(Narrow::Acc (&acc)[NB], const
         c[i] = (uint32_t)(CX ? pa[k] - pa_s : pa_s - pa[k]);
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
-            const int ri = m[b] - wa[i];
             if constexpr (CX)
-                rv[i][b] = YL::at(cur.y, ri >= 0 ? ri : m[b]);
+                rv[i][b] = YL::at_off(cur.y, shifted_off<YL::kBytes>((uint32_t)m[b] * YL::kBytes, wa[i]));
             else
                 rv[i][b] = XL::at(cur.x, m[b]);
         }

@@ -165,7 +165,12 @@ struct Wide {
     static constexpr int kBytes = 8;  // bytes per cell of the table it reads
     __device__ static const char *table(const int64_t *tab, const uint32_t *) { return (const char *)tab; }
     __device__ static Raw load_at(const char *row, int m) { return *(global_c64)(row + (uint32_t)m * 8u); }
+    __device__ static Raw load_off(const char *row, uint32_t off) { return *(global_c64)(row + off); }
     __device__ static Raw load(const int64_t *crow, const uint32_t *, int m) { return load64(crow, m); }
+    __device__ static Raw load_row_off(const int64_t *crow, const uint32_t *, uint32_t off)
+    {
+        return *(global_c64)((const char *)crow + off);
+    }
     __device__ static void init(Acc &a) { a.key = ~0ull; }
     // ok = false: the budget of Y was shifted below 0, the candidate is infinite
     __device__ static X xop(Raw x, uint64_t prefix, uint32_t sp, bool ok)
@@ -205,7 +210,12 @@ struct Narrow {
     static constexpr int kBytes = 4;
     __device__ static const char *table(const int64_t *, const uint32_t *shadow) { return (const char *)shadow; }
     __device__ static Raw load_at(const char *row, int m) { return *(global_c32)(row + (uint32_t)m * 4u); }
+    __device__ static Raw load_off(const char *row, uint32_t off) { return *(global_c32)(row + off); }
     __device__ static Raw load(const int64_t *, const uint32_t *srow, int m) { return load32(srow, m); }
+    __device__ static Raw load_row_off(const int64_t *, const uint32_t *srow, uint32_t off)
+    {
+        return *(global_c32)((const char *)srow + off);
+    }
     __device__ static void init(Acc &a)
     {
         a.val = kInf32;
@@ -325,14 +335,32 @@ __device__ inline int64_t least_time(const ChainWork &cw, int s, int t)
 // values there are below 2^15, and the infinity 0xFFFF becomes 0xFFFFFFFF).
 typedef const __attribute__((address_space(1))) int16_t *global_c16;
 struct Load32 {
+    static constexpr uint32_t kBytes = 4;
     __device__ static uint32_t at(const char *row, int m) { return *(global_c32)(row + (uint32_t)m * 4u); }
+    __device__ static uint32_t at_off(const char *row, uint32_t off) { return *(global_c32)(row + off); }
 };
 struct Load16 {
+    static constexpr uint32_t kBytes = 2;
     __device__ static uint32_t at(const char *row, int m)
     {
         return (uint32_t)(int32_t) * (global_c16)(row + (uint32_t)m * 2u);
     }
+    __device__ static uint32_t at_off(const char *row, uint32_t off)
+    {
+        return (uint32_t)(int32_t) * (global_c16)(row + off);
+    }
 };
+
+// Byte offset of budget m - w in a row of B-byte cells, from the lane's
+// m * B: budget 0 when m < w, where the caller's flag (m >= w) discards the
+// candidate.  One saturating subtraction instead of a compare and a select
+// before the scaling; in bounds for the shift sizes of ChainRows, which lie
+// in [0, M + 1].
+template <uint32_t B>
+__device__ inline uint32_t shifted_off(uint32_t m_bytes, int w)
+{
+    return __builtin_elementwise_sub_sat(m_bytes, (uint32_t)w * B);
+}
 
 // Whether the middle products of block-diagonal D of a chain, whose middle
 // split range has span + 1 splits, use packed keys.

@@ -59,6 +59,20 @@ __device__ __forceinline__ typename P::Raw diag_load(const ChainWork &cw, const 
     }
 }
 
+// diag_load at budget m - w, or at budget 0 when m < w (the caller's flag
+// discards that candidate).
+template <class P, bool H>
+__device__ __forceinline__ typename P::Raw diag_load_shifted(const ChainWork &cw, const int64_t *tab, int L,
+                                                             int64_t pitch, int s, int t, int m, int w)
+{
+    if constexpr (H) {
+        return Load16::at_off((const char *)cw.half_row(s, t), shifted_off<Load16::kBytes>((uint32_t)m * 2u, w));
+    } else {
+        const int64_t o = row_of(L, s, t) * pitch;
+        return P::load_row_off(tab + o, cw.shadow + o, shifted_off<P::kBytes>((uint32_t)m * P::kBytes, w));
+    }
+}
+
 // A finished cell's cost in the form the path loads it (infinity included).
 template <class P>
 __device__ __forceinline__ typename P::Raw final_raw(const typename P::Acc &a)
@@ -176,10 +190,9 @@ __device__ __forceinline__ void row_body(const ChainRows &r, const ChainWork &cw
         for (int i = 0; i < A; ++i) {
             const int64_t yrow = row_of(L, s + i + 1, t) * pitch;
 #pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                const int ri = m[b] - w_lo[i];
-                ld[j].yl[i][b] = P::load(tab + yrow, cw.shadow + yrow, ri >= 0 ? ri : m[b]);
-            }
+            for (int b = 0; b < NB; ++b)
+                ld[j].yl[i][b] = P::load_row_off(tab + yrow, cw.shadow + yrow,
+                                                 shifted_off<P::kBytes>((uint32_t)m[b] * P::kBytes, w_lo[i]));
         }
 #pragma unroll
         for (int i = 0; i < j; ++i) {
@@ -193,10 +206,8 @@ __device__ __forceinline__ void row_body(const ChainRows &r, const ChainWork &cw
                     ld[j].yh[i][b] = lt;
             } else {
 #pragma unroll
-                for (int b = 0; b < NB; ++b) {
-                    const int ri = m[b] - w_t[i];
-                    ld[j].yh[i][b] = diag_load<P, H>(cw, tab, L, pitch, k1, t, ri >= 0 ? ri : m[b]);
-                }
+                for (int b = 0; b < NB; ++b)
+                    ld[j].yh[i][b] = diag_load_shifted<P, H>(cw, tab, L, pitch, k1, t, m[b], w_t[i]);
             }
         }
     };
