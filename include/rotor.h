@@ -64,10 +64,15 @@
  * enqueuing, they clear the calling thread's pending HIP error (the one
  * hipGetLastError would return), so that ROTOR_EDEVICE reports a failure of
  * their own launches only.  The
- * library keeps no state between calls and allocates no device memory (the
- * caller passes the solve's workspace); concurrent calls on distinct output
- * buffers and workspaces are independent.  The one exception is
- * rotor_solve_noalloc, whose workspace is a static device array per device.
+ * library allocates no device memory (the caller passes the solve's
+ * workspace) and keeps no state between calls but two: the static workspace
+ * of rotor_solve_noalloc, one device array per device; and, for the blocked
+ * fill, one side stream and two events per device (created by the first
+ * solve on the device, kept until the process ends), on which part of each
+ * middle product runs beside the edges before it and which the solve joins
+ * back into `stream` before it returns.  Solves hold a lock while they
+ * enqueue; concurrent calls on distinct output buffers and workspaces are
+ * independent.
  */
 #ifndef ROTOR_H
 #define ROTOR_H
@@ -181,9 +186,10 @@ ROTOR_API int32_t rotor_solve(const int64_t *d_params, int32_t n_chains, int32_t
 
 /* rotor_solve for callers that cannot allocate device memory (code under
  * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
- * the same fill, same tables, same fill order, with the workspace taken from
- * a static device array of ROTOR_NOALLOC_WORK_BYTES bytes per device instead
- * of a caller buffer.  The caller still passes parameters and tables (as for
+ * the same fill and tables, with the workspace taken from a static device
+ * array of ROTOR_NOALLOC_WORK_BYTES bytes per device instead of a caller
+ * buffer, and every launch on `stream` (no side stream: the blocked fill's
+ * middle products wait for the edges before them).  The caller still passes parameters and tables (as for
  * rotor_solve).  It calls no hipMalloc, hipFree or allocating library
  * routine.  Every call on one device shares that device's array, so calls
  * that overlap on one device (different streams, or host threads) race and
@@ -235,12 +241,24 @@ ROTOR_API int32_t rotor_solve_status(const void *d_work, uint64_t work_bytes, in
  *                            uses).
  *   ROTOR_SCHEDULE_BLOCKED_ROWS, ROTOR_SCHEDULE_BLOCKED_ROUNDS
  *                            BLOCKED with the edges of every block-diagonal
- *                            by rows, or by anti-diagonals. */
+ *                            by rows, or by anti-diagonals.
+ *   ROTOR_SCHEDULE_BLOCKED_SERIAL
+ *                            BLOCKED with every middle product on the
+ *                            caller's stream after the edges of the
+ *                            block-diagonal before it.  The other blocked
+ *                            orders run the splits of a middle product that
+ *                            reach no further than two block-diagonals back
+ *                            on a second stream of the library's (one per
+ *                            device, created by the first solve on the
+ *                            device and kept until the process ends) beside
+ *                            those edges, and join it before the product's
+ *                            remaining splits. */
 #define ROTOR_SCHEDULE_AUTO 0
 #define ROTOR_SCHEDULE_BLOCKED 1
 #define ROTOR_SCHEDULE_DIAGONAL 2
 #define ROTOR_SCHEDULE_BLOCKED_ROWS 3
 #define ROTOR_SCHEDULE_BLOCKED_ROUNDS 4
+#define ROTOR_SCHEDULE_BLOCKED_SERIAL 5
 
 /* rotor_solve with an explicit fill order; ROTOR_EINVAL for an unknown one. */
 ROTOR_API int32_t rotor_solve_schedule(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M,

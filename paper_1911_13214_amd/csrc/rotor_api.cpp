@@ -126,7 +126,7 @@ int32_t rotor_solve(const int64_t *d_params, int32_t n_chains, int32_t L, int64_
 int32_t rotor_solve_schedule(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
                              int16_t *d_dec, void *d_work, uint64_t work_bytes, void *stream, int32_t schedule)
 {
-    if (schedule < ROTOR_SCHEDULE_AUTO || schedule > ROTOR_SCHEDULE_BLOCKED_ROUNDS ||
+    if (schedule < ROTOR_SCHEDULE_AUTO || schedule > ROTOR_SCHEDULE_BLOCKED_SERIAL ||
         !solve_args_ok(d_params, n_chains, L, M, d_cost, d_dec, d_work, work_bytes))
         return ROTOR_EINVAL;
     const Tables tb = make_tables(d_params, n_chains, L, M, d_cost, d_dec);

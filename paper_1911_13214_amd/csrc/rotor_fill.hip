@@ -70,9 +70,14 @@
 // edge_kernel in 30 steps over the block's anti-diagonals a + b = q = 1..30
 // (a = 16(I+1) - s low splits, b = t - 16J - 1 high splits), each step
 // reading only finished cells; the corner a + b = 0 has neither and is
-// finished by the middle kernels.  A small table is instead filled in the
+// finished by the middle kernels.  The middle splits whose operands lie in
+// block-diagonals up to D - 2 (all but the first and the last 16) need
+// nothing of D - 1: they run on a second stream beside the edges of D - 1
+// (latency-bound waves beside VALU-bound ones), and the remaining 32 follow
+// those edges, merged by atomic minimum.  A small table is instead filled in the
 // streamed order: one launch per diagonal d over all its pairs (diag_kernel,
 // or diag_split_kernel with the splits of a pair spread over four waves).
+#include <mutex>
 #include <type_traits>
 
 #include "rotor_paths.h"
@@ -1101,6 +1106,50 @@ __device__ inline void saturated_splits(const ChainWork &cw, const int32_t *wa_v
     }
 }
 
+// Which middle splits of the range [k_lo, k_hi] a launch takes (range) and
+// how its workgroups share them (n_part parts).  kMidAll: the whole range.
+// kMidInner: all but the first and the last kT splits, the ones whose
+// operands lie in blocks up to two block-diagonals back, so that this part
+// can run beside the previous block-diagonal's edge rounds; its slots are
+// written as with kMidAll.  kMidRim: those 2 kT splits, after the edges, in
+// one part that jumps from the first kT to the last kT and folds its minimum
+// into the slots the inner part wrote (a plain read, minimum and write: the
+// workgroup owns its slots).  The corner is finished here only with kMidAll
+// and one part; else its partial is stored like any other and the edge
+// round a + b = 0 finishes it.
+constexpr int kMidAll = 0, kMidInner = 1, kMidRim = 2;
+struct MiddleSplits {
+    int ka, kb;        // this workgroup's first and last split
+    int n_splits;      // splits it takes
+    int jump_from;     // after this split the next is jump_to (-1: none)
+    int jump_to;
+    bool merge;        // atomic minimum into the partial slots
+    bool owns_corner;  // finishes the corner cell of the block
+};
+__device__ inline MiddleSplits middle_splits(int k_lo, int k_hi, int range, int n_part, int part)
+{
+    MiddleSplits r;
+    r.jump_from = -1;
+    r.jump_to = -1;
+    if (range == kMidRim) {
+        r.ka = k_lo;
+        r.kb = k_hi;
+        r.n_splits = 2 * kT;
+        r.jump_from = k_lo + kT - 1;
+        r.jump_to = k_hi - kT + 1;
+    } else {
+        const int ra = range == kMidInner ? k_lo + kT : k_lo;
+        const int rb = range == kMidInner ? k_hi - kT : k_hi;
+        const int part_len = (rb - ra + n_part) / n_part;
+        r.ka = ra + part * part_len;
+        r.kb = min(rb, r.ka + part_len - 1);
+        r.n_splits = r.kb - r.ka + 1;
+    }
+    r.merge = n_part > 1 || range == kMidRim;
+    r.owns_corner = n_part == 1 && range == kMidAll;
+    return r;
+}
+
 // With n_part > 1 (block-diagonals of few blocks, whose launches would leave
 // most CUs idle), the middle split range of a block is cut into n_part runs
 // taken by different workgroups (x = part * chunks + chunk).  Their keys
@@ -1108,10 +1157,11 @@ __device__ inline void saturated_splits(const ChainWork &cw, const int32_t *wa_v
 // is the minimum over the whole range, ties included: each run merges its
 // keys with an atomic minimum into the partial slots, which fill_partials
 // has set to infinity, and the corners are left to the edge round a + b = 0.
+template <bool RIM>
 __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__restrict__ params, int L, int M,
-                                                            int64_t pitch, int64_t rows, int delta, int n_part,
-                                                            int64_t *__restrict__ cost, int16_t *__restrict__ dec,
-                                                            Work w)
+                                                            int64_t pitch, int64_t rows, int delta, int range,
+                                                            int n_part, int64_t *__restrict__ cost,
+                                                            int16_t *__restrict__ dec, Work w)
 {
     __shared__ uint32_t ring[kRing * kStage * kSplitWords];
     const Tile tile = xcd_tile();
@@ -1131,14 +1181,13 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     if (!full && !middle_runs(cw, delta, k_hi - k_lo))
         return;
     // this workgroup's part of the middle splits [ka, kb]
-    const int part_len = (k_hi - k_lo + n_part) / n_part;
-    const int ka = k_lo + part * part_len;
-    const int kb = min(k_hi, ka + part_len - 1);
+    const MiddleSplits ms = middle_splits(k_lo, k_hi, range, n_part, part);
+    const int ka = ms.ka, kb = ms.kb;
     if (ka > kb)
         return;
     const ChainRows r = chain_rows(params, w, L, c);
     if (block_saturated(cw, I, J, m - lane)) {
-        if (n_part == 1 && wave == 0 && m <= M)
+        if (ms.owns_corner && wave == 0 && m <= M)
             store_saturated_corner<Narrow>(cw, L, m, pitch, I, J, cost + (int64_t)c * rows * pitch,
                                            dec + (int64_t)c * rows * pitch);
         return;
@@ -1150,7 +1199,7 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     const int S = full ? (k_hi > k_lo ? 32 - __clz(k_hi - k_lo) : 0) : cw.pbits[delta];
     const int R = full ? INT_MAX : 1 << S;  // splits per run, a multiple of kStage
     const int mc = m <= M ? m : M;
-    const int n_stages = (kb - ka + kStage) / kStage;
+    const int n_stages = (ms.n_splits + kStage - 1) / kStage;
 
     // rows this wave copies: waves 0, 1 the X rows (s, k) of s = 16I+1+8w ..,
     // waves 2, 3 the Y rows (k+1, t) of t = 16J+1+8(w-2) .. (past L: row L)
@@ -1168,7 +1217,12 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     // saturated operand rows: X for the splits ka .. kx, Y for ky .. kb
     const int base = m - lane;
     int kx, ky;
-    saturated_splits(cw, w.shift + (int64_t)c * 2 * L, L, copies_x, first, ka, kb, base, lane, kx, ky);
+    saturated_splits(cw, w.shift + (int64_t)c * 2 * L, L, copies_x, first, ka, RIM ? ms.jump_from : kb, base, lane,
+                     kx, ky);
+    // the rim's second half has bounds of its own
+    int kx2 = 0, ky2 = 0;
+    if constexpr (RIM)
+        saturated_splits(cw, w.shift + (int64_t)c * 2 * L, L, copies_x, first, ms.jump_to, kb, base, lane, kx2, ky2);
     // the prefixes of u_f + u_b at the rows' other ends (X: s - 1, Y: t),
     // 32 bits suffice for a least time below 2^32 - 1
     const const_i64 pa = (const_i64)cw.preall;
@@ -1183,7 +1237,8 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
 #pragma unroll
         for (int p = 0; p < kStage; ++p) {
             const int k = k_copy;
-            if (copies_x ? k <= kx : k >= ky) {
+            const bool second = RIM && k > ms.jump_from;
+            if (copies_x ? k <= (second ? kx2 : kx) : k >= (second ? ky2 : ky)) {
                 const uint32_t pk = (uint32_t)pa[k];
 #pragma unroll
                 for (int i = 0; i < kDmaPerSplit; ++i)
@@ -1196,7 +1251,13 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
                     __builtin_amdgcn_global_load_lds((global_void *)(src[i] + off),
                                                      (lds_void *)(dst + p * kSplitWords + i * 64), 4, 0, 0);
             }
-            if (k < kb) {
+            if (RIM && k == ms.jump_from) {
+                k_copy = ms.jump_to;
+#pragma unroll
+                for (int i = 0; i < kDmaPerSplit; ++i)
+                    src[i] = (const char *)(cw.shadow + (copies_x ? row_of(L, first + i, k_copy) * pitch
+                                                                  : row_of(L, k_copy + 1, min(first + i, L)) * pitch));
+            } else if (k < kb) {
                 // to split k + 1: X rows advance one row, Y rows L - k - 1 rows
                 const int64_t step = copies_x ? row_bytes : (int64_t)(L - k - 1) * row_bytes;
 #pragma unroll
@@ -1228,11 +1289,11 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     int run_base = full ? k_lo : ka;  // split of key offset 0
     // Runs: at the end of each, the keys become (value << 32) | s' in the
     // cost table: a plain store for the first run when the workgroup owns its
-    // cells (n_part == 1), an atomic minimum otherwise (the slots then start
-    // at all ones).  The corner keeps its best form in registers when this
-    // kernel finishes it.
+    // cells' slots (no merge), an atomic minimum otherwise (the slots then
+    // start at all ones, or hold the inner part).  The corner keeps its best
+    // form in registers when this kernel finishes it.
     int64_t *const tab = cost + (int64_t)c * rows * pitch;
-    const bool corner = s0 + kSub - 1 == k_lo && t0 == k_hi + 1;
+    const bool corner = ms.owns_corner && s0 + kSub - 1 == k_lo && t0 == k_hi + 1;
     uint64_t corner_best = ~0ull;
     bool first_flush = true;
     auto flush = [&]() {
@@ -1253,15 +1314,16 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
                 const uint64_t st = key == kInf32 ? (uint64_t)kInf32 << 32
                                                   : ((uint64_t)(key >> S) << 32) |
                                                         (uint32_t)(run_base + 1 + (int)(key & mask));
-                if (n_part == 1 && i == kSub - 1 && j == 0 && corner) {
+                if (i == kSub - 1 && j == 0 && corner) {
                     corner_best = st < corner_best ? st : corner_best;
                 } else if (j < nt && m <= M) {
                     // a wave-uniform row base and the lane's 32-bit offset
                     global_u64 slot = (global_u64)((char *)(tab + (row + j) * pitch) + lane_off);
-                    if (n_part == 1 && first_flush)
+                    if (!ms.merge && first_flush) {
                         *slot = st;
-                    else if (key != kInf32)
+                    } else if (key != kInf32) {
                         __hip_atomic_fetch_min(slot, st, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    }
                 }
             }
         first_flush = false;
@@ -1301,11 +1363,20 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
             flush();
             run_base = k;
         }
+        if (RIM && k == ms.jump_from + 1) {
+            // the rim's second half: u_f of the splits skipped joins the prefix
+            k = ms.jump_to;
+            prefix = (uint32_t)(cw.pre[k - 1] - cw.pre[k_lo - 1]);
+            if (!full) {
+                flush();
+                run_base = k;
+            }
+        }
     }
     if (!full) {
         if (k > run_base)
             flush();
-        if (n_part == 1 && corner && m <= M) {
+        if (corner && m <= M) {
             Narrow::Acc a;
             Narrow::init(a);
             if (corner_best < ((uint64_t)kInf32 << 32)) {
@@ -1321,8 +1392,8 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
     // the partial stays a packed key, in the cell's compact copy, which
     // edge_kernel reads once and then overwrites with the final value; used
     // once, it is stored and loaded non-temporally.  The corner cell is
-    // finished here when the range is not cut.
-    if (n_part > 1) {
+    // finished here when this launch takes the whole range in one part.
+    if (ms.merge) {
 #pragma unroll
         for (int i = 0; i < kSub; ++i)
 #pragma unroll
@@ -1358,8 +1429,9 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
 // as middle_packed_kernel; the partial, counting u_f from the first middle
 // split, goes to the cost table in the stored() form ((value << 32) | s' or
 // the 64-bit key), merged by atomic minimum when the range is cut
-// (n_part > 1, slots set to all ones by fill_partials), and the corner cell
-// is finished here otherwise.
+// (n_part > 1, slots set to all ones by fill_partials) or for the rim (the
+// slots hold the inner part), and the corner cell is finished here when one
+// part takes the whole range.
 //
 // With F (a block-diagonal whose bound V_D is below 2^38) the accumulators
 // are exact doubles instead: a candidate of split k is the key
@@ -1408,17 +1480,18 @@ __device__ inline typename P::Acc f64_acc(double key, int k_lo)
     return a;
 }
 
-template <class P, bool F>
+template <class P, bool F, bool RIM>
 __device__ __forceinline__ void middle_lds_body(const ChainRows &r, const ChainWork &cw, int L, int M, int m,
-                                                int64_t pitch, int I, int J, int wave, int ka, int kb, int k_lo,
-                                                int k_hi, int n_part, int64_t *tab, int16_t *dtab, uint32_t *ring)
+                                                int64_t pitch, int I, int J, int wave, const MiddleSplits &ms,
+                                                int k_lo, int k_hi, int64_t *tab, int16_t *dtab, uint32_t *ring)
 {
     constexpr int EW = P::kBytes / 4;          // dwords per element
     constexpr int kSW = kSplitWords * EW;      // dwords per split slot: 32 rows of 64 elements
+    const int ka = ms.ka, kb = ms.kb;
     const int lane = threadIdx.x & 63;
     const int mc = min(m, M);
     const int m0 = m - lane;                   // the workgroup's first budget
-    const int n_stages = (kb - ka + kStage) / kStage;
+    const int n_stages = (ms.n_splits + kStage - 1) / kStage;
     const int s0 = I * kT + (wave >> 1) * kSub + 1;
     const int t0 = J * kT + (wave & 1) * kSub + 1;
     const int nt = t0 <= L ? min(kSub, L - t0 + 1) : 0;
@@ -1465,7 +1538,13 @@ __device__ __forceinline__ void middle_lds_body(const ChainRows &r, const ChainW
                     __builtin_amdgcn_global_load_lds((global_void *)(src[i] + off),
                                                      (lds_void *)(dst + p * kSW + i * 64 * EW + e * 64), 4, 0, 0);
             }
-            if (k < kb) {
+            if (RIM && k == ms.jump_from) {
+                k_copy = ms.jump_to;
+#pragma unroll
+                for (int i = 0; i < kDmaPerSplit; ++i)
+                    src[i] = base + (copies_x ? row_of(L, first + i, k_copy)
+                                              : row_of(L, k_copy + 1, min(first + i, L))) * row_bytes;
+            } else if (k < kb) {
                 // to split k + 1: X rows advance one row, Y rows L - k - 1 rows
                 const int64_t step = copies_x ? row_bytes : (int64_t)(L - k - 1) * row_bytes;
 #pragma unroll
@@ -1551,6 +1630,11 @@ __device__ __forceinline__ void middle_lds_body(const ChainRows &r, const ChainW
                     else
                         P::relax(acc[i][j], x[p][i], y[p][j], sp[p]);
                 }
+        if (RIM && k == ms.jump_from + 1) {
+            // the rim's second half: u_f of the splits skipped joins the prefix
+            k = ms.jump_to;
+            prefix = (uint64_t)(cw.pre[k - 1] - cw.pre[k_lo - 1]);
+        }
     }
     if (m > M || nt == 0)
         return;
@@ -1560,8 +1644,8 @@ __device__ __forceinline__ void middle_lds_body(const ChainRows &r, const ChainW
         else
             return P::stored(a);
     };
-    if (n_part > 1) {
-        // a run of a cut range: the stored forms (value << 32) | s' and
+    if (ms.merge) {
+        // a part of a cut range: the stored forms (value << 32) | s' and
         // (value << 16) | s' order by value, then split, as unsigned words
 #pragma unroll
         for (int i = 0; i < kSub; ++i)
@@ -1572,9 +1656,10 @@ __device__ __forceinline__ void middle_lds_body(const ChainRows &r, const ChainW
                               (unsigned long long)stored(acc[i][j]));
         return;
     }
+
     // the wave whose last row is 16I + 16 and first column 16J + 1 holds the
     // corner
-    const bool corner = s0 + kSub - 1 == k_lo && t0 == k_hi + 1;
+    const bool corner = ms.owns_corner && s0 + kSub - 1 == k_lo && t0 == k_hi + 1;
 #pragma unroll
     for (int i = 0; i < kSub; ++i)
 #pragma unroll
@@ -1590,8 +1675,9 @@ __device__ __forceinline__ void middle_lds_body(const ChainRows &r, const ChainW
         }
 }
 
+template <bool RIM>
 __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__ params, int L, int M,
-                                                     int64_t pitch, int64_t rows, int delta, int n_part,
+                                                     int64_t pitch, int64_t rows, int delta, int range, int n_part,
                                                      int64_t *__restrict__ cost, int16_t *__restrict__ dec, Work w)
 {
     // a ring of 64-bit elements (the narrow path uses the first half)
@@ -1611,16 +1697,14 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
     if (middle_packed(cw, delta, k_hi - k_lo) || middle_runs(cw, delta, k_hi - k_lo))
         return;  // middle_packed_kernel takes this block-diagonal
     // this workgroup's part of the middle splits, as in middle_packed_kernel
-    const int part_len = (k_hi - k_lo + n_part) / n_part;
-    const int ka = k_lo + part * part_len;
-    const int kb = min(k_hi, ka + part_len - 1);
-    if (ka > kb)
+    const MiddleSplits ms = middle_splits(k_lo, k_hi, range, n_part, part);
+    if (ms.ka > ms.kb)
         return;
     const ChainRows r = chain_rows(params, w, L, c);
     int64_t *tab = cost + (int64_t)c * rows * pitch;
     int16_t *dtab = dec + (int64_t)c * rows * pitch;
     if (block_saturated(cw, I, J, m - (threadIdx.x & 63))) {
-        if (n_part == 1 && wave == 0 && m <= M) {
+        if (ms.owns_corner && wave == 0 && m <= M) {
             if (cw.narrow(delta))
                 store_saturated_corner<Narrow>(cw, L, m, pitch, I, J, tab, dtab);
             else
@@ -1629,11 +1713,11 @@ __global__ __launch_bounds__(256) void middle_kernel(const int64_t *__restrict__
         return;
     }
     if (cw.narrow(delta))
-        middle_lds_body<Narrow, true>(r, cw, L, M, m, pitch, I, J, wave, ka, kb, k_lo, k_hi, n_part, tab, dtab, ring);
+        middle_lds_body<Narrow, true, RIM>(r, cw, L, M, m, pitch, I, J, wave, ms, k_lo, k_hi, tab, dtab, ring);
     else if (cw.f64_keys(delta))
-        middle_lds_body<Wide, true>(r, cw, L, M, m, pitch, I, J, wave, ka, kb, k_lo, k_hi, n_part, tab, dtab, ring);
+        middle_lds_body<Wide, true, RIM>(r, cw, L, M, m, pitch, I, J, wave, ms, k_lo, k_hi, tab, dtab, ring);
     else
-        middle_lds_body<Wide, false>(r, cw, L, M, m, pitch, I, J, wave, ka, kb, k_lo, k_hi, n_part, tab, dtab, ring);
+        middle_lds_body<Wide, false, RIM>(r, cw, L, M, m, pitch, I, J, wave, ms, k_lo, k_hi, tab, dtab, ring);
 }
 
 // Edge splits, C_2 and the gates for the cells a + b = q of every block
@@ -1832,7 +1916,51 @@ Work work_view(void *base, int n_chains, int L, int64_t pitch)
     return w;
 }
 
-hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_t stream, LaunchObserver *obs)
+// The side stream of a device, for the middle products that run beside the
+// edge rounds, and the two events that order it with the caller's stream:
+// created on the first solve on the device and kept until the process ends.
+// A solve holds side_mutex while it enqueues, so that solves from several
+// host threads record and wait the events in turn; their device work still
+// overlaps.
+struct SideStream {
+    hipStream_t stream = nullptr;
+    hipEvent_t ready = nullptr, done = nullptr;
+};
+constexpr int kMaxDevices = 64;
+std::mutex side_mutex;
+SideStream side_streams[kMaxDevices];
+
+hipError_t device_side_stream(hipStream_t stream, SideStream *&side, std::unique_lock<std::mutex> &lock)
+{
+    hipDevice_t dev = 0;
+    hipError_t e = hipStreamGetDevice(stream, &dev);
+    if (e != hipSuccess)
+        return e;
+    if (dev < 0 || dev >= kMaxDevices)
+        return hipErrorInvalidDevice;
+    lock = std::unique_lock<std::mutex>(side_mutex);
+    SideStream &sd = side_streams[dev];
+    if (!sd.stream) {
+        int cur = 0;
+        if ((e = hipGetDevice(&cur)) != hipSuccess || (cur != dev && (e = hipSetDevice(dev)) != hipSuccess))
+            return e;
+        SideStream n;
+        e = hipStreamCreateWithFlags(&n.stream, hipStreamNonBlocking);
+        if (e == hipSuccess)
+            e = hipEventCreateWithFlags(&n.ready, hipEventDisableTiming);
+        if (e == hipSuccess)
+            e = hipEventCreateWithFlags(&n.done, hipEventDisableTiming);
+        const hipError_t r = cur != dev ? hipSetDevice(cur) : hipSuccess;
+        if (e != hipSuccess || r != hipSuccess)
+            return e != hipSuccess ? e : r;
+        sd = n;
+    }
+    side = &sd;
+    return hipSuccess;
+}
+
+hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_t stream, LaunchObserver *obs,
+                       bool side_stream)
 {
     // hipGetLastError also returns an error an earlier runtime call of the
     // caller left behind: clear it, so that the checks below see only these
@@ -1891,43 +2019,84 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
     if (streamed)
         return hipSuccess;
     const int nb = (L + kT - 1) / kT;
+    // workgroups of the middle launches: few blocks cut the middle ranges
+    // into runs for more workgroups (about 512), each of 32 splits or more
+    auto parts_of = [&](int delta) {
+        const unsigned wgs = mb64 * (unsigned)(nb - delta) * (unsigned)tb.n_chains;
+        const int span = (delta - 1) * kT + 1;
+        return wgs < 256 ? max(1, min((int)((512 + wgs - 1) / wgs), span / 32)) : 1;
+    };
+    // The middle launches of block-diagonal delta over one range (the
+    // packed-key kernel and the general one: each chain is taken by one of
+    // the two, the other returns at once), slots set to infinity first when
+    // the parts merge into them.  Work counts go with the packed kernel's
+    // launch (split candidates c1, corner cells finished).
+    auto middle = [&](int delta, int range, int n_part, hipStream_t st, uint64_t c1, uint64_t corners) {
+        hipError_t e;
+        if (n_part > 1 && range != kMidRim) {
+            fill_partials_kernel<<<dim3(mb256, (nb - delta) * kT * kT, tb.n_chains), 256, 0, st>>>(
+                L, tb.M, tb.pitch, tb.rows, delta, tb.cost, w);
+            if ((e = launched(kMiddle, 0, 0, 0)) != hipSuccess)
+                return e;
+        }
+        const dim3 grid(mb64 * n_part, nb - delta, tb.n_chains);
+        if (range == kMidRim)
+            middle_packed_kernel<true><<<grid, 256, 0, st>>>(tb.params, L, tb.M, tb.pitch, tb.rows, delta, range,
+                                                             n_part, tb.cost, tb.dec, w);
+        else
+            middle_packed_kernel<false><<<grid, 256, 0, st>>>(tb.params, L, tb.M, tb.pitch, tb.rows, delta, range,
+                                                              n_part, tb.cost, tb.dec, w);
+        if ((e = launched(kMiddle, c1, corners, corners)) != hipSuccess)
+            return e;
+        if (range == kMidRim)
+            middle_kernel<true><<<grid, 256, 0, st>>>(tb.params, L, tb.M, tb.pitch, tb.rows, delta, range, n_part,
+                                                      tb.cost, tb.dec, w);
+        else
+            middle_kernel<false><<<grid, 256, 0, st>>>(tb.params, L, tb.M, tb.pitch, tb.rows, delta, range, n_part,
+                                                       tb.cost, tb.dec, w);
+        return launched(kMiddle, 0, 0, 0);
+    };
+    // The inner middle range of block-diagonal delta + 1 (from delta + 1 = 3
+    // on) reads only block-diagonals up to delta - 1: it runs on the
+    // device's side stream beside the rim and the edges of delta, and its
+    // own rim follows them.  Only beside edges by rounds (the row edges of
+    // a batch lose: 4.95 -> 5.06 ms for 256 chains of L = 64), and not under
+    // an observer, whose per-class times need one stream.
+    const bool overlap = side_stream && !obs && schedule != ROTOR_SCHEDULE_BLOCKED_SERIAL && nb >= 4;
+    SideStream *side = nullptr;
+    std::unique_lock<std::mutex> side_lock;
+    if (overlap && (e = device_side_stream(stream, side, side_lock)) != hipSuccess)
+        return e;
+    bool inner_done = false;  // the inner range of delta ran beside the edges of delta - 1
     for (int delta = 1; delta < nb; ++delta) {
         // pairs of the block-diagonal: full rows of 16, columns up to L
         uint64_t pairs = 0;
         for (int I = 0; I + delta < nb; ++I)
             pairs += (uint64_t)kT * (uint64_t)min(kT, L - (I + delta) * kT);
-        // A block-diagonal of few blocks cuts the middle ranges into runs for
-        // more workgroups (about 512), each of 32 splits or more; the corners
-        // then go to the edge round a + b = 0.
-        const unsigned wgs = mb64 * (unsigned)(nb - delta) * (unsigned)tb.n_chains;
         const int span = (delta - 1) * kT + 1;
-        int n_part = 1;
-        if (wgs < 256)
-            n_part = max(1, min((int)((512 + wgs - 1) / wgs), span / 32));
-        const int finish = n_part == 1 ? 1 : 0;
-        if ((e = before(kMiddle)) != hipSuccess)
-            return e;
-        if (n_part > 1) {
-            fill_partials_kernel<<<dim3(mb256, (nb - delta) * kT * kT, tb.n_chains), 256, 0, stream>>>(
-                L, tb.M, tb.pitch, tb.rows, delta, tb.cost, w);
-            if ((e = launched(kMiddle, 0, 0, 0)) != hipSuccess)
-                return e;
-        }
-        // each chain is taken by one of the two kernels, the other returns at once
-        middle_packed_kernel<<<dim3(mb64 * n_part, nb - delta, tb.n_chains), 256, 0, stream>>>(
-            tb.params, L, tb.M, tb.pitch, tb.rows, delta, n_part, tb.cost, tb.dec, w);
-        // the middle splits of every pair, and C_2 of the corner cell of every block
-        const uint64_t corners = finish ? (uint64_t)(nb - delta) : 0;
-        if ((e = launched(kMiddle, pairs * (uint64_t)span, corners, corners)) != hipSuccess)
-            return e;
-        if ((e = before(kMiddle)) != hipSuccess)
-            return e;
-        middle_kernel<<<dim3(mb64 * n_part, nb - delta, tb.n_chains), 256, 0, stream>>>(
-            tb.params, L, tb.M, tb.pitch, tb.rows, delta, n_part, tb.cost, tb.dec, w);
-        if ((e = launched(kMiddle, 0, 0, 0)) != hipSuccess)
-            return e;
         const bool rows = schedule == ROTOR_SCHEDULE_BLOCKED_ROWS ||
                           (schedule != ROTOR_SCHEDULE_BLOCKED_ROUNDS && row_edges((int64_t)(nb - delta) * tb.n_chains));
+        // the middle splits of every pair, and C_2 of the corner cell of
+        // every block when the middle products finish the corners
+        const int n_part = inner_done ? 1 : parts_of(delta);
+        const int finish = !inner_done && n_part == 1 ? 1 : 0;
+        const uint64_t corners = finish ? (uint64_t)(nb - delta) : 0;
+        if ((e = before(kMiddle)) != hipSuccess)
+            return e;
+        if (inner_done && (e = hipStreamWaitEvent(stream, side->done, 0)) != hipSuccess)
+            return e;
+        const bool next_inner = overlap && !rows && delta + 1 < nb && delta + 1 >= 3;
+        if (next_inner) {
+            if ((e = hipEventRecord(side->ready, stream)) != hipSuccess ||
+                (e = hipStreamWaitEvent(side->stream, side->ready, 0)) != hipSuccess ||
+                (e = middle(delta + 1, kMidInner, parts_of(delta + 1), side->stream, 0, 0)) != hipSuccess ||
+                (e = hipEventRecord(side->done, side->stream)) != hipSuccess)
+                return e;
+        }
+        if ((e = middle(delta, inner_done ? kMidRim : kMidAll, n_part, stream, pairs * (uint64_t)span, corners)) !=
+            hipSuccess)
+            return e;
+        inner_done = next_inner;
         if (rows) {
             for (int a = 0; a < kT; ++a) {
                 uint64_t c1 = 0, cells = 0;

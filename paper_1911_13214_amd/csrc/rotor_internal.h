@@ -98,9 +98,11 @@ struct LaunchObserver {
 };
 
 // Enqueue the whole table fill on `stream` with one of the ROTOR_SCHEDULE_*
-// orders.  Returns a HIP error code.
+// orders; with side_stream, the blocked orders run the inner middle ranges
+// on the device's side stream beside the edges (joined back into `stream`).
+// Returns a HIP error code.
 hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_t stream,
-                       LaunchObserver *obs = nullptr);
+                       LaunchObserver *obs = nullptr, bool side_stream = true);
 
 // Edges of the blocked fill by rows: whether a block-diagonal with `blocks`
 // blocks over all chains takes them, and the launch of row 16(I + 1) - a of

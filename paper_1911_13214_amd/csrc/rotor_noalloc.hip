@@ -65,5 +65,7 @@ extern "C" int32_t rotor_solve_noalloc(const int64_t *d_params, int32_t n_chains
     // the fill overwrites every workspace word it reads before reading it,
     // so nothing left by an earlier call needs clearing
     const Work w = work_view(work, n_chains, L, tb.pitch);
-    return launch_fill(tb, w, ROTOR_SCHEDULE_AUTO, (hipStream_t)stream) == hipSuccess ? ROTOR_OK : ROTOR_EDEVICE;
+    // no side stream: creating one on the first call would allocate
+    return launch_fill(tb, w, ROTOR_SCHEDULE_AUTO, (hipStream_t)stream, nullptr, false) == hipSuccess ? ROTOR_OK
+                                                                                                      : ROTOR_EDEVICE;
 }

@@ -51,7 +51,7 @@ SIGNATURES = {
 }
 
 KERNEL_CLASSES = ("leaf", "diag", "middle", "edge", "prep")
-SCHEDULES = {"auto": 0, "blocked": 1, "diagonal": 2, "rows": 3, "rounds": 4}
+SCHEDULES = {"auto": 0, "blocked": 1, "diagonal": 2, "rows": 3, "rounds": 4, "serial": 5}
 
 
 class KernelStats(ctypes.Structure):
@@ -181,7 +181,8 @@ def rotor_solve_schedule(d_params, n_chains: int, L: int, M: int, d_cost, d_dec,
                          stream=None):
     """rotor_solve with an explicit fill order, a key of SCHEDULES: "auto",
     "blocked" (edges by rounds or rows, chosen per block-diagonal), "rows",
-    "rounds" or "diagonal" (same tables, different speed)."""
+    "rounds", "serial" (blocked, every middle product on the caller's
+    stream) or "diagonal" (same tables, different speed)."""
     p, c, d, w, wb = _solve_ptrs(d_params, n_chains, L, M, d_cost, d_dec, d_work)
     _check(lib().rotor_solve_schedule(p, n_chains, L, M, c, d, w, wb, _stream_ptr(stream), SCHEDULES[schedule]),
            "rotor_solve_schedule")

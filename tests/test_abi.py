@@ -128,7 +128,7 @@ def test_solve_and_reconstruct_reject_bad_arguments_before_any_device_work():
     assert lib.rotor_solve(fake, 1, 10, 100, fake, ctypes.c_void_p(0x1001), fake, big, None) == rotor.ROTOR_EINVAL
     assert lib.rotor_solve(fake, 1, 10, 100, fake, fake, ctypes.c_void_p(0x1004), big, None) == rotor.ROTOR_EINVAL
     s = lib.rotor_solve_schedule
-    for bad in (-1, 5, 1 << 20):
+    for bad in (-1, 6, 1 << 20):
         assert s(fake, 1, 10, 100, fake, fake, fake, big, None, bad) == rotor.ROTOR_EINVAL
     assert s(fake, 1, 10, 100, fake, fake, fake, need - 1, None, rotor.SCHEDULES["blocked"]) == rotor.ROTOR_EINVAL
     assert s(None, 1, 10, 100, fake, fake, fake, big, None, rotor.SCHEDULES["diagonal"]) == rotor.ROTOR_EINVAL

@@ -20,10 +20,11 @@ def say(msg):
     print(msg, flush=True)
 
 
-# the blocked fill with its edges by anti-diagonal rounds and by rows, and
-# the streamed diagonals
-SCHEDULES = ["rounds", "rows", "diagonal"]
-EDGE_ORDERS = ["rounds", "rows"]
+# the blocked fill with its edges by anti-diagonal rounds and by rows (both
+# with the inner middle products beside the previous edges), the blocked fill
+# on one stream, and the streamed diagonals
+SCHEDULES = ["rounds", "rows", "serial", "diagonal"]
+EDGE_ORDERS = ["rounds", "rows", "serial"]
 _oracle_cache = {}
 
 
