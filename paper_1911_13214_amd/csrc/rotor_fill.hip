@@ -2026,19 +2026,22 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
         const int span = (delta - 1) * kT + 1;
         return wgs < 256 ? max(1, min((int)((512 + wgs - 1) / wgs), span / 32)) : 1;
     };
-    // The middle launches of block-diagonal delta over one range (the
-    // packed-key kernel and the general one: each chain is taken by one of
+    // The middle launches of block-diagonal delta over one range: the
+    // general kernel and the packed-key one (each chain is taken by one of
     // the two, the other returns at once), slots set to infinity first when
     // the parts merge into them.  Work counts go with the packed kernel's
     // launch (split candidates c1, corner cells finished).
-    auto middle = [&](int delta, int range, int n_part, hipStream_t st, uint64_t c1, uint64_t corners) {
-        hipError_t e;
-        if (n_part > 1 && range != kMidRim) {
-            fill_partials_kernel<<<dim3(mb256, (nb - delta) * kT * kT, tb.n_chains), 256, 0, st>>>(
-                L, tb.M, tb.pitch, tb.rows, delta, tb.cost, w);
-            if ((e = launched(kMiddle, 0, 0, 0)) != hipSuccess)
-                return e;
-        }
+    auto middle_general = [&](int delta, int range, int n_part, hipStream_t st) {
+        const dim3 grid(mb64 * n_part, nb - delta, tb.n_chains);
+        if (range == kMidRim)
+            middle_kernel<true><<<grid, 256, 0, st>>>(tb.params, L, tb.M, tb.pitch, tb.rows, delta, range, n_part,
+                                                      tb.cost, tb.dec, w);
+        else
+            middle_kernel<false><<<grid, 256, 0, st>>>(tb.params, L, tb.M, tb.pitch, tb.rows, delta, range, n_part,
+                                                       tb.cost, tb.dec, w);
+        return launched(kMiddle, 0, 0, 0);
+    };
+    auto middle_packed = [&](int delta, int range, int n_part, hipStream_t st, uint64_t c1, uint64_t corners) {
         const dim3 grid(mb64 * n_part, nb - delta, tb.n_chains);
         if (range == kMidRim)
             middle_packed_kernel<true><<<grid, 256, 0, st>>>(tb.params, L, tb.M, tb.pitch, tb.rows, delta, range,
@@ -2046,14 +2049,11 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
         else
             middle_packed_kernel<false><<<grid, 256, 0, st>>>(tb.params, L, tb.M, tb.pitch, tb.rows, delta, range,
                                                               n_part, tb.cost, tb.dec, w);
-        if ((e = launched(kMiddle, c1, corners, corners)) != hipSuccess)
-            return e;
-        if (range == kMidRim)
-            middle_kernel<true><<<grid, 256, 0, st>>>(tb.params, L, tb.M, tb.pitch, tb.rows, delta, range, n_part,
-                                                      tb.cost, tb.dec, w);
-        else
-            middle_kernel<false><<<grid, 256, 0, st>>>(tb.params, L, tb.M, tb.pitch, tb.rows, delta, range, n_part,
-                                                       tb.cost, tb.dec, w);
+        return launched(kMiddle, c1, corners, corners);
+    };
+    auto fill_partials = [&](int delta, hipStream_t st) {
+        fill_partials_kernel<<<dim3(mb256, (nb - delta) * kT * kT, tb.n_chains), 256, 0, st>>>(
+            L, tb.M, tb.pitch, tb.rows, delta, tb.cost, w);
         return launched(kMiddle, 0, 0, 0);
     };
     // The inner middle range of block-diagonal delta + 1 (from delta + 1 = 3
@@ -2085,16 +2085,26 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
             return e;
         if (inner_done && (e = hipStreamWaitEvent(stream, side->done, 0)) != hipSuccess)
             return e;
+        const int range = inner_done ? kMidRim : kMidAll;
+        if (n_part > 1 && (e = fill_partials(delta, stream)) != hipSuccess)
+            return e;
+        // the general kernel first: its workgroups, with their larger LDS
+        // ring, would otherwise wait for those of the next inner range even
+        // where they return at once
+        if ((e = middle_general(delta, range, n_part, stream)) != hipSuccess)
+            return e;
         const bool next_inner = overlap && !rows && delta + 1 < nb && delta + 1 >= 3;
         if (next_inner) {
+            const int np = parts_of(delta + 1);
             if ((e = hipEventRecord(side->ready, stream)) != hipSuccess ||
                 (e = hipStreamWaitEvent(side->stream, side->ready, 0)) != hipSuccess ||
-                (e = middle(delta + 1, kMidInner, parts_of(delta + 1), side->stream, 0, 0)) != hipSuccess ||
+                (np > 1 && (e = fill_partials(delta + 1, side->stream)) != hipSuccess) ||
+                (e = middle_packed(delta + 1, kMidInner, np, side->stream, 0, 0)) != hipSuccess ||
+                (e = middle_general(delta + 1, kMidInner, np, side->stream)) != hipSuccess ||
                 (e = hipEventRecord(side->done, side->stream)) != hipSuccess)
                 return e;
         }
-        if ((e = middle(delta, inner_done ? kMidRim : kMidAll, n_part, stream, pairs * (uint64_t)span, corners)) !=
-            hipSuccess)
+        if ((e = middle_packed(delta, range, n_part, stream, pairs * (uint64_t)span, corners)) != hipSuccess)
             return e;
         inner_done = next_inner;
         if (rows) {
