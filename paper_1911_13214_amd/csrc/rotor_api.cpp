@@ -3,6 +3,7 @@
 // kernels; the host-only entry points are in rotor_host.cpp.
 #include <stdint.h>
 
+#include <map>
 #include <vector>
 
 #include "rotor_internal.h"
@@ -36,16 +37,17 @@ Tables make_tables(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t
 }
 
 // Adds up the work counts of every launch and times each run of consecutive
-// launches of one kernel class with one pair of HIP events on the launch
-// stream (about two runs per block-diagonal), so the events add little to
-// what they measure.
+// launches of one kernel class on one stream with one pair of HIP events on
+// that stream (about two runs per block-diagonal and stream), so the events
+// add little to what they measure.  Runs on the side stream overlap those on
+// the caller's: the class times then add up to more than the solve.
 struct TimingObserver : LaunchObserver {
     struct Run {
         hipEvent_t start, stop;
         KernelClass k;
     };
     std::vector<Run> runs;
-    bool open = false;  // the last run has no stop recorded yet
+    std::map<hipStream_t, size_t> open;  // the run of each stream with no stop recorded yet
     rotor_kernel_stats *stats;
 
     explicit TimingObserver(rotor_kernel_stats *st) : stats(st)
@@ -55,14 +57,18 @@ struct TimingObserver : LaunchObserver {
     }
     hipError_t close(hipStream_t s)
     {
-        if (!open)
+        auto it = open.find(s);
+        if (it == open.end())
             return hipSuccess;
-        open = false;
-        return hipEventRecord(runs.back().stop, s);
+        const size_t i = it->second;
+        open.erase(it);
+        return hipEventRecord(runs[i].stop, s);
     }
+    hipError_t end_stream(hipStream_t s) override { return close(s); }
     hipError_t before(KernelClass k, hipStream_t s) override
     {
-        if (open && runs.back().k == k)
+        auto it = open.find(s);
+        if (it != open.end() && runs[it->second].k == k)
             return hipSuccess;
         hipError_t e = close(s);
         Run r{nullptr, nullptr, k};
@@ -73,7 +79,8 @@ struct TimingObserver : LaunchObserver {
         if (e == hipSuccess)
             e = hipEventRecord(r.start, s);
         runs.push_back(r);
-        open = e == hipSuccess;
+        if (e == hipSuccess)
+            open[s] = runs.size() - 1;
         return e;
     }
     hipError_t after(KernelClass k, const LaunchWork &w, hipStream_t) override
@@ -87,9 +94,23 @@ struct TimingObserver : LaunchObserver {
     }
     hipError_t finish(hipStream_t s)
     {
-        hipError_t e = close(s);
+        // runs still open (a launch failed before its stream joined) close
+        // on their own streams, which are then waited for too
+        std::vector<hipStream_t> others;
+        for (const auto &o : open)
+            if (o.first != s)
+                others.push_back(o.first);
+        hipError_t e = hipSuccess;
+        for (hipStream_t o : others)
+            if (e == hipSuccess)
+                e = close(o);
+        if (e == hipSuccess)
+            e = close(s);
         if (e == hipSuccess)
             e = hipStreamSynchronize(s);
+        for (hipStream_t o : others)
+            if (e == hipSuccess)
+                e = hipStreamSynchronize(o);
         for (Run &r : runs) {
             float ms = 0.f;
             if (e == hipSuccess && r.start && r.stop)

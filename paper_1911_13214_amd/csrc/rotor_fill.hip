@@ -1112,11 +1112,11 @@ __device__ inline void saturated_splits(const ChainWork &cw, const int32_t *wa_v
 // operands lie in blocks up to two block-diagonals back, so that this part
 // can run beside the previous block-diagonal's edge rounds; its slots are
 // written as with kMidAll.  kMidRim: those 2 kT splits, after the edges, in
-// one part that jumps from the first kT to the last kT and folds its minimum
-// into the slots the inner part wrote (a plain read, minimum and write: the
-// workgroup owns its slots).  The corner is finished here only with kMidAll
-// and one part; else its partial is stored like any other and the edge
-// round a + b = 0 finishes it.
+// one part that jumps from the first kT to the last kT and merges its
+// minimum into the slots the inner part wrote by atomic minimum.  The corner
+// is finished by the launch that completes its range: kMidAll in one part,
+// or kMidRim (which reads the inner part's slot for it); else its partial is
+// stored like any other and the edge round a + b = 0 finishes it.
 constexpr int kMidAll = 0, kMidInner = 1, kMidRim = 2;
 struct MiddleSplits {
     int ka, kb;        // this workgroup's first and last split
@@ -1146,7 +1146,7 @@ __device__ inline MiddleSplits middle_splits(int k_lo, int k_hi, int range, int 
         r.n_splits = r.kb - r.ka + 1;
     }
     r.merge = n_part > 1 || range == kMidRim;
-    r.owns_corner = n_part == 1 && range == kMidAll;
+    r.owns_corner = (n_part == 1 && range == kMidAll) || range == kMidRim;
     return r;
 }
 
@@ -1377,6 +1377,11 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
         if (k > run_base)
             flush();
         if (corner && m <= M) {
+            if constexpr (RIM) {
+                // the inner part's form in the corner's slot
+                const uint64_t inner = (uint64_t)tab[row_of(L, k_lo, k_hi + 1) * pitch + m];
+                corner_best = inner < corner_best ? inner : corner_best;
+            }
             Narrow::Acc a;
             Narrow::init(a);
             if (corner_best < ((uint64_t)kInf32 << 32)) {
@@ -1398,16 +1403,22 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
         for (int i = 0; i < kSub; ++i)
 #pragma unroll
             for (int j = 0; j < kSub; ++j)
-                if (j < nt)
+                if (j < nt && !(i == kSub - 1 && j == 0 && corner))
                     atomicMin(&cw.shadow[row_of(L, s0 + i, t0 + j) * pitch + m], acc[i][j]);
-        return;
+        if (!corner)
+            return;
     }
 #pragma unroll
     for (int i = 0; i < kSub; ++i)
 #pragma unroll
         for (int j = 0; j < kSub; ++j) {
             if (i == kSub - 1 && j == 0 && corner) {
-                const uint32_t key = acc[i][j];
+                uint32_t key = acc[i][j];
+                if constexpr (RIM) {
+                    // the inner part's key in the corner's slot
+                    const uint32_t inner = __builtin_nontemporal_load(&cw.shadow[row_of(L, k_lo, k_hi + 1) * pitch + m]);
+                    key = inner < key ? inner : key;
+                }
                 Narrow::Acc a;
                 Narrow::init(a);
                 if (key != kInf32) {
@@ -1415,7 +1426,7 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
                     a.sp = (uint32_t)(k_lo + 1) + (key & ((1u << S) - 1u));
                 }
                 finish_corner<Narrow>(r, cw, L, m, pitch, k_lo, k_hi + 1, a, tab, dec + (int64_t)c * rows * pitch);
-            } else if (j < nt) {
+            } else if (j < nt && !ms.merge) {
                 __builtin_nontemporal_store(acc[i][j], &cw.shadow[row_of(L, s0 + i, t0 + j) * pitch + m]);
             }
         }
@@ -1644,6 +1655,9 @@ __device__ __forceinline__ void middle_lds_body(const ChainRows &r, const ChainW
         else
             return P::stored(a);
     };
+    // the wave whose last row is 16I + 16 and first column 16J + 1 holds the
+    // corner
+    const bool corner = ms.owns_corner && s0 + kSub - 1 == k_lo && t0 == k_hi + 1;
     if (ms.merge) {
         // a part of a cut range: the stored forms (value << 32) | s' and
         // (value << 16) | s' order by value, then split, as unsigned words
@@ -1651,15 +1665,23 @@ __device__ __forceinline__ void middle_lds_body(const ChainRows &r, const ChainW
         for (int i = 0; i < kSub; ++i)
 #pragma unroll
             for (int j = 0; j < kSub; ++j)
-                if (j < nt)
+                if (j < nt && !(i == kSub - 1 && j == 0 && corner))
                     atomicMin((unsigned long long *)&tab[row_of(L, s0 + i, t0 + j) * pitch + m],
                               (unsigned long long)stored(acc[i][j]));
+        if constexpr (RIM) {
+            if (corner) {
+                // the smaller of the rim's form and the inner part's in the
+                // corner's slot completes the corner's middle range
+                const uint64_t inner = (uint64_t)tab[row_of(L, k_lo, k_hi + 1) * pitch + m];
+                const uint64_t own = (uint64_t)stored(acc[kSub - 1][0]);
+                typename P::Acc a;
+                P::init(a);
+                P::merge_later(a, (int64_t)(inner < own ? inner : own));
+                finish_corner<P>(r, cw, L, m, pitch, k_lo, k_hi + 1, a, tab, dtab);
+            }
+        }
         return;
     }
-
-    // the wave whose last row is 16I + 16 and first column 16J + 1 holds the
-    // corner
-    const bool corner = ms.owns_corner && s0 + kSub - 1 == k_lo && t0 == k_hi + 1;
 #pragma unroll
     for (int i = 0; i < kSub; ++i)
 #pragma unroll
@@ -1973,13 +1995,19 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
     const unsigned mb64 = (unsigned)((tb.M + 1 + 63) / 64);
     const unsigned mb_edge = (unsigned)((tb.M + kEdgeThreads * kEdgeBudgets) / (kEdgeThreads * kEdgeBudgets));
     const unsigned mb_diag = (unsigned)((tb.M + kEdgeThreads * kDiagBudgets) / (kEdgeThreads * kDiagBudgets));
-    auto launched = [&](KernelClass k, uint64_t c1, uint64_t c2, uint64_t cells) -> hipError_t {
+    auto launched_on = [&](hipStream_t st, KernelClass k, uint64_t c1, uint64_t c2, uint64_t cells) -> hipError_t {
         hipError_t e = check();
         if (e == hipSuccess && obs)
-            e = obs->after(k, LaunchWork{c1 * W * nc, c2 * W * nc, cells * W * nc}, stream);
+            e = obs->after(k, LaunchWork{c1 * W * nc, c2 * W * nc, cells * W * nc}, st);
         return e;
     };
-    auto before = [&](KernelClass k) -> hipError_t { return obs ? obs->before(k, stream) : hipSuccess; };
+    auto launched = [&](KernelClass k, uint64_t c1, uint64_t c2, uint64_t cells) {
+        return launched_on(stream, k, c1, c2, cells);
+    };
+    auto before_on = [&](hipStream_t st, KernelClass k) -> hipError_t {
+        return obs ? obs->before(k, st) : hipSuccess;
+    };
+    auto before = [&](KernelClass k) { return before_on(stream, k); };
     hipError_t e;
 
     if ((e = before(kPrep)) != hipSuccess)
@@ -2032,6 +2060,9 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
     // the parts merge into them.  Work counts go with the packed kernel's
     // launch (split candidates c1, corner cells finished).
     auto middle_general = [&](int delta, int range, int n_part, hipStream_t st) {
+        hipError_t e = before_on(st, kMiddle);
+        if (e != hipSuccess)
+            return e;
         const dim3 grid(mb64 * n_part, nb - delta, tb.n_chains);
         if (range == kMidRim)
             middle_kernel<true><<<grid, 256, 0, st>>>(tb.params, L, tb.M, tb.pitch, tb.rows, delta, range, n_part,
@@ -2039,9 +2070,12 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
         else
             middle_kernel<false><<<grid, 256, 0, st>>>(tb.params, L, tb.M, tb.pitch, tb.rows, delta, range, n_part,
                                                        tb.cost, tb.dec, w);
-        return launched(kMiddle, 0, 0, 0);
+        return launched_on(st, kMiddle, 0, 0, 0);
     };
     auto middle_packed = [&](int delta, int range, int n_part, hipStream_t st, uint64_t c1, uint64_t corners) {
+        hipError_t e = before_on(st, kMiddle);
+        if (e != hipSuccess)
+            return e;
         const dim3 grid(mb64 * n_part, nb - delta, tb.n_chains);
         if (range == kMidRim)
             middle_packed_kernel<true><<<grid, 256, 0, st>>>(tb.params, L, tb.M, tb.pitch, tb.rows, delta, range,
@@ -2049,40 +2083,45 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
         else
             middle_packed_kernel<false><<<grid, 256, 0, st>>>(tb.params, L, tb.M, tb.pitch, tb.rows, delta, range,
                                                               n_part, tb.cost, tb.dec, w);
-        return launched(kMiddle, c1, corners, corners);
+        return launched_on(st, kMiddle, c1, corners, corners);
     };
     auto fill_partials = [&](int delta, hipStream_t st) {
+        hipError_t e = before_on(st, kMiddle);
+        if (e != hipSuccess)
+            return e;
         fill_partials_kernel<<<dim3(mb256, (nb - delta) * kT * kT, tb.n_chains), 256, 0, st>>>(
             L, tb.M, tb.pitch, tb.rows, delta, tb.cost, w);
-        return launched(kMiddle, 0, 0, 0);
+        return launched_on(st, kMiddle, 0, 0, 0);
+    };
+    // pairs of block-diagonal delta: full rows of 16, columns up to L
+    auto pairs_of = [&](int delta) {
+        uint64_t pairs = 0;
+        for (int I = 0; I + delta < nb; ++I)
+            pairs += (uint64_t)kT * (uint64_t)min(kT, L - (I + delta) * kT);
+        return pairs;
     };
     // The inner middle range of block-diagonal delta + 1 (from delta + 1 = 3
     // on) reads only block-diagonals up to delta - 1: it runs on the
     // device's side stream beside the rim and the edges of delta, and its
-    // own rim follows them.  Only beside edges by rounds (the row edges of
-    // a batch lose: 4.95 -> 5.06 ms for 256 chains of L = 64), and not under
-    // an observer, whose per-class times need one stream.
-    const bool overlap = side_stream && !obs && schedule != ROTOR_SCHEDULE_BLOCKED_SERIAL && nb >= 4;
+    // own rim follows them; only beside edges by rounds (the row edges of a
+    // batch lose: 4.95 -> 5.06 ms for 256 chains of L = 64).  An observer
+    // sees the side stream's launches on that stream.
+    const bool overlap = side_stream && schedule != ROTOR_SCHEDULE_BLOCKED_SERIAL && nb >= 4;
     SideStream *side = nullptr;
     std::unique_lock<std::mutex> side_lock;
     if (overlap && (e = device_side_stream(stream, side, side_lock)) != hipSuccess)
         return e;
     bool inner_done = false;  // the inner range of delta ran beside the edges of delta - 1
     for (int delta = 1; delta < nb; ++delta) {
-        // pairs of the block-diagonal: full rows of 16, columns up to L
-        uint64_t pairs = 0;
-        for (int I = 0; I + delta < nb; ++I)
-            pairs += (uint64_t)kT * (uint64_t)min(kT, L - (I + delta) * kT);
+        const uint64_t pairs = pairs_of(delta);
         const int span = (delta - 1) * kT + 1;
         const bool rows = schedule == ROTOR_SCHEDULE_BLOCKED_ROWS ||
                           (schedule != ROTOR_SCHEDULE_BLOCKED_ROUNDS && row_edges((int64_t)(nb - delta) * tb.n_chains));
         // the middle splits of every pair, and C_2 of the corner cell of
         // every block when the middle products finish the corners
         const int n_part = inner_done ? 1 : parts_of(delta);
-        const int finish = !inner_done && n_part == 1 ? 1 : 0;
+        const int finish = inner_done || n_part == 1 ? 1 : 0;
         const uint64_t corners = finish ? (uint64_t)(nb - delta) : 0;
-        if ((e = before(kMiddle)) != hipSuccess)
-            return e;
         if (inner_done && (e = hipStreamWaitEvent(stream, side->done, 0)) != hipSuccess)
             return e;
         const int range = inner_done ? kMidRim : kMidAll;
@@ -2095,16 +2134,21 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
             return e;
         const bool next_inner = overlap && !rows && delta + 1 < nb && delta + 1 >= 3;
         if (next_inner) {
+            // the inner splits of every pair of delta + 1: all but 2 kT
             const int np = parts_of(delta + 1);
+            const uint64_t inner = pairs_of(delta + 1) * (uint64_t)(delta * kT + 1 - 2 * kT);
             if ((e = hipEventRecord(side->ready, stream)) != hipSuccess ||
                 (e = hipStreamWaitEvent(side->stream, side->ready, 0)) != hipSuccess ||
                 (np > 1 && (e = fill_partials(delta + 1, side->stream)) != hipSuccess) ||
-                (e = middle_packed(delta + 1, kMidInner, np, side->stream, 0, 0)) != hipSuccess ||
+                (e = middle_packed(delta + 1, kMidInner, np, side->stream, inner, 0)) != hipSuccess ||
                 (e = middle_general(delta + 1, kMidInner, np, side->stream)) != hipSuccess ||
+                (obs && (e = obs->end_stream(side->stream)) != hipSuccess) ||
                 (e = hipEventRecord(side->done, side->stream)) != hipSuccess)
                 return e;
         }
-        if ((e = middle_packed(delta, range, n_part, stream, pairs * (uint64_t)span, corners)) != hipSuccess)
+        // the middle splits of every pair (the rim's 2 kT after an inner range)
+        const uint64_t c1 = pairs * (uint64_t)(range == kMidRim ? 2 * kT : span);
+        if ((e = middle_packed(delta, range, n_part, stream, c1, corners)) != hipSuccess)
             return e;
         inner_done = next_inner;
         if (rows) {

@@ -94,13 +94,16 @@ struct LaunchWork {
 struct LaunchObserver {
     virtual hipError_t before(KernelClass k, hipStream_t s) = 0;
     virtual hipError_t after(KernelClass k, const LaunchWork &w, hipStream_t s) = 0;
+    // no more launches on s before it joins the caller's stream
+    virtual hipError_t end_stream(hipStream_t s) = 0;
     virtual ~LaunchObserver() {}
 };
 
 // Enqueue the whole table fill on `stream` with one of the ROTOR_SCHEDULE_*
 // orders; with side_stream, the blocked orders run the inner middle ranges
-// on the device's side stream beside the edges (joined back into `stream`).
-// Returns a HIP error code.
+// on the device's side stream beside the edges (joined back into `stream`),
+// and the observer sees those launches on that stream.  Returns a HIP error
+// code.
 hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_t stream,
                        LaunchObserver *obs = nullptr, bool side_stream = true);
 
