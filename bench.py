@@ -372,7 +372,10 @@ def main():
     # rates that can reach a peak.  Without a current record the algorithmic
     # rate is all there is, and the line says so.
     alg_achieved = kd["alg_bytes"] / (kd["ms"] * 1e-3) / 1e9
-    roof = {"kernel": f"{dom}_kernel", "launches_per_step": kd["launches"], "avg_launch_us": kd["avg_launch_us"],
+    # the class's kernels as the counter record names them (else the class)
+    kernel_names = "+".join(records[dom]["kernels"]) if records[dom] and records[dom].get("kernels") else dom
+    roof = {"kernel": kernel_names, "kernel_class": dom, "launches_per_step": kd["launches"],
+            "avg_launch_us": kd["avg_launch_us"],
             "alg_GBps": round(alg_achieved, 1), "alg_frac": round(alg_achieved / HBM_PEAK_GBS, 4),
             "alg_basis": "16 B per C_1 candidate, 8 per C_2 candidate, 10 per cell written"}
     if "hbm_frac" in kd:
