@@ -1169,8 +1169,6 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
                                                             int16_t *__restrict__ dec, Work w)
 {
     __shared__ uint32_t ring[kRing * kStage * kSplitWords];
-    if (RIM)
-        __builtin_amdgcn_s_setprio(3);  // on the critical path, as the edges
     const Tile tile = xcd_tile();
     const int c = tile.z;
     const int I = tile.y;
@@ -1881,10 +1879,6 @@ __global__ __launch_bounds__(kEdgeThreads) void edge_kernel(const int64_t *__res
                                                    int n_q, int64_t *__restrict__ cost, int16_t *__restrict__ dec,
                                                    Work w)
 {
-    // the caller's stream carries the critical path (edges and rims): its
-    // waves are issued before the inner middle products' beside them
-    // (measured on MI355X at L = 500, M = 5000: 18.00 -> 17.96 ms)
-    __builtin_amdgcn_s_setprio(3);
     const int c = blockIdx.z;
     const int blk = blockIdx.y / n_q;
     const int a = a_min + (blockIdx.y - blk * n_q);
