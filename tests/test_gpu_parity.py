@@ -778,6 +778,38 @@ def test_fill_replays_from_a_captured_graph():
         assert_same(params, M, cost, dec)
 
 
+def test_two_stream_fill_replays_from_a_captured_graph():
+    # the blocked order forks its inner middle products onto the library's
+    # side stream and joins it back with events: under capture that is a
+    # fork and a join of the graph, and every replay must rebuild the tables
+    import torch
+    from paper_1911_13214_amd import rotor
+    L, M = 80, 300
+    params = chaingen.random_chains(1, L, seed=808)
+    say(f"graph replay of the two-stream blocked fill L={L} M={M}")
+    d_params = rotor.upload_params(params, M)
+    cost, dec = rotor.alloc_tables(1, L, M)
+    work = rotor.alloc_workspace(1, L, M)
+    st = torch.cuda.Stream()
+    st.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(st):
+        rotor.rotor_solve_schedule(d_params, 1, L, M, cost, dec, work, "rounds", st)
+    torch.cuda.synchronize()
+    assert_same(params, M, cost, dec)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=st):
+        rotor.rotor_solve_schedule(d_params, 1, L, M, cost, dec, work, "rounds", st)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        cost.fill_(-7)
+        dec.fill_(-7)
+        work.fill_(-7)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert_same(params, M, cost, dec)
+
+
 def test_workspace_too_small_is_rejected():
     import torch
     from paper_1911_13214_amd import rotor
