@@ -810,6 +810,42 @@ def test_two_stream_fill_replays_from_a_captured_graph():
         assert_same(params, M, cost, dec)
 
 
+def test_two_stream_fills_from_two_host_threads():
+    # solves from several host threads share the device's side stream: each
+    # enqueues under the library's lock, and every table must come out whole
+    import threading
+    import torch
+    from paper_1911_13214_amd import rotor
+    L, M = 72, 260
+    chains = [chaingen.random_chains(1, L, seed=900 + i) for i in range(2)]
+    say(f"two host threads, two-stream blocked fills L={L} M={M}")
+    bufs = []
+    for p in chains:
+        bufs.append((rotor.upload_params(p, M), *rotor.alloc_tables(1, L, M), rotor.alloc_workspace(1, L, M),
+                     torch.cuda.Stream()))
+    torch.cuda.synchronize()
+    errors = []
+
+    def run(i):
+        try:
+            d_params, cost, dec, work, st = bufs[i]
+            for _ in range(4):
+                rotor.rotor_solve_schedule(d_params, 1, L, M, cost, dec, work, "rounds", st)
+            st.synchronize()
+        except Exception as e:  # reported in the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=run, args=(i,)) for i in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    torch.cuda.synchronize()
+    for p, (_, cost, dec, _, _) in zip(chains, bufs):
+        assert_same(p, M, cost, dec)
+
+
 def test_workspace_too_small_is_rejected():
     import torch
     from paper_1911_13214_amd import rotor
