@@ -282,9 +282,11 @@ typedef struct {
 } rotor_kernel_stats;
 
 /* rotor_solve, plus a breakdown of the fill by kernel class: a HIP event pair
- * is recorded on `stream` around each run of consecutive launches of one
- * class (the runs' times summed per class), and the call waits for the
- * stream.  stats: HOST array of ROTOR_N_KERNEL_CLASSES entries, overwritten.
+ * is recorded around each run of consecutive launches of one class on one
+ * stream (`stream`, or the side stream of the blocked fill), the runs' times
+ * summed per class, and the call waits for both streams.  Runs on the two
+ * streams overlap, so the class times can add up to more than the fill.
+ * stats: HOST array of ROTOR_N_KERNEL_CLASSES entries, overwritten.
  * Summed over the classes, split_candidates is (L^3 - L)/6 (M+1) n_chains and
  * all_candidates L(L-1)/2 (M+1) n_chains.  Same return codes as rotor_solve. */
 ROTOR_API int32_t rotor_solve_timed(const int64_t *d_params, int32_t n_chains, int32_t L, int64_t M, int64_t *d_cost,
