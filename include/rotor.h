@@ -70,7 +70,8 @@
  * fill, one side stream and two events per device (created by the first
  * solve on the device, kept until the process ends), on which part of each
  * middle product runs beside the edges before it and which the solve joins
- * back into `stream` before it returns.  Solves hold a lock while they
+ * back into `stream` before it returns (if the side stream cannot be
+ * created, every launch goes to `stream`).  Solves hold a lock while they
  * enqueue; concurrent calls on distinct output buffers and workspaces are
  * independent.
  */

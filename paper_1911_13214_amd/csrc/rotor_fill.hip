@@ -2111,11 +2111,18 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
     // own rim follows them; only beside edges by rounds (the row edges of a
     // batch lose: 4.95 -> 5.06 ms for 256 chains of L = 64).  An observer
     // sees the side stream's launches on that stream.
-    const bool overlap = side_stream && schedule != ROTOR_SCHEDULE_BLOCKED_SERIAL && nb >= 4;
+    bool overlap = side_stream && schedule != ROTOR_SCHEDULE_BLOCKED_SERIAL && nb >= 4;
     SideStream *side = nullptr;
     std::unique_lock<std::mutex> side_lock;
-    if (overlap && (e = device_side_stream(stream, side, side_lock)) != hipSuccess)
-        return e;
+    if (overlap && device_side_stream(stream, side, side_lock) != hipSuccess) {
+        // no side stream on this device: everything on the caller's
+        // stream (the failed call's error is not this solve's)
+        (void)hipGetLastError();
+        overlap = false;
+        side = nullptr;
+        if (side_lock.owns_lock())
+            side_lock.unlock();
+    }
     bool inner_done = false;  // the inner range of delta ran beside the edges of delta - 1
     for (int delta = 1; delta < nb; ++delta) {
         const uint64_t pairs = pairs_of(delta);
