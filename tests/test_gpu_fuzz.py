@@ -1,7 +1,8 @@
 """GPU parity on seeded chains of varied shape and value range: many equal
 costs (ties between splits and between C_1 and C_2), zero sizes and
 overheads, sizes beyond the budget, heavy overheads, and costs scaled onto
-the 64-bit value path; batches of one to three chains; the four fill orders (rounds and rows with two streams, one stream, streamed diagonals).
+the 64-bit value path; batches of one to three chains; four fill orders
+(edges by rounds beside the side stream, by rows, one stream, streamed).
 Longer chains (8 to 13 blocks of 16 stages) at costs scaled by up to 2^18
 put their block-diagonals on every side of the value-path thresholds (2-byte
 copy of the diagonal blocks, packed middle keys, 4-byte or 64-bit values).
