@@ -20,9 +20,9 @@ def say(msg):
     print(msg, flush=True)
 
 
-# the blocked fill with its edges by anti-diagonal rounds and by rows (both
-# with the inner middle products beside the previous edges), the blocked fill
-# on one stream, and the streamed diagonals
+# the blocked fill with its edges by anti-diagonal rounds (the inner middle
+# products beside the previous edges, on the side stream) and by rows, the
+# blocked fill on one stream, and the streamed diagonals
 SCHEDULES = ["rounds", "rows", "serial", "diagonal"]
 EDGE_ORDERS = ["rounds", "rows", "serial"]
 _oracle_cache = {}
