@@ -69,7 +69,8 @@
  * of rotor_solve_noalloc, one device array per device; and, for the blocked
  * fill, one side stream and two events per device (created by the first
  * solve on the device, kept until the process ends), on which part of each
- * middle product runs beside the edges before it and which the solve joins
+ * middle product runs beside the edge rounds before it (edges by
+ * anti-diagonal rounds, not by rows) and which the solve joins
  * back into `stream` before it returns (if the side stream cannot be
  * created, every launch goes to `stream`).  Solves hold a lock while they
  * enqueue; concurrent calls on distinct output buffers and workspaces are
