@@ -1421,7 +1421,8 @@ __global__ __launch_bounds__(256) void middle_packed_kernel(const int64_t *__res
                 uint32_t key = acc[i][j];
                 if constexpr (RIM) {
                     // the inner part's key in the corner's slot
-                    const uint32_t inner = __builtin_nontemporal_load(&cw.shadow[row_of(L, k_lo, k_hi + 1) * pitch + m]);
+                    const uint32_t inner =
+                        __builtin_nontemporal_load(&cw.shadow[row_of(L, k_lo, k_hi + 1) * pitch + m]);
                     key = inner < key ? inner : key;
                 }
                 Narrow::Acc a;
@@ -2124,80 +2125,92 @@ hipError_t launch_fill(const Tables &tb, const Work &w, int schedule, hipStream_
             side_lock.unlock();
     }
     bool inner_done = false;  // the inner range of delta ran beside the edges of delta - 1
-    for (int delta = 1; delta < nb; ++delta) {
-        const uint64_t pairs = pairs_of(delta);
-        const int span = (delta - 1) * kT + 1;
-        const bool rows = schedule == ROTOR_SCHEDULE_BLOCKED_ROWS ||
-                          (schedule != ROTOR_SCHEDULE_BLOCKED_ROUNDS && row_edges((int64_t)(nb - delta) * tb.n_chains));
-        // the middle splits of every pair, and C_2 of the corner cell of
-        // every block when the middle products finish the corners
-        const int n_part = inner_done ? 1 : parts_of(delta);
-        const int finish = inner_done || n_part == 1 ? 1 : 0;
-        const uint64_t corners = finish ? (uint64_t)(nb - delta) : 0;
-        if (inner_done && (e = hipStreamWaitEvent(stream, side->done, 0)) != hipSuccess)
-            return e;
-        const int range = inner_done ? kMidRim : kMidAll;
-        if (n_part > 1 && (e = fill_partials(delta, stream)) != hipSuccess)
-            return e;
-        // the general kernel first: its workgroups, with their larger LDS
-        // ring, would otherwise wait for those of the next inner range even
-        // where they return at once
-        if ((e = middle_general(delta, range, n_part, stream)) != hipSuccess)
-            return e;
-        const bool next_inner = overlap && !rows && delta + 1 < nb && delta + 1 >= 3;
-        if (next_inner) {
-            // the inner splits of every pair of delta + 1: all but 2 kT
-            const int np = parts_of(delta + 1);
-            const uint64_t inner = pairs_of(delta + 1) * (uint64_t)(delta * kT + 1 - 2 * kT);
-            if ((e = hipEventRecord(side->ready, stream)) != hipSuccess ||
-                (e = hipStreamWaitEvent(side->stream, side->ready, 0)) != hipSuccess ||
-                (np > 1 && (e = fill_partials(delta + 1, side->stream)) != hipSuccess) ||
-                (e = middle_packed(delta + 1, kMidInner, np, side->stream, inner, 0)) != hipSuccess ||
-                (e = middle_general(delta + 1, kMidInner, np, side->stream)) != hipSuccess ||
-                (obs && (e = obs->end_stream(side->stream)) != hipSuccess) ||
-                (e = hipEventRecord(side->done, side->stream)) != hipSuccess)
+    auto blocked = [&]() -> hipError_t {
+        hipError_t e;
+        for (int delta = 1; delta < nb; ++delta) {
+            const uint64_t pairs = pairs_of(delta);
+            const int span = (delta - 1) * kT + 1;
+            const bool rows = schedule == ROTOR_SCHEDULE_BLOCKED_ROWS ||
+                              (schedule != ROTOR_SCHEDULE_BLOCKED_ROUNDS &&
+                               row_edges((int64_t)(nb - delta) * tb.n_chains));
+            // the middle splits of every pair, and C_2 of the corner cell of
+            // every block when the middle products finish the corners
+            const int n_part = inner_done ? 1 : parts_of(delta);
+            const int finish = inner_done || n_part == 1 ? 1 : 0;
+            const uint64_t corners = finish ? (uint64_t)(nb - delta) : 0;
+            if (inner_done && (e = hipStreamWaitEvent(stream, side->done, 0)) != hipSuccess)
                 return e;
-        }
-        // the middle splits of every pair (the rim's 2 kT after an inner range)
-        const uint64_t c1 = pairs * (uint64_t)(range == kMidRim ? 2 * kT : span);
-        if ((e = middle_packed(delta, range, n_part, stream, c1, corners)) != hipSuccess)
-            return e;
-        inner_done = next_inner;
-        if (rows) {
-            for (int a = 0; a < kT; ++a) {
-                uint64_t c1 = 0, cells = 0;
-                for (int I = 0; I + delta < nb; ++I) {
-                    const int nt = min(kT, L - (I + delta) * kT);
-                    for (int j = (a == 0 && finish) ? 1 : 0; j < nt; ++j) {
-                        c1 += (uint64_t)(a + j);
-                        ++cells;
-                    }
-                }
-                if ((e = before(kEdge)) != hipSuccess)
-                    return e;
-                launch_edge_row(a, nb - delta, stream, tb, delta, finish, w);
-                if ((e = launched(kEdge, c1, cells, cells)) != hipSuccess)
+            const int range = inner_done ? kMidRim : kMidAll;
+            if (n_part > 1 && (e = fill_partials(delta, stream)) != hipSuccess)
+                return e;
+            // the general kernel first: its workgroups, with their larger LDS
+            // ring, would otherwise wait for those of the next inner range even
+            // where they return at once
+            if ((e = middle_general(delta, range, n_part, stream)) != hipSuccess)
+                return e;
+            const bool next_inner = overlap && !rows && delta + 1 < nb && delta + 1 >= 3;
+            if (next_inner) {
+                // the inner splits of every pair of delta + 1: all but 2 kT
+                const int np = parts_of(delta + 1);
+                const uint64_t inner = pairs_of(delta + 1) * (uint64_t)(delta * kT + 1 - 2 * kT);
+                if ((e = hipEventRecord(side->ready, stream)) != hipSuccess ||
+                    (e = hipStreamWaitEvent(side->stream, side->ready, 0)) != hipSuccess ||
+                    (np > 1 && (e = fill_partials(delta + 1, side->stream)) != hipSuccess) ||
+                    (e = middle_packed(delta + 1, kMidInner, np, side->stream, inner, 0)) != hipSuccess ||
+                    (e = middle_general(delta + 1, kMidInner, np, side->stream)) != hipSuccess ||
+                    (obs && (e = obs->end_stream(side->stream)) != hipSuccess) ||
+                    (e = hipEventRecord(side->done, side->stream)) != hipSuccess)
                     return e;
             }
-            continue;
-        }
-        for (int q = finish; q <= 2 * kT - 2; ++q) {
-            const int a_min = q - (kT - 1) > 0 ? q - (kT - 1) : 0;
-            const int a_max = q < kT - 1 ? q : kT - 1;
-            const int n_q = a_max - a_min + 1;
-            uint64_t cells = 0;
-            for (int I = 0; I + delta < nb; ++I)
-                for (int a = a_min; a <= a_max; ++a)
-                    cells += ((I + delta) * kT + 1 + (q - a) <= L) ? 1 : 0;
-            if ((e = before(kEdge)) != hipSuccess)
+            // the middle splits of every pair (the rim's 2 kT after an inner range)
+            const uint64_t c1 = pairs * (uint64_t)(range == kMidRim ? 2 * kT : span);
+            if ((e = middle_packed(delta, range, n_part, stream, c1, corners)) != hipSuccess)
                 return e;
-            edge_kernel<<<dim3(mb_edge, (nb - delta) * n_q, tb.n_chains), kEdgeThreads, 0, stream>>>(
-                tb.params, L, tb.M, tb.pitch, tb.rows, delta, q, a_min, n_q, tb.cost, tb.dec, w);
-            if ((e = launched(kEdge, cells * (uint64_t)q, cells, cells)) != hipSuccess)
-                return e;
+            inner_done = next_inner;
+            if (rows) {
+                for (int a = 0; a < kT; ++a) {
+                    uint64_t c1 = 0, cells = 0;
+                    for (int I = 0; I + delta < nb; ++I) {
+                        const int nt = min(kT, L - (I + delta) * kT);
+                        for (int j = (a == 0 && finish) ? 1 : 0; j < nt; ++j) {
+                            c1 += (uint64_t)(a + j);
+                            ++cells;
+                        }
+                    }
+                    if ((e = before(kEdge)) != hipSuccess)
+                        return e;
+                    launch_edge_row(a, nb - delta, stream, tb, delta, finish, w);
+                    if ((e = launched(kEdge, c1, cells, cells)) != hipSuccess)
+                        return e;
+                }
+                continue;
+            }
+            for (int q = finish; q <= 2 * kT - 2; ++q) {
+                const int a_min = q - (kT - 1) > 0 ? q - (kT - 1) : 0;
+                const int a_max = q < kT - 1 ? q : kT - 1;
+                const int n_q = a_max - a_min + 1;
+                uint64_t cells = 0;
+                for (int I = 0; I + delta < nb; ++I)
+                    for (int a = a_min; a <= a_max; ++a)
+                        cells += ((I + delta) * kT + 1 + (q - a) <= L) ? 1 : 0;
+                if ((e = before(kEdge)) != hipSuccess)
+                    return e;
+                edge_kernel<<<dim3(mb_edge, (nb - delta) * n_q, tb.n_chains), kEdgeThreads, 0, stream>>>(
+                    tb.params, L, tb.M, tb.pitch, tb.rows, delta, q, a_min, n_q, tb.cost, tb.dec, w);
+                if ((e = launched(kEdge, cells * (uint64_t)q, cells, cells)) != hipSuccess)
+                    return e;
+            }
         }
+        return hipSuccess;
+    };
+    e = blocked();
+    if (e != hipSuccess && side) {
+        // a failed launch leaves no side-stream work behind the caller's
+        // stream: it waits for all of it
+        (void)hipEventRecord(side->done, side->stream);
+        (void)hipStreamWaitEvent(stream, side->done, 0);
     }
-    return hipSuccess;
+    return e;
 }
 
 }  // namespace rotor
